@@ -1,0 +1,210 @@
+/*
+ * catekv.h -- C ABI of the CateKV hybrid-KV decode path on MI355X (gfx950).
+ *
+ * CateKV (ICML 2025) splits the attention heads of a long-context model into
+ * "consistent" heads, which attend to a fixed small set of critical tokens
+ * chosen at prefill time, and "adaptive" heads, which keep (most of) their
+ * KV cache.  This library implements the data-parallel path of that method:
+ *
+ *   catekv_score_heads      CV head score per KV head      (Section 3.2, Eq. 1-4)
+ *   catekv_classify_heads   consistent/adaptive head types (Eq. 5; static identification)
+ *   catekv_select_critical  critical chunks per head       (Algorithm 1, pre-filling stage)
+ *   catekv_compact_kv       dense compact K/V per head     (Algorithm 1, Cache(K, V, i_k, L_obs))
+ *   catekv_decode_plan      split-KV work list for a batch (host side, once per request)
+ *   catekv_decode_attn      GQA decode over mixed per-head cache lengths
+ *                                                         (Algorithm 1, decoding stage)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Tensor arguments are caller-owned DEVICE pointers unless the name ends in
+ *   _host.  Layouts are row-major with the head dimension d innermost and
+ *   contiguous; every K/V row is d elements.
+ * - dtype selects the storage type of K, V and Q: CATEKV_F32 (float) or
+ *   CATEKV_BF16 (bfloat16 bit patterns).  Arithmetic is fp32 (fp64 for the
+ *   final CV statistics); every output is fp32 or an integer.
+ * - Supported shapes: d == 128, 1 <= Hkv, Hq % Hkv == 0, Hq / Hkv in
+ *   {1, 2, 4, 8}.
+ * - Device work is enqueued asynchronously on `stream` (a hipStream_t; NULL
+ *   means the default stream).  Only catekv_decode_plan blocks the host.
+ * - The library never allocates device memory: calls that need scratch take
+ *   a caller-owned workspace sized by the matching *_workspace() function.
+ *   Workspaces must be 256-byte aligned.  Two calls that overlap in time must
+ *   not share a workspace.
+ * - Every call validates all arguments BEFORE enqueuing any work.  A status
+ *   other than CATEKV_OK means nothing was enqueued and no output was
+ *   touched; catekv_last_error() then returns a message (per host thread).
+ *   Launch failures report CATEKV_ERR_HIP.  Faults inside a kernel surface
+ *   as HIP errors at the caller's next synchronisation.
+ */
+#ifndef CATEKV_H
+#define CATEKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  CATEKV_OK = 0,
+  CATEKV_ERR_INVALID_ARG = -1,  /* null pointer, bad size or inconsistent arguments */
+  CATEKV_ERR_UNSUPPORTED = -2,  /* valid request outside the supported shapes/dtypes */
+  CATEKV_ERR_WORKSPACE = -3,    /* workspace missing, misaligned or too small */
+  CATEKV_ERR_HIP = -4           /* a HIP runtime call failed */
+} catekv_status;
+
+typedef enum { CATEKV_F32 = 0, CATEKV_BF16 = 1 } catekv_dtype;
+
+/* K and V base pointers of one (sequence, KV head) cache view.  Row t of the
+ * view is at k + t * d elements (same for v). */
+typedef struct catekv_kv_ptrs {
+  const void* k;
+  const void* v;
+} catekv_kv_ptrs;
+
+/* Host-side descriptor of a decode work list, filled by catekv_decode_plan and
+ * passed back to catekv_decode_attn.  Treat as opaque. */
+typedef struct catekv_decode_plan_t {
+  uint64_t magic;
+  int32_t batch, hq, hkv, split_tokens;
+  int32_t n_items, n_slots, reserved0, reserved1;
+  uint64_t items_off, bh_off, counters_off, partials_off, ws_bytes;
+  int64_t max_len_total;
+} catekv_decode_plan_t;
+
+/* ------------------------------------------------------------------------ */
+/* CV head scoring -- Section 3.2, Eq. 1-4.                                  */
+/* ------------------------------------------------------------------------ */
+
+/* Workspace bytes for catekv_score_heads with these sizes. */
+size_t catekv_score_heads_workspace(int hq, int hkv, int lq, int64_t n,
+                                    int64_t l_init, int64_t l_rec);
+
+/* For every KV head h computes the coefficient-of-variation score of its
+ * observation matrix:
+ *   A   = mean over the G query heads g of group h of
+ *         softmax_j( q_rows[g][i] . k[h][l_init + j] / sqrt(d) ),
+ *         j over the key range [l_init, n - l_rec), restricted to keys at
+ *         positions <= q_pos0 + i when `causal` is non-zero      (Eq. 1)
+ *   Phi = alpha * (linearly interpolated k_pct-quantile of all entries of A)
+ *   B   = (A >= Phi),  C_j = sum_i B[i][j]                        (Eq. 2-3)
+ *   cv  = population-std(C) / mean(C), and 0 when mean(C) == 0      (Eq. 4)
+ *
+ * q_rows  [hq][lq][d]  observation rows; row i sits at absolute position
+ *                      q_pos0 + i (prefill window: q_pos0 = n - lq;
+ *                      decode-time calibration rows: q_pos0 >= n).
+ * k       [hkv][n][d]  keys of one sequence.
+ * cv_out  [hkv] fp32, device.
+ * Errors: INVALID_ARG if l_init < 0, l_rec < 0, l_init + l_rec >= n, lq < 1,
+ * k_pct outside [0, 1], alpha <= 0, or (causal and q_pos0 < l_init, which
+ * would leave a row with no visible key); WORKSPACE if ws is too small. */
+int catekv_score_heads(int dtype, const void* q_rows, int64_t q_pos0, const void* k,
+                       int hq, int hkv, int lq, int64_t n, int d,
+                       int64_t l_init, int64_t l_rec, double k_pct, double alpha, int causal,
+                       float* cv_out, void* ws, size_t ws_bytes, void* stream);
+
+/* Head classification -- Eq. 5 and the reference-based static
+ * identification of Section 3.2.  Host only, synchronous.
+ * cv_host [S][H]: scores of H heads (all layers of a model, flattened) in S
+ * reference samples.  In each sample a head is consistent iff its score is
+ * strictly above the linearly interpolated r-quantile of that sample's
+ * scores.  The result marks the H - 1 - floor((H - 1) r) heads most often
+ * consistent (ties: higher mean score, then lower index), which is the Eq. 5
+ * count for distinct scores.  is_consistent_host [H] receives 1/0.
+ * Errors: INVALID_ARG for null pointers, S < 1, H < 1 or r outside [0, 1). */
+int catekv_classify_heads(const float* cv_host, int S, int H, double r,
+                          uint8_t* is_consistent_host);
+
+/* ------------------------------------------------------------------------ */
+/* Critical-token selection -- Algorithm 1, pre-filling stage.               */
+/* ------------------------------------------------------------------------ */
+
+/* Workspace bytes for catekv_select_critical. */
+size_t catekv_select_workspace(int hq, int hkv, int l_obs, int64_t n, int cs, int n_sel);
+
+/* For each KV head h = sel_heads_host[s] (s < n_sel):
+ *   A       = mean over the G query heads of group h of
+ *             softmax_j( q_obs[g][i] . k[h][j] / sqrt(d) ),  j < n' = n - l_obs
+ *   C_j     = sum_i A[i][j]
+ *   S_c     = max of C_j over chunk c = [c cs, min((c + 1) cs, n'))
+ *   idx_out[s][0 .. b_eff) = the b_eff = min(b, ceil(n'/cs)) chunks with the
+ *             largest S_c (ties to the lower chunk index), ascending;
+ *             entries b_eff .. b-1 are set to -1.
+ * q_obs  [hq][l_obs][d]  the last l_obs prefill query rows.
+ * k      [hkv][n][d].
+ * sel_heads_host [n_sel] distinct KV head ids (host array).
+ * idx_out [n_sel][b] int32, device.
+ * Errors: INVALID_ARG if l_obs < 1, l_obs >= n, cs < 1, b < 1, n_sel < 1 or a
+ * head id is out of range or repeated; WORKSPACE if ws is too small. */
+int catekv_select_critical(int dtype, const void* q_obs, const void* k,
+                           int hq, int hkv, int l_obs, int64_t n, int d, int cs,
+                           const int32_t* sel_heads_host, int n_sel, int b,
+                           int32_t* idx_out, void* ws, size_t ws_bytes, void* stream);
+
+/* Cache(K, V, i_k, L_obs) of Algorithm 1: for each selected head s, writes the
+ * rows of the chunks idx[s][*] (ascending; entries < 0 ignored; the last chunk
+ * may be partial) followed by the last l_obs rows k[h][n - l_obs .. n) into
+ * k_c[s] (and likewise V into v_c[s]) as one dense run of rows, and stores
+ * the run's length in lens_out[sel_heads_host[s]].
+ * k, v      [hkv][n][d]
+ * idx       [n_sel][b] int32, device, as written by catekv_select_critical
+ * k_c, v_c  [n_sel][b * cs + l_obs][d], device (capacity per head)
+ * lens_out  int64 device array indexed by KV head id (e.g. one sequence's
+ *           row of a [batch][hkv] length table); other entries untouched.
+ * Errors: INVALID_ARG for null pointers or the selection errors above.  Index
+ * values must come from catekv_select_critical with the same n, l_obs, cs. */
+int catekv_compact_kv(int dtype, const void* k, const void* v, int hkv, int64_t n, int d,
+                      int cs, int l_obs, const int32_t* sel_heads_host, int n_sel,
+                      const int32_t* idx, int b, void* k_c, void* v_c, int64_t* lens_out,
+                      void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Hybrid decode attention -- Algorithm 1, decoding stage.                   */
+/* ------------------------------------------------------------------------ */
+
+/* Workspace bytes for a decode plan over max_len_host [batch][hkv].
+ * split_tokens <= 0 picks the default split. */
+size_t catekv_decode_workspace(const int64_t* max_len_host, int batch, int hq, int hkv,
+                               int split_tokens);
+
+/* Builds the split-KV work list for upper-bound cache lengths
+ * max_len_host [batch][hkv] (full length for adaptive heads, b cs + l_obs for
+ * consistent heads), writes it into ws and fills *plan.  Blocks until the
+ * upload has completed, so max_len_host may be reused on return.  The plan and
+ * ws serve every later catekv_decode_attn call with the same shapes.
+ * Errors: INVALID_ARG for null pointers, batch < 1, negative lengths or a
+ * length above 2^31 - 1; WORKSPACE if ws is too small; HIP on upload failure. */
+int catekv_decode_plan(const int64_t* max_len_host, int batch, int hq, int hkv,
+                       int split_tokens, catekv_decode_plan_t* plan,
+                       void* ws, size_t ws_bytes, void* stream);
+
+/* One decode step: for every sequence b and query head g (KV head
+ * h = g / (hq / hkv)), with L = min(lens[b][h], planned max_len[b][h]):
+ *   s_t = scale * q[b][g] . K_{b,h}[t],  t < L
+ *   out[b][g] = sum_t softmax(s)_t V_{b,h}[t],  lse[b][g] = log sum_t exp(s_t)
+ * and out = 0, lse = -inf when L == 0.
+ * q     [batch][hq][d] (dtype)
+ * kv    [batch][hkv] catekv_kv_ptrs, device array (views may point into a
+ *       full cache or into compact caches; rows beyond L are never used)
+ * lens  [batch][hkv] int64, device (read on the device at run time)
+ * out   [batch][hq][d] fp32; lse [batch][hq] fp32 or NULL.
+ * ws must be the workspace given to catekv_decode_plan for `plan`.
+ * Errors: INVALID_ARG if shapes disagree with the plan or pointers are null;
+ * WORKSPACE if ws is too small. */
+int catekv_decode_attn(int dtype, const catekv_decode_plan_t* plan, const void* q,
+                       const catekv_kv_ptrs* kv, const int64_t* lens,
+                       int batch, int hq, int hkv, int d, float scale,
+                       float* out, float* lse, void* ws, size_t ws_bytes, void* stream);
+
+/* Message describing the last failure on the calling host thread. */
+const char* catekv_last_error(void);
+
+/* Library version string. */
+const char* catekv_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CATEKV_H */

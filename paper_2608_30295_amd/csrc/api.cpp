@@ -1,0 +1,411 @@
+// Host side of the CateKV C ABI: argument validation, workspace layout, the
+// decode work list and head classification.  Every argument is checked
+// before anything is enqueued; kernel launches live in the .hip files.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <numeric>
+#include <string>
+#include <vector>
+
+#include "../../include/catekv.h"
+#include "internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+constexpr uint64_t kPlanMagic = 0x43617465504c414eull;   // "CatePLAN"
+constexpr int kMaxHeads = 128;
+constexpr int kMaxRows = 512;                           // G * L rows per KV head in the score passes
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int ok() {
+  g_err.clear();
+  return CATEKV_OK;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(CATEKV_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool valid_dtype(int dt) { return dt == CATEKV_F32 || dt == CATEKV_BF16; }
+
+int check_heads(int hq, int hkv, int d) {
+  if (d != catekv::kD) return fail(CATEKV_ERR_UNSUPPORTED, "head dimension %d unsupported (only 128)", d);
+  if (hkv < 1 || hq < 1) return fail(CATEKV_ERR_INVALID_ARG, "hq=%d hkv=%d must be positive", hq, hkv);
+  if (hkv > kMaxHeads) return fail(CATEKV_ERR_UNSUPPORTED, "hkv=%d above %d", hkv, kMaxHeads);
+  if (hq % hkv) return fail(CATEKV_ERR_INVALID_ARG, "hq=%d is not a multiple of hkv=%d", hq, hkv);
+  const int G = hq / hkv;
+  if (G != 1 && G != 2 && G != 4 && G != 8)
+    return fail(CATEKV_ERR_UNSUPPORTED, "group size hq/hkv=%d unsupported (1, 2, 4 or 8)", G);
+  return CATEKV_OK;
+}
+
+int check_ws(const void* ws, size_t ws_bytes, size_t need) {
+  if (need == 0) return CATEKV_OK;
+  if (!ws) return fail(CATEKV_ERR_WORKSPACE, "workspace pointer is null (need %zu bytes)", need);
+  if (reinterpret_cast<uintptr_t>(ws) % 256) return fail(CATEKV_ERR_WORKSPACE, "workspace not 256-byte aligned");
+  if (ws_bytes < need) return fail(CATEKV_ERR_WORKSPACE, "workspace %zu bytes, need %zu", ws_bytes, need);
+  return CATEKV_OK;
+}
+
+// Linearly interpolated quantile of x (copied, sorted ascending).
+double quantile_linear(std::vector<double> x, double p) {
+  std::sort(x.begin(), x.end());
+  const double h = (double)(x.size() - 1) * p;
+  const size_t lo = (size_t)std::floor(h);
+  const size_t hi = std::min(lo + 1, x.size() - 1);
+  return x[lo] + (h - (double)lo) * (x[hi] - x[lo]);
+}
+
+constexpr int kDefaultItems = 1024;   // aim for ~4 work items per compute unit
+constexpr int kSplitQuantum = 64;     // tokens one workgroup covers per loop trip
+
+int default_split(const int64_t* max_len, int n_views) {
+  int64_t tot = 0;
+  for (int i = 0; i < n_views; ++i) tot += max_len[i];
+  int64_t s = (tot + kDefaultItems - 1) / kDefaultItems;
+  s = ((s + kSplitQuantum - 1) / kSplitQuantum) * kSplitQuantum;
+  return (int)std::max<int64_t>(256, std::min<int64_t>(s, 1 << 20));
+}
+
+struct PlanShape {
+  int n_items = 0, n_slots = 0, n_gslots = 0, n_gcounters = 0;
+  size_t items_off = 0, views_off = 0, counters_off = 0, slots_off = 0, gslots_off = 0, total = 0;
+};
+
+size_t a256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+PlanShape plan_shape(const int64_t* max_len, int n_views, int G, int split) {
+  PlanShape P;
+  for (int v = 0; v < n_views; ++v) {
+    const int64_t L = max_len[v];
+    const int parts = L <= 0 ? 1 : (int)((L + split - 1) / split);
+    const int groups = (parts + catekv::kMergeGroup - 1) / catekv::kMergeGroup;
+    P.n_items += parts;
+    P.n_slots += parts;
+    if (groups > 1) {
+      P.n_gslots += groups;
+      P.n_gcounters += groups;
+    }
+  }
+  const size_t sf = catekv::decode_slot_floats(G) * sizeof(float);
+  size_t o = 0;
+  P.items_off = o; o += a256((size_t)P.n_items * sizeof(catekv::DecodeItem));
+  P.views_off = o; o += a256((size_t)n_views * sizeof(catekv::ViewInfo));
+  P.counters_off = o; o += a256((size_t)(n_views + P.n_gcounters) * sizeof(int32_t));
+  P.slots_off = o; o += a256((size_t)P.n_slots * sf);
+  P.gslots_off = o; o += a256((size_t)std::max(P.n_gslots, 1) * sf);
+  P.total = o;
+  return P;
+}
+
+int check_lengths(const int64_t* max_len, int n) {
+  for (int i = 0; i < n; ++i) {
+    if (max_len[i] < 0) return fail(CATEKV_ERR_INVALID_ARG, "max_len[%d] = %lld is negative", i, (long long)max_len[i]);
+    if (max_len[i] > INT32_MAX)
+      return fail(CATEKV_ERR_UNSUPPORTED, "max_len[%d] = %lld above 2^31 - 1", i, (long long)max_len[i]);
+  }
+  return CATEKV_OK;
+}
+
+int check_head_list(int hkv, const int32_t* heads, int n_sel) {
+  if (n_sel < 1 || n_sel > hkv) return fail(CATEKV_ERR_INVALID_ARG, "n_sel=%d outside [1, hkv=%d]", n_sel, hkv);
+  if (!heads) return fail(CATEKV_ERR_INVALID_ARG, "sel_heads_host is null");
+  std::vector<char> seen(hkv, 0);
+  for (int i = 0; i < n_sel; ++i) {
+    if (heads[i] < 0 || heads[i] >= hkv) return fail(CATEKV_ERR_INVALID_ARG, "sel_heads_host[%d]=%d out of range", i, heads[i]);
+    if (seen[heads[i]]) return fail(CATEKV_ERR_INVALID_ARG, "KV head %d selected twice", heads[i]);
+    seen[heads[i]] = 1;
+  }
+  return CATEKV_OK;
+}
+
+// Checks shared by selection and compaction (window, chunking, budget, heads).
+int check_window(int hkv, int l_obs, int64_t n, int cs, const int32_t* heads, int n_sel, int b) {
+  if (l_obs < 1) return fail(CATEKV_ERR_INVALID_ARG, "l_obs=%d must be >= 1", l_obs);
+  if ((int64_t)l_obs >= n) return fail(CATEKV_ERR_INVALID_ARG, "l_obs=%d must be below n=%lld", l_obs, (long long)n);
+  if (n > INT32_MAX) return fail(CATEKV_ERR_UNSUPPORTED, "n=%lld above 2^31 - 1", (long long)n);
+  if (cs < 1) return fail(CATEKV_ERR_INVALID_ARG, "chunk size %d must be >= 1", cs);
+  if (b < 1) return fail(CATEKV_ERR_INVALID_ARG, "chunk budget %d must be >= 1", b);
+  if ((int64_t)b * cs + l_obs > INT32_MAX) return fail(CATEKV_ERR_UNSUPPORTED, "compact capacity above 2^31 - 1");
+  return check_head_list(hkv, heads, n_sel);
+}
+
+int check_selection(int hq, int hkv, int l_obs, int64_t n, int d, int cs, const int32_t* heads,
+                    int n_sel, int b) {
+  int rc = check_heads(hq, hkv, d);
+  if (rc) return rc;
+  rc = check_window(hkv, l_obs, n, cs, heads, n_sel, b);
+  if (rc) return rc;
+  if ((hq / hkv) * l_obs > kMaxRows)
+    return fail(CATEKV_ERR_UNSUPPORTED, "G * l_obs = %d rows above %d", (hq / hkv) * l_obs, kMaxRows);
+  return CATEKV_OK;
+}
+
+catekv::SelectGeom select_geom(int hq, int hkv, int l_obs, int64_t n, int cs, const int32_t* heads,
+                               int n_sel, int b) {
+  catekv::SelectGeom g{};
+  g.hq = hq; g.hkv = hkv; g.G = hq / hkv; g.l_obs = l_obs; g.cs = cs; g.n_sel = n_sel; g.b = b;
+  g.n = n;
+  g.n_keys = n - l_obs;
+  g.n_chunks = (g.n_keys + cs - 1) / cs;
+  g.n_colblk = (int)catekv::score_colblocks(g.n_keys);
+  for (int i = 0; i < n_sel && heads; ++i) g.heads[i] = heads[i];
+  return g;
+}
+
+catekv::ScoreGeom score_geom(int hq, int hkv, int lq, int64_t n, int64_t l_init, int64_t l_rec) {
+  catekv::ScoreGeom g{};
+  g.hq = hq; g.hkv = hkv; g.G = hkv > 0 ? hq / hkv : 1; g.lq = lq; g.n = n;
+  g.l_init = l_init; g.l_rec = l_rec;
+  g.n_keys = n - l_init - l_rec;
+  g.n_colblk = (int)catekv::score_colblocks(g.n_keys > 0 ? g.n_keys : 1);
+  return g;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* catekv_last_error(void) { return g_err.c_str(); }
+
+const char* catekv_version(void) { return "catekv-mi355x 0.1 (gfx950)"; }
+
+size_t catekv_score_heads_workspace(int hq, int hkv, int lq, int64_t n, int64_t l_init, int64_t l_rec) {
+  if (hkv < 1 || hq < 1 || lq < 1 || n - l_init - l_rec < 1) return 0;
+  return catekv::score_workspace_bytes(score_geom(hq, hkv, lq, n, l_init, l_rec));
+}
+
+int catekv_score_heads(int dtype, const void* q_rows, int64_t q_pos0, const void* k, int hq, int hkv,
+                       int lq, int64_t n, int d, int64_t l_init, int64_t l_rec, double k_pct,
+                       double alpha, int causal, float* cv_out, void* ws, size_t ws_bytes,
+                       void* stream) {
+  if (!valid_dtype(dtype)) return fail(CATEKV_ERR_UNSUPPORTED, "dtype %d unsupported", dtype);
+  if (!q_rows || !k || !cv_out) return fail(CATEKV_ERR_INVALID_ARG, "null tensor pointer");
+  int rc = check_heads(hq, hkv, d);
+  if (rc) return rc;
+  if (lq < 1) return fail(CATEKV_ERR_INVALID_ARG, "lq=%d must be >= 1", lq);
+  if (l_init < 0 || l_rec < 0) return fail(CATEKV_ERR_INVALID_ARG, "l_init and l_rec must be >= 0");
+  if (l_init + l_rec >= n) return fail(CATEKV_ERR_INVALID_ARG, "l_init + l_rec = %lld leaves no key of n=%lld",
+                                       (long long)(l_init + l_rec), (long long)n);
+  if (n > INT32_MAX) return fail(CATEKV_ERR_UNSUPPORTED, "n=%lld above 2^31 - 1", (long long)n);
+  if (!(k_pct >= 0.0 && k_pct <= 1.0)) return fail(CATEKV_ERR_INVALID_ARG, "k_pct=%g outside [0, 1]", k_pct);
+  if (!(alpha > 0.0) || !std::isfinite(alpha)) return fail(CATEKV_ERR_INVALID_ARG, "alpha=%g must be > 0", alpha);
+  if (causal && q_pos0 < l_init)
+    return fail(CATEKV_ERR_INVALID_ARG, "q_pos0=%lld < l_init=%lld leaves a row with no visible key",
+                (long long)q_pos0, (long long)l_init);
+  if ((hq / hkv) * lq > kMaxRows)
+    return fail(CATEKV_ERR_UNSUPPORTED, "G * lq = %d rows above %d", (hq / hkv) * lq, kMaxRows);
+  if ((int64_t)lq * (n - l_init - l_rec) > (int64_t)INT32_MAX * 2)
+    return fail(CATEKV_ERR_UNSUPPORTED, "observation matrix too large");
+  catekv::ScoreGeom g = score_geom(hq, hkv, lq, n, l_init, l_rec);
+  g.q_pos0 = q_pos0;
+  g.causal = causal ? 1 : 0;
+  g.k_pct = k_pct;
+  g.alpha = alpha;
+  rc = check_ws(ws, ws_bytes, catekv::score_workspace_bytes(g));
+  if (rc) return rc;
+  hipError_t e = catekv::launch_score(dtype, g, q_rows, k, cv_out, ws, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "score_heads launch");
+  return ok();
+}
+
+int catekv_classify_heads(const float* cv_host, int S, int H, double r, uint8_t* is_consistent_host) {
+  if (!cv_host || !is_consistent_host) return fail(CATEKV_ERR_INVALID_ARG, "null pointer");
+  if (S < 1 || H < 1) return fail(CATEKV_ERR_INVALID_ARG, "S=%d H=%d must be >= 1", S, H);
+  if (!(r >= 0.0 && r < 1.0)) return fail(CATEKV_ERR_INVALID_ARG, "r=%g outside [0, 1)", r);
+  std::vector<double> freq(H, 0.0), mean(H, 0.0);
+  for (int s = 0; s < S; ++s) {
+    std::vector<double> row(cv_host + (size_t)s * H, cv_host + (size_t)(s + 1) * H);
+    const double gamma = quantile_linear(row, r);
+    for (int h = 0; h < H; ++h) {
+      if (row[h] > gamma) freq[h] += 1.0;
+      mean[h] += row[h];
+    }
+  }
+  std::vector<int> order(H);
+  std::iota(order.begin(), order.end(), 0);
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) {
+    if (freq[a] != freq[b]) return freq[a] > freq[b];
+    if (mean[a] != mean[b]) return mean[a] > mean[b];
+    return a < b;
+  });
+  const int n_cons = H - 1 - (int)std::floor((double)(H - 1) * r);
+  for (int h = 0; h < H; ++h) is_consistent_host[h] = 0;
+  for (int i = 0; i < n_cons; ++i) is_consistent_host[order[i]] = 1;
+  return ok();
+}
+
+size_t catekv_select_workspace(int hq, int hkv, int l_obs, int64_t n, int cs, int n_sel) {
+  if (hkv < 1 || hq < 1 || l_obs < 1 || (int64_t)l_obs >= n || cs < 1 || n_sel < 1) return 0;
+  return catekv::select_workspace_bytes(select_geom(hq, hkv, l_obs, n, cs, nullptr, n_sel, 1));
+}
+
+int catekv_select_critical(int dtype, const void* q_obs, const void* k, int hq, int hkv, int l_obs,
+                           int64_t n, int d, int cs, const int32_t* sel_heads_host, int n_sel, int b,
+                           int32_t* idx_out, void* ws, size_t ws_bytes, void* stream) {
+  if (!valid_dtype(dtype)) return fail(CATEKV_ERR_UNSUPPORTED, "dtype %d unsupported", dtype);
+  if (!q_obs || !k || !idx_out) return fail(CATEKV_ERR_INVALID_ARG, "null tensor pointer");
+  int rc = check_selection(hq, hkv, l_obs, n, d, cs, sel_heads_host, n_sel, b);
+  if (rc) return rc;
+  const catekv::SelectGeom g = select_geom(hq, hkv, l_obs, n, cs, sel_heads_host, n_sel, b);
+  rc = check_ws(ws, ws_bytes, catekv::select_workspace_bytes(g));
+  if (rc) return rc;
+  hipError_t e = catekv::launch_select(dtype, g, q_obs, k, idx_out, ws, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "select_critical launch");
+  return ok();
+}
+
+int catekv_compact_kv(int dtype, const void* k, const void* v, int hkv, int64_t n, int d, int cs,
+                      int l_obs, const int32_t* sel_heads_host, int n_sel, const int32_t* idx, int b,
+                      void* k_c, void* v_c, int64_t* lens_out, void* stream) {
+  if (!valid_dtype(dtype)) return fail(CATEKV_ERR_UNSUPPORTED, "dtype %d unsupported", dtype);
+  if (!k || !v || !idx || !k_c || !v_c || !lens_out) return fail(CATEKV_ERR_INVALID_ARG, "null tensor pointer");
+  int rc = check_heads(hkv, hkv, d);
+  if (rc) return rc;
+  rc = check_window(hkv, l_obs, n, cs, sel_heads_host, n_sel, b);
+  if (rc) return rc;
+  hipError_t e = catekv::launch_compact(dtype, k, v, hkv, n, cs, l_obs, sel_heads_host, n_sel, idx, b, k_c,
+                                        v_c, lens_out, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "compact_kv launch");
+  return ok();
+}
+
+size_t catekv_decode_workspace(const int64_t* max_len_host, int batch, int hq, int hkv, int split_tokens) {
+  if (!max_len_host || batch < 1 || hkv < 1 || hq < 1 || hq % hkv) return 0;
+  const int nv = batch * hkv;
+  for (int i = 0; i < nv; ++i)
+    if (max_len_host[i] < 0 || max_len_host[i] > INT32_MAX) return 0;
+  const int split = split_tokens > 0 ? split_tokens : default_split(max_len_host, nv);
+  return plan_shape(max_len_host, nv, hq / hkv, split).total;
+}
+
+int catekv_decode_plan(const int64_t* max_len_host, int batch, int hq, int hkv, int split_tokens,
+                       catekv_decode_plan_t* plan, void* ws, size_t ws_bytes, void* stream) {
+  if (!max_len_host || !plan) return fail(CATEKV_ERR_INVALID_ARG, "null pointer");
+  if (batch < 1) return fail(CATEKV_ERR_INVALID_ARG, "batch=%d must be >= 1", batch);
+  int rc = check_heads(hq, hkv, catekv::kD);
+  if (rc) return rc;
+  const int nv = batch * hkv;
+  rc = check_lengths(max_len_host, nv);
+  if (rc) return rc;
+  const int split = split_tokens > 0 ? split_tokens : default_split(max_len_host, nv);
+  const int G = hq / hkv;
+  const PlanShape P = plan_shape(max_len_host, nv, G, split);
+  rc = check_ws(ws, ws_bytes, P.total);
+  if (rc) return rc;
+
+  std::vector<catekv::DecodeItem> items;
+  items.reserve(P.n_items);
+  std::vector<catekv::ViewInfo> views(nv);
+  int slot = 0, gslot = 0, gctr = 0;
+  int64_t total = 0;
+  for (int v = 0; v < nv; ++v) {
+    const int64_t L = max_len_host[v];
+    total += L;
+    const int parts = L <= 0 ? 1 : (int)((L + split - 1) / split);
+    const int groups = (parts + catekv::kMergeGroup - 1) / catekv::kMergeGroup;
+    catekv::ViewInfo& vi = views[v];
+    std::memset(&vi, 0, sizeof vi);
+    vi.first_slot = slot;
+    vi.n_parts = parts;
+    vi.n_groups = groups;
+    vi.first_gslot = groups > 1 ? gslot : -1;
+    vi.gcounter = groups > 1 ? gctr : -1;
+    for (int p = 0; p < parts; ++p) {
+      const int64_t t0 = (int64_t)p * split;
+      const int64_t t1 = std::min<int64_t>(L, t0 + split);
+      items.push_back({v, p, (int32_t)t0, (int32_t)std::max<int64_t>(t0, t1)});
+    }
+    slot += parts;
+    if (groups > 1) {
+      gslot += groups;
+      gctr += groups;
+    }
+  }
+  // largest items first so that short consistent-head items fill the tail
+  std::stable_sort(items.begin(), items.end(), [](const catekv::DecodeItem& a, const catekv::DecodeItem& b) {
+    return (a.t1 - a.t0) > (b.t1 - b.t0);
+  });
+
+  std::vector<unsigned char> host(P.slots_off, 0);
+  std::memcpy(host.data() + P.items_off, items.data(), items.size() * sizeof(catekv::DecodeItem));
+  std::memcpy(host.data() + P.views_off, views.data(), views.size() * sizeof(catekv::ViewInfo));
+  // counters stay zero
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = hipMemcpyAsync(ws, host.data(), host.size(), hipMemcpyHostToDevice, s);
+  if (e != hipSuccess) return hip_fail(e, "decode_plan upload");
+  e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "decode_plan synchronize");
+
+  std::memset(plan, 0, sizeof *plan);
+  plan->magic = kPlanMagic;
+  plan->batch = batch;
+  plan->hq = hq;
+  plan->hkv = hkv;
+  plan->split_tokens = split;
+  plan->n_items = P.n_items;
+  plan->n_slots = P.n_slots;
+  plan->reserved0 = P.n_gslots;
+  plan->reserved1 = P.n_gcounters;
+  plan->items_off = P.items_off;
+  plan->bh_off = P.views_off;
+  plan->counters_off = P.counters_off;
+  plan->partials_off = P.slots_off;
+  plan->ws_bytes = P.total;
+  plan->max_len_total = total;
+  (void)P.gslots_off;
+  return ok();
+}
+
+int catekv_decode_attn(int dtype, const catekv_decode_plan_t* plan, const void* q, const catekv_kv_ptrs* kv,
+                       const int64_t* lens, int batch, int hq, int hkv, int d, float scale, float* out,
+                       float* lse, void* ws, size_t ws_bytes, void* stream) {
+  if (!valid_dtype(dtype)) return fail(CATEKV_ERR_UNSUPPORTED, "dtype %d unsupported", dtype);
+  if (!plan || plan->magic != kPlanMagic) return fail(CATEKV_ERR_INVALID_ARG, "plan missing or not built by catekv_decode_plan");
+  if (!q || !kv || !lens || !out) return fail(CATEKV_ERR_INVALID_ARG, "null tensor pointer");
+  int rc = check_heads(hq, hkv, d);
+  if (rc) return rc;
+  if (plan->batch != batch || plan->hq != hq || plan->hkv != hkv)
+    return fail(CATEKV_ERR_INVALID_ARG, "shapes (batch=%d hq=%d hkv=%d) differ from the plan (%d, %d, %d)", batch, hq,
+                hkv, plan->batch, plan->hq, plan->hkv);
+  if (!std::isfinite(scale)) return fail(CATEKV_ERR_INVALID_ARG, "scale is not finite");
+  rc = check_ws(ws, ws_bytes, plan->ws_bytes);
+  if (rc) return rc;
+  char* w = reinterpret_cast<char*>(ws);
+  catekv::DecodeArgs a{};
+  a.q = q;
+  a.kv = kv;
+  a.lens = lens;
+  a.items = reinterpret_cast<const catekv::DecodeItem*>(w + plan->items_off);
+  a.views = reinterpret_cast<const catekv::ViewInfo*>(w + plan->bh_off);
+  a.counters = reinterpret_cast<int*>(w + plan->counters_off);
+  a.slots = reinterpret_cast<float*>(w + plan->partials_off);
+  const size_t sf = catekv::decode_slot_floats(hq / hkv) * sizeof(float);
+  a.gslots = reinterpret_cast<float*>(w + plan->partials_off + a256((size_t)plan->n_slots * sf));
+  a.n_items = plan->n_items;
+  a.n_views = batch * hkv;
+  a.hkv = hkv;
+  a.scale = scale;
+  a.out = out;
+  a.lse = lse;
+  hipError_t e = catekv::launch_decode(dtype, hq / hkv, a, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "decode_attn launch");
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,90 @@
+// Internal interface between the host C ABI (api.cpp) and the kernel
+// launchers (*.hip).  Plain C++: no HIP types beyond hipStream_t.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/catekv.h"
+
+namespace catekv {
+
+constexpr int kD = 128;   // supported head dimension
+
+// One split-KV work item of the decode plan: tokens [t0, t1) of the view
+// bh = b * hkv + h; `part` is its index among the view's items.
+struct DecodeItem {
+  int32_t bh;
+  int32_t part;
+  int32_t t0;
+  int32_t t1;
+};
+
+// Partials of a view are merged in groups of kMergeGroup by the last item of
+// each group to finish, then the group results by the last group.
+constexpr int kMergeGroup = 16;
+
+// Per view: where its partial slots, group slots and group counters live.
+struct ViewInfo {
+  int32_t first_slot;     // slot of part 0
+  int32_t n_parts;
+  int32_t first_gslot;    // group slot of group 0 (views with more than one group)
+  int32_t n_groups;
+  int32_t gcounter;       // index of group 0's counter in the counter array
+  int32_t pad[3];
+};
+
+// Floats per decode partial slot for a group of G query heads: o[G][128],
+// m[G], l[G].
+inline size_t decode_slot_floats(int G) { return (size_t)G * 128 + 2 * (size_t)G; }
+
+struct DecodeArgs {
+  const void* q;
+  const catekv_kv_ptrs* kv;
+  const int64_t* lens;
+  const DecodeItem* items;
+  const ViewInfo* views;
+  int* counters;          // [n_views] view counters, then group counters
+  float* slots;           // partial slots
+  float* gslots;          // group slots
+  int n_items, n_views, hkv;
+  float scale;
+  float* out;
+  float* lse;
+};
+
+hipError_t launch_decode(int dtype, int G, const DecodeArgs& a, hipStream_t stream);
+
+// ---- critical-token selection ------------------------------------------
+struct SelectGeom {
+  int hq, hkv, G, l_obs, cs, n_sel, b;
+  int64_t n, n_keys;       // n_keys = n - l_obs
+  int64_t n_chunks;
+  int n_colblk;            // column blocks of the score passes
+  int heads[128];
+};
+
+int64_t score_colblocks(int64_t n_keys);
+size_t select_workspace_bytes(const SelectGeom& g);
+hipError_t launch_select(int dtype, const SelectGeom& g, const void* q_obs, const void* k,
+                         int32_t* idx_out, void* ws, hipStream_t stream);
+hipError_t launch_compact(int dtype, const void* k, const void* v, int hkv, int64_t n, int cs,
+                          int l_obs, const int32_t* heads, int n_sel, const int32_t* idx, int b,
+                          void* k_c, void* v_c, int64_t* lens_out, hipStream_t stream);
+
+// ---- CV head scoring -----------------------------------------------------
+struct ScoreGeom {
+  int hq, hkv, G, lq;
+  int64_t n, l_init, l_rec, n_keys;   // n_keys = n - l_init - l_rec
+  int64_t q_pos0;
+  int causal;
+  double k_pct, alpha;
+  int n_colblk;
+};
+
+size_t score_workspace_bytes(const ScoreGeom& g);
+hipError_t launch_score(int dtype, const ScoreGeom& g, const void* q_rows, const void* k,
+                        float* cv_out, void* ws, hipStream_t stream);
+
+}  // namespace catekv

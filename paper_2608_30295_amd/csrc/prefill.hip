@@ -1,0 +1,802 @@
+// Prefill-time kernels of CateKV: critical-token selection (Algorithm 1,
+// pre-filling stage), compaction (Cache(K, V, i_k, L_obs)) and CV head
+// scoring (Section 3.2, Eq. 1-4).
+//
+// Both the selection and the CV score need softmax rows over a long key
+// range for the G * L query rows of one KV head (the GQA group mean of
+// Section 3.2).  The rows are short (64-512) and the key range long, so the
+// score block Q K^T is produced tile by tile with MFMA and never stored:
+//   pass 1  per row: running max m and sum l of exp(s - m)   (row statistics)
+//   merge   per row: offset = m * log2(e) / sqrt(d) + log2(l)
+//   pass 2  p = exp2(s * log2(e) / sqrt(d) - offset), then either the column
+//           mass C_j = (1/G) sum_rows p (selection) or the group-mean
+//           observation matrix A[i][j] (CV).
+// Workgroup = 4 waves sharing one 64-token K tile staged in LDS; wave w owns
+// rows [w * MT * 16, (w + 1) * MT * 16) with their Q fragments in registers.
+#include "common.h"
+#include "internal.h"
+
+#include <algorithm>
+
+namespace catekv {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr int kTileTok = 64;     // tokens per LDS tile (4 MFMA column tiles)
+constexpr int kSWaves = 4;       // waves per score workgroup
+constexpr float kMInit = -1e30f; // finite "minus infinity" for running maxima
+
+// MFMA fragment traits.  In k-group kg a lane holds 16 bytes of its row:
+// byte offset kg * 64 + (lane / 16) * 16, i.e. 16-byte segment kg * 4 + lane / 16.
+// The contraction runs over the head dimension, so any dim permutation that is
+// the same for Q and K gives the same dot products.
+template <typename T> struct Frag;
+template <> struct Frag<uint16_t> {
+  static constexpr int KG = 4;   // 4 x (16 x 16 x 32) per 128 dims
+  static constexpr int SEG = 16; // 16-byte segments per row
+  __device__ static __forceinline__ floatx4 mma(uint4 a, uint4 b, floatx4 acc) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
+  }
+};
+template <> struct Frag<float> {
+  static constexpr int KG = 8;   // 8 x 4 x (16 x 16 x 4) per 128 dims
+  static constexpr int SEG = 32;
+  __device__ static __forceinline__ floatx4 mma(uint4 a, uint4 b, floatx4 acc) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
+    return acc;
+  }
+};
+
+// XOR-swizzled slot of (token, segment) in the LDS tile: 16 consecutive
+// tokens reading the same segment hit 16 distinct bank groups.
+template <typename T>
+__device__ __forceinline__ int tile_slot(int tok, int seg) {
+  return tok * Frag<T>::SEG + (seg ^ (tok & 15));
+}
+
+enum ScoreMode { kRowStats = 0, kColMass = 1, kObsMatrix = 2 };
+
+struct ScoreArgs {
+  const void* q;          // [hq][lq][d]
+  const void* k;          // [hkv][n][d]
+  int hkv, lq, G, R;      // R = G * lq rows per KV head
+  int64_t n;
+  int64_t key_off;        // absolute position of key column 0
+  int64_t n_keys;         // key columns
+  int64_t cb_tokens;      // key columns per workgroup
+  int n_colblk;
+  int64_t q_pos0;         // absolute position of query row i = 0 (causal mask)
+  float c;                // log2(e) / sqrt(d)
+  int32_t heads[128];     // KV head per blockIdx.y
+  float2* rowpart;        // kRowStats out: [n_sel][n_colblk][R_pad] (m, l)
+  const float* rowoff;    // kColMass / kObsMatrix in: [n_sel][R_pad]
+  float* colmass;         // kColMass out: [n_sel][n_keys]
+  float* obs;             // kObsMatrix out: [n_sel][lq][n_keys]
+};
+
+template <typename T, int MT, int MODE, int G, bool CAUSAL>
+__global__ __launch_bounds__(kSWaves * 64) void score_kernel(ScoreArgs a) {
+  using F = Frag<T>;
+  constexpr int KG = F::KG, SEG = F::SEG;
+  constexpr int RPAD = kSWaves * MT * 16;
+  constexpr int NSTAGE = kTileTok * SEG / (kSWaves * 64);   // 16-byte loads per thread per tile
+  __shared__ uint4 s_tile[2][kTileTok * SEG];
+  __shared__ float s_col[kSWaves][kTileTok];
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int sel = blockIdx.y, cb = blockIdx.x;
+  const int h = a.heads[sel];
+  const int64_t col0 = (int64_t)cb * a.cb_tokens;                   // first key column
+  const int64_t col_end = min(col0 + a.cb_tokens, a.n_keys);
+  const int n_tiles = (int)((col_end - col0 + kTileTok - 1) / kTileTok);
+  const T* kh = reinterpret_cast<const T*>(a.k) + (size_t)h * a.n * kD;
+  const T* qb = reinterpret_cast<const T*>(a.q);
+
+  // Q fragments: wave-local M tile mt, lane row (lane & 15), segment kg*4 + lane/16
+  uint4 qf[MT][KG];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    const int row = (wave * MT + mt) * 16 + (lane & 15);
+    const bool ok = row < a.R;
+    const int i = row / G, g = row - (row / G) * G;
+    const T* qrow = qb + ((size_t)(h * G + g) * a.lq + (ok ? i : 0)) * kD;
+#pragma unroll
+    for (int kg = 0; kg < KG; ++kg) {
+      uint4 v = ld16(reinterpret_cast<const char*>(qrow) + (kg * 4 + (lane >> 4)) * 16);
+      qf[mt][kg] = ok ? v : make_uint4(0, 0, 0, 0);
+    }
+  }
+
+  // rows owned by this lane's accumulator registers: (mt, r) -> row
+  float st_m[MT][4], st_l[MT][4];      // kRowStats
+  float off[MT][4];                    // kColMass / kObsMatrix
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      st_m[mt][r] = kMInit;
+      st_l[mt][r] = 0.f;
+      if (MODE != kRowStats) {
+        const int row = (wave * MT + mt) * 16 + 4 * (lane >> 4) + r;
+        off[mt][r] = a.rowoff[(size_t)sel * RPAD + row];
+      }
+    }
+  const float thr = 8.0f / a.c;
+
+  uint4 stage[NSTAGE];
+  auto stage_load = [&](int tile) {
+#pragma unroll
+    for (int i = 0; i < NSTAGE; ++i) {
+      const int flat = i * kSWaves * 64 + threadIdx.x;
+      const int tok = flat / SEG, seg = flat - (flat / SEG) * SEG;
+      int64_t col = col0 + (int64_t)tile * kTileTok + tok;
+      col = col < col_end ? col : col0;
+      stage[i] = ld16(reinterpret_cast<const char*>(kh + (size_t)(a.key_off + col) * kD) + seg * 16);
+    }
+  };
+  auto stage_store = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < NSTAGE; ++i) {
+      const int flat = i * kSWaves * 64 + threadIdx.x;
+      const int tok = flat / SEG, seg = flat - (flat / SEG) * SEG;
+      s_tile[buf][tile_slot<T>(tok, seg)] = stage[i];
+    }
+  };
+
+  if (n_tiles > 0) {
+    stage_load(0);
+    stage_store(0);
+  }
+  __syncthreads();
+
+  for (int tile = 0; tile < n_tiles; ++tile) {
+    const int buf = tile & 1;
+    if (tile + 1 < n_tiles) stage_load(tile + 1);
+    uint4 bf[4][KG];
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt)
+#pragma unroll
+      for (int kg = 0; kg < KG; ++kg)
+        bf[nt][kg] = s_tile[buf][tile_slot<T>(nt * 16 + (lane & 15), kg * 4 + (lane >> 4))];
+
+    const int64_t tcol0 = col0 + (int64_t)tile * kTileTok;
+    bool colok[4];
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) colok[nt] = tcol0 + nt * 16 + (lane & 15) < col_end;
+    float cmass[4] = {0.f, 0.f, 0.f, 0.f};
+
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      floatx4 acc[4];
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) acc[nt] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kg = 0; kg < KG; ++kg)
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) acc[nt] = F::mma(qf[mt][kg], bf[nt][kg], acc[nt]);
+
+      // scores with the column and causal masks applied
+      float s[4][4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = (wave * MT + mt) * 16 + 4 * (lane >> 4) + r;
+        const int64_t qpos = a.q_pos0 + row / G;
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) {
+          bool ok = colok[nt];
+          if (CAUSAL) ok = ok && (a.key_off + tcol0 + nt * 16 + (lane & 15) <= qpos);
+          s[r][nt] = ok ? acc[nt][r] : -INFINITY;
+        }
+      }
+
+      if (MODE == kRowStats) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float mx = fmaxf(fmaxf(s[r][0], s[r][1]), fmaxf(s[r][2], s[r][3]));
+          float m = st_m[mt][r];
+          if (mx > m + thr) {
+            st_l[mt][r] *= fast_exp2((m - mx) * a.c);
+            m = mx;
+            st_m[mt][r] = m;
+          }
+          const float mc = m * a.c;
+          float add = 0.f;
+#pragma unroll
+          for (int nt = 0; nt < 4; ++nt) add += fast_exp2(__builtin_fmaf(s[r][nt], a.c, -mc));
+          st_l[mt][r] += add;
+        }
+      } else if (MODE == kColMass) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int nt = 0; nt < 4; ++nt)
+            cmass[nt] += fast_exp2(__builtin_fmaf(s[r][nt], a.c, -off[mt][r]));
+      } else {  // kObsMatrix: group mean over the G rows of each query i
+        float p[4][4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int nt = 0; nt < 4; ++nt) p[r][nt] = fast_exp2(__builtin_fmaf(s[r][nt], a.c, -off[mt][r]));
+        const float invG = 1.0f / (float)G;
+        const int rbase = (wave * MT + mt) * 16 + 4 * (lane >> 4);
+        if (G == 1 || G == 2 || G == 4) {
+#pragma unroll
+          for (int r0 = 0; r0 < 4; r0 += G) {
+            const int i = (rbase + r0) / G;
+#pragma unroll
+            for (int nt = 0; nt < 4; ++nt) {
+              float v = 0.f;
+#pragma unroll
+              for (int r = 0; r < G; ++r) v += p[r0 + r][nt];
+              const int64_t col = tcol0 + nt * 16 + (lane & 15);
+              if (i < a.lq && colok[nt]) a.obs[((size_t)sel * a.lq + i) * a.n_keys + col] = v * invG;
+            }
+          }
+        } else {  // G == 8: the 8 rows of a query span lane groups 2k and 2k + 1
+#pragma unroll
+          for (int nt = 0; nt < 4; ++nt) {
+            float v = p[0][nt] + p[1][nt] + p[2][nt] + p[3][nt];
+            v += shfl_xor(v, 16);
+            const int i = rbase / 8;
+            const int64_t col = tcol0 + nt * 16 + (lane & 15);
+            if (((lane >> 4) & 1) == 0 && i < a.lq && colok[nt])
+              a.obs[((size_t)sel * a.lq + i) * a.n_keys + col] = v * invG;
+          }
+        }
+      }
+    }
+
+    if (MODE == kColMass) {
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) {
+        float v = cmass[nt];
+        v += shfl_xor(v, 16);
+        v += shfl_xor(v, 32);
+        if (lane < 16) s_col[wave][nt * 16 + lane] = v;
+      }
+    }
+    if (tile + 1 < n_tiles) stage_store(buf ^ 1);
+    __syncthreads();
+    if (MODE == kColMass) {
+      if (threadIdx.x < kTileTok) {
+        const int t = threadIdx.x;
+        float v = 0.f;
+#pragma unroll
+        for (int w = 0; w < kSWaves; ++w) v += s_col[w][t];
+        const int64_t col = tcol0 + t;
+        if (col < col_end) a.colmass[(size_t)sel * a.n_keys + col] = v * (1.0f / (float)G);
+      }
+      // s_col is rewritten only after the next tile's barrier
+    }
+  }
+
+  if (MODE == kRowStats) {
+    // merge the 16 lanes that share each row
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float m = st_m[mt][r];
+        const float M = max16(m);
+        const float lsum = sum16(st_l[mt][r] * fast_exp2((m - M) * a.c));
+        const int row = (wave * MT + mt) * 16 + 4 * (lane >> 4) + r;
+        if ((lane & 15) == 0)
+          a.rowpart[((size_t)sel * a.n_colblk + cb) * RPAD + row] = make_float2(M, lsum);
+      }
+  }
+}
+
+// Merge the per-column-block row statistics: offset = m c + log2(l), +inf
+// for rows with no visible key and for padding rows.
+__global__ void rowstats_merge_kernel(const float2* __restrict__ part, int n_colblk, int R, int rpad,
+                                      float c, float* __restrict__ off) {
+  const int sel = blockIdx.y;
+  const int row = blockIdx.x * blockDim.x + threadIdx.x;
+  if (row >= rpad) return;
+  float res = INFINITY;
+  if (row < R) {
+    const float2* p = part + (size_t)sel * n_colblk * rpad + row;
+    float M = kMInit;
+    for (int b = 0; b < n_colblk; ++b) M = fmaxf(M, p[(size_t)b * rpad].x);
+    float L = 0.f;
+    for (int b = 0; b < n_colblk; ++b) {
+      const float2 v = p[(size_t)b * rpad];
+      L += v.y * fast_exp2((v.x - M) * c);
+    }
+    if (L > 0.f) res = M * c + __log2f(L);
+  }
+  off[(size_t)sel * rpad + row] = res;
+}
+
+// ---------------------------------------------------------------------------
+// selection: chunk maxima, radix top-k, compaction
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ uint32_t ord_key(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// S_c = max of C over chunk c (BlockMax of Algorithm 1).
+__global__ void chunk_max_kernel(const float* __restrict__ C, int64_t n_keys, int cs,
+                                 int64_t n_chunks, float* __restrict__ S) {
+  const int sel = blockIdx.y;
+  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= n_chunks) return;
+  const float* Cs = C + (size_t)sel * n_keys;
+  const int64_t e = min((c + 1) * (int64_t)cs, n_keys);
+  float mx = -INFINITY;
+  for (int64_t j = c * cs; j < e; ++j) mx = fmaxf(mx, Cs[j]);
+  S[(size_t)sel * n_chunks + c] = mx;
+}
+
+constexpr int kTopkThreads = 1024;
+
+__device__ int block_exclusive_scan(int v, int* s_buf, int* total) {
+  // Hillis-Steele over kTopkThreads entries in LDS
+  const int t = threadIdx.x;
+  s_buf[t] = v;
+  __syncthreads();
+  for (int off = 1; off < kTopkThreads; off <<= 1) {
+    const int x = t >= off ? s_buf[t - off] : 0;
+    __syncthreads();
+    s_buf[t] += x;
+    __syncthreads();
+  }
+  const int incl = s_buf[t];
+  *total = s_buf[kTopkThreads - 1];
+  __syncthreads();
+  return incl - v;
+}
+
+// Indices of the k largest chunk scores of one head (ties to the lower
+// index), written ascending, then -1 padding up to b.
+__global__ __launch_bounds__(kTopkThreads) void topk_kernel(const float* __restrict__ S, int64_t n_chunks,
+                                                            int k, int b, int32_t* __restrict__ idx_out) {
+  __shared__ int s_hist[256];
+  __shared__ int s_scan[kTopkThreads];
+  __shared__ uint32_t s_prefix;
+  __shared__ int s_remaining;
+  const int sel = blockIdx.x;
+  const float* Ss = S + (size_t)sel * n_chunks;
+  const int t = threadIdx.x;
+
+  uint32_t prefix = 0, mask = 0;
+  int remaining = k;   // rank (1-based, from the top) still to locate within the prefix
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    if (t < 256) s_hist[t] = 0;
+    __syncthreads();
+    for (int64_t i = t; i < n_chunks; i += kTopkThreads) {
+      const uint32_t key = ord_key(Ss[i]);
+      if ((key & mask) == prefix) atomicAdd(&s_hist[(key >> shift) & 255], 1);
+    }
+    __syncthreads();
+    if (t == 0) {
+      int cum = 0, bin = 0;
+      for (bin = 255; bin > 0; --bin) {
+        if (cum + s_hist[bin] >= remaining) break;
+        cum += s_hist[bin];
+      }
+      s_prefix = prefix | ((uint32_t)bin << shift);
+      s_remaining = remaining - cum;
+    }
+    __syncthreads();
+    prefix = s_prefix;
+    remaining = s_remaining;
+    mask |= 255u << shift;
+    __syncthreads();
+  }
+  const uint32_t tau = prefix;   // key of the k-th largest score
+  // remaining = how many entries equal to tau are taken (lowest indices first)
+
+  const int64_t per = (n_chunks + kTopkThreads - 1) / kTopkThreads;
+  const int64_t lo = min((int64_t)t * per, n_chunks), hi = min(lo + per, n_chunks);
+  int n_eq = 0;
+  for (int64_t i = lo; i < hi; ++i) n_eq += ord_key(Ss[i]) == tau;
+  int tot;
+  int eq_before = block_exclusive_scan(n_eq, s_scan, &tot);
+  int n_take = 0;
+  {
+    int eb = eq_before;
+    for (int64_t i = lo; i < hi; ++i) {
+      const uint32_t key = ord_key(Ss[i]);
+      if (key > tau) ++n_take;
+      else if (key == tau) { if (eb < remaining) ++n_take; ++eb; }
+    }
+  }
+  int pos = block_exclusive_scan(n_take, s_scan, &tot);
+  int32_t* out = idx_out + (size_t)sel * b;
+  {
+    int eb = eq_before;
+    for (int64_t i = lo; i < hi; ++i) {
+      const uint32_t key = ord_key(Ss[i]);
+      bool take = false;
+      if (key > tau) take = true;
+      else if (key == tau) { take = eb < remaining; ++eb; }
+      if (take && pos < k) out[pos++] = (int32_t)i;
+    }
+  }
+  for (int i = k + t; i < b; i += kTopkThreads) out[i] = -1;
+}
+
+
+struct CompactArgs {
+  const void* k;
+  const void* v;
+  int64_t n;
+  int cs, l_obs, b, b_eff;
+  int64_t n_keys, n_chunks;
+  const int32_t* idx;     // [n_sel][b]
+  void* k_c;
+  void* v_c;
+  int64_t cap;            // rows per head in k_c / v_c
+  int64_t* lens_out;
+  int32_t heads[128];
+};
+
+// Cache(K, V, i_k, L_obs): rows of the selected chunks (ascending) then the
+// last l_obs rows.  One thread moves one 16-byte segment of K and of V.
+template <typename T>
+__global__ void compact_kernel(CompactArgs a) {
+  constexpr int SEG = kD * (int)sizeof(T) / 16;
+  const int sel = blockIdx.y;
+  const int h = a.heads[sel];
+  const int32_t* ix = a.idx + (size_t)sel * a.b;
+  const int64_t last = ix[a.b_eff - 1];
+  const int64_t tail = a.n_keys - (a.n_chunks - 1) * a.cs;        // size of the last chunk
+  const int64_t n_sel_tok = (int64_t)a.b_eff * a.cs - ((last == a.n_chunks - 1) ? (a.cs - tail) : 0);
+  const int64_t len = n_sel_tok + a.l_obs;
+  if (blockIdx.x == 0 && threadIdx.x == 0) a.lens_out[h] = len;
+  const int64_t flat = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t row = flat / SEG;
+  const int seg = (int)(flat - row * SEG);
+  if (row >= len) return;
+  int64_t src;
+  if (row < n_sel_tok) {
+    int64_t c = ix[row / a.cs];
+    c = c < 0 ? 0 : (c >= a.n_chunks ? a.n_chunks - 1 : c);      // defensive clamp
+    src = c * a.cs + row % a.cs;
+    src = src < a.n_keys ? src : a.n_keys - 1;
+  } else {
+    src = a.n - a.l_obs + (row - n_sel_tok);
+  }
+  const size_t so = ((size_t)h * a.n + src) * kD * sizeof(T) + (size_t)seg * 16;
+  const size_t dof = ((size_t)sel * a.cap + row) * kD * sizeof(T) + (size_t)seg * 16;
+  *reinterpret_cast<uint4*>(reinterpret_cast<char*>(a.k_c) + dof) =
+      ld16(reinterpret_cast<const char*>(a.k) + so);
+  *reinterpret_cast<uint4*>(reinterpret_cast<char*>(a.v_c) + dof) =
+      ld16(reinterpret_cast<const char*>(a.v) + so);
+}
+
+// ---------------------------------------------------------------------------
+// CV: exact order statistics of the observation matrix, counts, score
+// ---------------------------------------------------------------------------
+
+struct CvState {                 // per KV head, in the workspace
+  uint32_t prefix;               // radix prefix of the order statistic x_(lo)
+  int32_t remaining;             // 0-based rank still to resolve inside the prefix
+  uint32_t min_above_key;        // smallest ordered key strictly above x_(lo)
+  uint32_t pad;
+  unsigned long long cnt_lt;     // entries strictly below x_(lo)
+  double phi;
+  unsigned long long sum_c, sum_c2;
+};
+
+constexpr int kRadixBins = 2048;   // digits: bits [31:21], [20:10] (11 bits), [9:0] (10 bits)
+
+__device__ __forceinline__ int digit_shift(int pass) { return pass == 0 ? 21 : (pass == 1 ? 10 : 0); }
+__device__ __forceinline__ uint32_t digit_mask_above(int pass) {
+  return pass == 0 ? 0u : (pass == 1 ? 0xFFE00000u : 0xFFFFFC00u);
+}
+__device__ __forceinline__ float key_to_float(uint32_t key) {
+  return __uint_as_float((key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key);
+}
+
+__global__ void cv_init_kernel(CvState* st, uint32_t* hist, int64_t N, double k_pct, int hkv) {
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < 3 * hkv * kRadixBins; i += gridDim.x * blockDim.x)
+    hist[i] = 0;
+  if (blockIdx.x == 0 && threadIdx.x < hkv) {
+    CvState& s = st[threadIdx.x];
+    s.prefix = 0;
+    s.remaining = (int32_t)(int64_t)floor((double)(N - 1) * k_pct);
+    s.min_above_key = 0xFFFFFFFFu;
+    s.cnt_lt = 0;
+    s.phi = 0.0;
+    s.sum_c = 0;
+    s.sum_c2 = 0;
+  }
+}
+
+// Histogram of one radix digit over the entries whose higher digits match
+// the prefix found so far.  hist: [hkv][kRadixBins] for this pass.
+__global__ void radix_hist_kernel(const float* __restrict__ A, int64_t N, int pass,
+                                  const CvState* __restrict__ st, uint32_t* __restrict__ hist) {
+  __shared__ uint32_t s_h[kRadixBins];
+  const int h = blockIdx.y;
+  for (int i = threadIdx.x; i < kRadixBins; i += blockDim.x) s_h[i] = 0;
+  __syncthreads();
+  const uint32_t pm = digit_mask_above(pass), pv = st[h].prefix & pm;
+  const int shift = digit_shift(pass);
+  const uint32_t dmask = pass == 2 ? 0x3FFu : 0x7FFu;
+  const float* Ah = A + (size_t)h * N;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const uint32_t key = ord_key(Ah[i]);
+    if ((key & pm) == pv) atomicAdd(&s_h[(key >> shift) & dmask], 1u);
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < kRadixBins; i += blockDim.x)
+    if (s_h[i]) atomicAdd(&hist[(size_t)h * kRadixBins + i], s_h[i]);
+}
+
+// Pick the digit that holds the target rank; one thread per head.  The
+// entries of lower digits are strictly below x_(lo) and are counted.
+__global__ void radix_pick_kernel(const uint32_t* __restrict__ hist, int pass, CvState* st, int hkv) {
+  const int h = blockIdx.x * blockDim.x + threadIdx.x;
+  if (h >= hkv) return;
+  const uint32_t* hh = hist + (size_t)h * kRadixBins;
+  const int nb = pass == 2 ? 1024 : kRadixBins;
+  const int64_t rem = st[h].remaining;
+  int64_t cum = 0;
+  int bin = 0;
+  for (bin = 0; bin < nb - 1; ++bin) {
+    if (cum + hh[bin] > rem) break;
+    cum += hh[bin];
+  }
+  st[h].prefix |= (uint32_t)bin << digit_shift(pass);
+  st[h].remaining = (int32_t)(rem - cum);
+  st[h].cnt_lt += (unsigned long long)cum;
+}
+
+// Smallest ordered key strictly above x_(lo) (needed when x_(lo + 1) differs).
+__global__ void radix_min_above_kernel(const float* __restrict__ A, int64_t N, CvState* st) {
+  __shared__ uint32_t s_min;
+  const int h = blockIdx.y;
+  if (threadIdx.x == 0) s_min = 0xFFFFFFFFu;
+  __syncthreads();
+  const uint32_t x = st[h].prefix;
+  const float* Ah = A + (size_t)h * N;
+  uint32_t mn = 0xFFFFFFFFu;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const uint32_t key = ord_key(Ah[i]);
+    if (key > x) mn = min(mn, key);
+  }
+  atomicMin(&s_min, mn);
+  __syncthreads();
+  if (threadIdx.x == 0) atomicMin(&st[h].min_above_key, s_min);
+}
+
+// Phi = alpha * (x_(lo) + frac * (x_(lo+1) - x_(lo))) in fp64 (Eq. 2).
+__global__ void cv_threshold_kernel(CvState* st, const uint32_t* __restrict__ hist_last, int64_t N,
+                                    double k_pct, double alpha, int hkv) {
+  const int h = blockIdx.x * blockDim.x + threadIdx.x;
+  if (h >= hkv) return;
+  const double pos = (double)(N - 1) * k_pct;
+  const int64_t lo = (int64_t)floor(pos);
+  const double frac = pos - (double)lo;
+  const uint32_t xk = st[h].prefix;
+  const unsigned long long eq = hist_last[(size_t)h * kRadixBins + (xk & 0x3FFu)];
+  const unsigned long long le = st[h].cnt_lt + eq;        // entries <= x_(lo)
+  const double xlo = (double)key_to_float(xk);
+  double xhi = xlo;
+  if ((int64_t)le < lo + 2 && lo + 1 <= N - 1) xhi = (double)key_to_float(st[h].min_above_key);
+  st[h].phi = alpha * (xlo + frac * (xhi - xlo));
+}
+
+// C_j = #{i : A[i][j] >= Phi} (Eq. 2-3); exact integer sums of C and C^2.
+__global__ void cv_count_kernel(const float* __restrict__ A, int lq, int64_t n_keys, CvState* st) {
+  __shared__ unsigned long long s1, s2;
+  const int h = blockIdx.y;
+  if (threadIdx.x == 0) { s1 = 0; s2 = 0; }
+  __syncthreads();
+  const double phi = st[h].phi;
+  const float* Ah = A + (size_t)h * lq * n_keys;
+  unsigned long long a1 = 0, a2 = 0;
+  for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n_keys;
+       j += (int64_t)gridDim.x * blockDim.x) {
+    unsigned long long cj = 0;
+    for (int i = 0; i < lq; ++i) cj += (double)Ah[(size_t)i * n_keys + j] >= phi;
+    a1 += cj;
+    a2 += cj * cj;
+  }
+  atomicAdd(&s1, a1);
+  atomicAdd(&s2, a2);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    atomicAdd(&st[h].sum_c, s1);
+    atomicAdd(&st[h].sum_c2, s2);
+  }
+}
+
+// Eq. 4: population standard deviation over the mean, from exact integers.
+__global__ void cv_final_kernel(const CvState* __restrict__ st, int64_t n_keys, float* cv_out, int hkv) {
+  const int h = blockIdx.x * blockDim.x + threadIdx.x;
+  if (h >= hkv) return;
+  const double N = (double)n_keys;
+  const double mu = (double)st[h].sum_c / N;
+  if (mu == 0.0) { cv_out[h] = 0.f; return; }
+  double var = (double)st[h].sum_c2 / N - mu * mu;
+  var = var < 0.0 ? 0.0 : var;
+  cv_out[h] = (float)(sqrt(var) / mu);
+}
+
+// ---------------------------------------------------------------------------
+// host-side launchers
+// ---------------------------------------------------------------------------
+
+static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+static inline int rows_pad(int R) {
+  const int mt = (R + 63) / 64;
+  return (mt <= 1 ? 1 : mt <= 2 ? 2 : mt <= 4 ? 4 : 8) * 64;
+}
+constexpr int64_t kColBlockTokens = 512;
+
+int64_t score_colblocks(int64_t n_keys) { return (n_keys + kColBlockTokens - 1) / kColBlockTokens; }
+
+struct SelectLayout {
+  size_t rowpart, rowoff, colmass, chunks, total;
+};
+static SelectLayout select_layout(const SelectGeom& g) {
+  SelectLayout L{};
+  const int rp = rows_pad(g.G * g.l_obs);
+  size_t o = 0;
+  L.rowpart = o; o += align256((size_t)g.n_sel * g.n_colblk * rp * sizeof(float2));
+  L.rowoff = o; o += align256((size_t)g.n_sel * rp * sizeof(float));
+  L.colmass = o; o += align256((size_t)g.n_sel * g.n_keys * sizeof(float));
+  L.chunks = o; o += align256((size_t)g.n_sel * g.n_chunks * sizeof(float));
+  L.total = o;
+  return L;
+}
+
+size_t select_workspace_bytes(const SelectGeom& g) { return select_layout(g).total; }
+
+template <typename T, int MODE, int G, bool CAUSAL>
+static hipError_t launch_score_mt(int mt, dim3 grid, hipStream_t s, const ScoreArgs& a) {
+  switch (mt) {
+    case 1: hipLaunchKernelGGL((score_kernel<T, 1, MODE, G, CAUSAL>), grid, dim3(kSWaves * 64), 0, s, a); break;
+    case 2: hipLaunchKernelGGL((score_kernel<T, 2, MODE, G, CAUSAL>), grid, dim3(kSWaves * 64), 0, s, a); break;
+    case 4: hipLaunchKernelGGL((score_kernel<T, 4, MODE, G, CAUSAL>), grid, dim3(kSWaves * 64), 0, s, a); break;
+    case 8: hipLaunchKernelGGL((score_kernel<T, 8, MODE, G, CAUSAL>), grid, dim3(kSWaves * 64), 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+template <int MODE, bool CAUSAL>
+static hipError_t launch_score_any(int dtype, int G, int mt, dim3 grid, hipStream_t s, const ScoreArgs& a) {
+#define CATEKV_SC(T, GG) \
+  if (G == GG) return launch_score_mt<T, MODE, GG, CAUSAL>(mt, grid, s, a);
+  if (dtype == CATEKV_BF16) {
+    CATEKV_SC(uint16_t, 1) CATEKV_SC(uint16_t, 2) CATEKV_SC(uint16_t, 4) CATEKV_SC(uint16_t, 8)
+  } else {
+    CATEKV_SC(float, 1) CATEKV_SC(float, 2) CATEKV_SC(float, 4) CATEKV_SC(float, 8)
+  }
+#undef CATEKV_SC
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_select(int dtype, const SelectGeom& g, const void* q_obs, const void* k,
+                         int32_t* idx_out, void* ws, hipStream_t stream) {
+  const SelectLayout L = select_layout(g);
+  char* w = reinterpret_cast<char*>(ws);
+  const int R = g.G * g.l_obs;
+  const int rp = rows_pad(R);
+  const int mt = rp / 64;
+  ScoreArgs a{};
+  a.q = q_obs; a.k = k; a.hkv = g.hkv; a.lq = g.l_obs; a.G = g.G; a.R = R; a.n = g.n;
+  a.key_off = 0; a.n_keys = g.n_keys; a.cb_tokens = kColBlockTokens; a.n_colblk = g.n_colblk;
+  a.q_pos0 = g.n - g.l_obs; a.c = kLog2e / sqrtf((float)kD);
+  for (int i = 0; i < g.n_sel; ++i) a.heads[i] = g.heads[i];
+  a.rowpart = reinterpret_cast<float2*>(w + L.rowpart);
+  a.rowoff = reinterpret_cast<const float*>(w + L.rowoff);
+  a.colmass = reinterpret_cast<float*>(w + L.colmass);
+  const dim3 grid(g.n_colblk, g.n_sel);
+  hipError_t e = launch_score_any<kRowStats, false>(dtype, g.G, mt, grid, stream, a);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(rowstats_merge_kernel, dim3((rp + 255) / 256, g.n_sel), dim3(256), 0, stream,
+                     a.rowpart, g.n_colblk, R, rp, a.c, reinterpret_cast<float*>(w + L.rowoff));
+  e = launch_score_any<kColMass, false>(dtype, g.G, mt, grid, stream, a);
+  if (e != hipSuccess) return e;
+  float* S = reinterpret_cast<float*>(w + L.chunks);
+  hipLaunchKernelGGL(chunk_max_kernel, dim3((unsigned)((g.n_chunks + 255) / 256), g.n_sel), dim3(256), 0,
+                     stream, a.colmass, g.n_keys, g.cs, g.n_chunks, S);
+  const int k_eff = (int)(g.b < g.n_chunks ? g.b : g.n_chunks);
+  hipLaunchKernelGGL(topk_kernel, dim3(g.n_sel), dim3(kTopkThreads), 0, stream, S, g.n_chunks, k_eff,
+                     g.b, idx_out);
+  return hipGetLastError();
+}
+
+hipError_t launch_compact(int dtype, const void* k, const void* v, int hkv, int64_t n, int cs,
+                          int l_obs, const int32_t* heads, int n_sel, const int32_t* idx, int b,
+                          void* k_c, void* v_c, int64_t* lens_out, hipStream_t stream) {
+  (void)hkv;
+  CompactArgs a{};
+  a.k = k; a.v = v; a.n = n; a.cs = cs; a.l_obs = l_obs; a.b = b;
+  a.n_keys = n - l_obs;
+  a.n_chunks = (a.n_keys + cs - 1) / cs;
+  a.b_eff = (int)(b < a.n_chunks ? b : a.n_chunks);
+  a.idx = idx; a.k_c = k_c; a.v_c = v_c;
+  a.cap = (int64_t)b * cs + l_obs;
+  a.lens_out = lens_out;
+  for (int i = 0; i < n_sel; ++i) a.heads[i] = heads[i];
+  const int64_t seg = dtype == CATEKV_BF16 ? 16 : 32;
+  const int64_t rows = (int64_t)a.b_eff * cs + l_obs;
+  const unsigned nblk = (unsigned)((rows * seg + 255) / 256);
+  if (dtype == CATEKV_BF16)
+    hipLaunchKernelGGL(compact_kernel<uint16_t>, dim3(nblk, n_sel), dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL(compact_kernel<float>, dim3(nblk, n_sel), dim3(256), 0, stream, a);
+  return hipGetLastError();
+}
+
+struct ScoreLayout {
+  size_t rowpart, rowoff, obs, hist, state, total;
+};
+static ScoreLayout score_layout(const ScoreGeom& g) {
+  ScoreLayout L{};
+  const int rp = rows_pad(g.G * g.lq);
+  size_t o = 0;
+  L.rowpart = o; o += align256((size_t)g.hkv * g.n_colblk * rp * sizeof(float2));
+  L.rowoff = o; o += align256((size_t)g.hkv * rp * sizeof(float));
+  L.obs = o; o += align256((size_t)g.hkv * g.lq * g.n_keys * sizeof(float));
+  L.hist = o; o += align256((size_t)3 * g.hkv * kRadixBins * sizeof(uint32_t));
+  L.state = o; o += align256((size_t)g.hkv * sizeof(CvState));
+  L.total = o;
+  return L;
+}
+
+size_t score_workspace_bytes(const ScoreGeom& g) { return score_layout(g).total; }
+
+hipError_t launch_score(int dtype, const ScoreGeom& g, const void* q_rows, const void* k,
+                        float* cv_out, void* ws, hipStream_t stream) {
+  const ScoreLayout L = score_layout(g);
+  char* w = reinterpret_cast<char*>(ws);
+  const int R = g.G * g.lq;
+  const int rp = rows_pad(R);
+  const int mt = rp / 64;
+  ScoreArgs a{};
+  a.q = q_rows; a.k = k; a.hkv = g.hkv; a.lq = g.lq; a.G = g.G; a.R = R; a.n = g.n;
+  a.key_off = g.l_init; a.n_keys = g.n_keys; a.cb_tokens = kColBlockTokens; a.n_colblk = g.n_colblk;
+  a.q_pos0 = g.q_pos0; a.c = kLog2e / sqrtf((float)kD);
+  for (int i = 0; i < g.hkv; ++i) a.heads[i] = i;
+  a.rowpart = reinterpret_cast<float2*>(w + L.rowpart);
+  a.rowoff = reinterpret_cast<const float*>(w + L.rowoff);
+  a.obs = reinterpret_cast<float*>(w + L.obs);
+  const dim3 grid(g.n_colblk, g.hkv);
+  hipError_t e = g.causal ? launch_score_any<kRowStats, true>(dtype, g.G, mt, grid, stream, a)
+                          : launch_score_any<kRowStats, false>(dtype, g.G, mt, grid, stream, a);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(rowstats_merge_kernel, dim3((rp + 255) / 256, g.hkv), dim3(256), 0, stream,
+                     a.rowpart, g.n_colblk, R, rp, a.c, reinterpret_cast<float*>(w + L.rowoff));
+  e = g.causal ? launch_score_any<kObsMatrix, true>(dtype, g.G, mt, grid, stream, a)
+               : launch_score_any<kObsMatrix, false>(dtype, g.G, mt, grid, stream, a);
+  if (e != hipSuccess) return e;
+
+  const int64_t N = (int64_t)g.lq * g.n_keys;
+  uint32_t* hist = reinterpret_cast<uint32_t*>(w + L.hist);
+  CvState* st = reinterpret_cast<CvState*>(w + L.state);
+  hipLaunchKernelGGL(cv_init_kernel, dim3(24), dim3(256), 0, stream, st, hist, N, g.k_pct, g.hkv);
+  const unsigned hb = (unsigned)std::min<int64_t>(512, (N + 1023) / 1024);
+  const unsigned pb = (unsigned)((g.hkv + 63) / 64);
+  for (int pass = 0; pass < 3; ++pass) {
+    uint32_t* hp = hist + (size_t)pass * g.hkv * kRadixBins;
+    hipLaunchKernelGGL(radix_hist_kernel, dim3(hb, g.hkv), dim3(256), 0, stream, a.obs, N, pass, st, hp);
+    hipLaunchKernelGGL(radix_pick_kernel, dim3(pb), dim3(64), 0, stream, hp, pass, st, g.hkv);
+  }
+  hipLaunchKernelGGL(radix_min_above_kernel, dim3(hb, g.hkv), dim3(256), 0, stream, a.obs, N, st);
+  hipLaunchKernelGGL(cv_threshold_kernel, dim3(pb), dim3(64), 0, stream, st,
+                     hist + (size_t)2 * g.hkv * kRadixBins, N, g.k_pct, g.alpha, g.hkv);
+  const unsigned cb = (unsigned)std::min<int64_t>(1024, (g.n_keys + 255) / 256);
+  hipLaunchKernelGGL(cv_count_kernel, dim3(cb, g.hkv), dim3(256), 0, stream, a.obs, g.lq, g.n_keys, st);
+  hipLaunchKernelGGL(cv_final_kernel, dim3(pb), dim3(64), 0, stream, st, g.n_keys, cv_out, g.hkv);
+  return hipGetLastError();
+}
+
+}  // namespace catekv

@@ -1,0 +1,309 @@
+"""GPU parity: every C-ABI call against the CPU oracle on the same seeded
+inputs (small and ragged sizes here; full sizes in test_gpu_fullsize.py)."""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2608_30295_amd as ck
+import synth
+from gpu_util import DEV, assert_rows_close, check_topk, f64, to_dev, to_host_storage
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _views(rng, lens, dtype, heavy=True):
+    """Independent K/V buffers per view (storage arrays)."""
+    out = []
+    for L in lens:
+        k = rng.standard_normal((max(L, 1), 128), dtype=np.float32)
+        v = rng.standard_normal((max(L, 1), 128), dtype=np.float32)
+        if heavy and L > 10:
+            hot = rng.choice(L, size=max(1, L // 100), replace=False)
+            k[hot] *= 3
+        if dtype == "bf16":
+            k, v = synth.f32_to_bf16_bits(k), synth.f32_to_bf16_bits(v)
+        out.append((k, v))
+    return out
+
+
+def run_decode(views, B, hq, hkv, dtype, q_st, split=0, lens_dev=None, max_len=None):
+    kd = [(to_dev(k), to_dev(v)) for k, v in views]
+    table = ck.kv_table([(k.data_ptr(), v.data_ptr()) for k, v in kd], DEV)
+    lens = np.array([0 if L is None else L for L in (max_len if max_len is not None else
+                                                     [kv[0].shape[0] for kv in views])], dtype=np.int64)
+    plan = ck.decode_plan(lens, hq, hkv, DEV, split_tokens=split)
+    if lens_dev is None:
+        lens_dev = torch.from_numpy(lens).to(DEV)
+    q = to_dev(q_st)
+    out, lse = ck.decode_attn(plan, q, table, lens_dev)
+    torch.cuda.synchronize()
+    return out.cpu().numpy(), lse.cpu().numpy(), kd, plan
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_decode_ragged_views(dtype):
+    rng = np.random.default_rng(11)
+    B, hq, hkv = 2, 8, 2
+    lens = [37, 40000, 1, 2113]
+    views = _views(rng, lens, dtype)
+    q = rng.standard_normal((B, hq, 128), dtype=np.float32)
+    q_st = synth.f32_to_bf16_bits(q) if dtype == "bf16" else q
+    say(f"decode ragged {dtype} lens={lens}")
+    out, lse, _, plan = run_decode(views, B, hq, hkv, dtype, q_st, split=256)
+    assert plan.plan.reserved0 > 0          # a view with more than one merge group
+    qq = f64(q_st)
+    for b in range(B):
+        vv = [(f64(views[b * hkv + h][0])[:lens[b * hkv + h]], f64(views[b * hkv + h][1])[:lens[b * hkv + h]])
+              for h in range(hkv)]
+        o_ref, l_ref = O.decode_gqa(qq[b], vv)
+        assert_rows_close(out[b], o_ref, dtype, f"b={b}")
+        np.testing.assert_allclose(lse[b], l_ref, atol=1e-4, rtol=0)
+
+
+def test_decode_empty_and_single_token_views():
+    rng = np.random.default_rng(12)
+    B, hq, hkv = 1, 4, 4
+    lens = [0, 1, 2, 300]
+    views = _views(rng, lens, "bf16")
+    q_st = synth.f32_to_bf16_bits(rng.standard_normal((B, hq, 128), dtype=np.float32))
+    say("decode empty/single views")
+    out, lse, _, _ = run_decode(views, B, hq, hkv, "bf16", q_st, max_len=lens)
+    assert (out[0, 0] == 0).all() and lse[0, 0] == -np.inf
+    np.testing.assert_allclose(out[0, 1], f64(views[1][1])[0], atol=1e-6)
+    for h in (2, 3):
+        o_ref, l_ref, _ = O.attention_decode(f64(q_st)[0, h], f64(views[h][0])[:lens[h]], f64(views[h][1])[:lens[h]],
+                                             1 / math.sqrt(128))
+        assert_rows_close(out[0, h][None], o_ref[None], "bf16")
+
+
+def test_decode_device_length_below_plan():
+    # the plan holds upper bounds; the actual length is read on the device
+    rng = np.random.default_rng(13)
+    B, hq, hkv = 1, 8, 2
+    cap = [3000, 1200]
+    actual = [2111, 1200]
+    views = _views(rng, cap, "bf16")
+    q_st = synth.f32_to_bf16_bits(rng.standard_normal((B, hq, 128), dtype=np.float32))
+    say("decode device lengths below plan")
+    lens_dev = torch.tensor(actual, dtype=torch.int64, device=DEV)
+    out, lse, _, _ = run_decode(views, B, hq, hkv, "bf16", q_st, split=512, lens_dev=lens_dev, max_len=cap)
+    vv = [(f64(views[h][0])[:actual[h]], f64(views[h][1])[:actual[h]]) for h in range(hkv)]
+    o_ref, l_ref = O.decode_gqa(f64(q_st)[0], vv)
+    assert_rows_close(out[0], o_ref, "bf16")
+
+
+@pytest.mark.parametrize("G", [1, 2, 4, 8])
+def test_decode_group_sizes(G):
+    rng = np.random.default_rng(20 + G)
+    hkv = 2
+    hq = G * hkv
+    lens = [777, 3001]
+    views = _views(rng, lens, "bf16")
+    q_st = synth.f32_to_bf16_bits(rng.standard_normal((1, hq, 128), dtype=np.float32))
+    say(f"decode G={G}")
+    out, lse, _, _ = run_decode(views, 1, hq, hkv, "bf16", q_st, split=256)
+    vv = [(f64(k), f64(v)) for k, v in views]
+    o_ref, l_ref = O.decode_gqa(f64(q_st)[0], vv)
+    assert_rows_close(out[0], o_ref, "bf16")
+    np.testing.assert_allclose(lse[0], l_ref, atol=1e-4, rtol=0)
+
+
+def test_decode_repeated_steps_reuse_plan():
+    # counters are reset by the kernel itself: several steps on one plan agree
+    rng = np.random.default_rng(14)
+    lens = [9000, 500]
+    views = _views(rng, lens, "bf16")
+    q_st = synth.f32_to_bf16_bits(rng.standard_normal((1, 8, 128), dtype=np.float32))
+    say("decode repeated steps")
+    kd = [(to_dev(k), to_dev(v)) for k, v in views]
+    table = ck.kv_table([(k.data_ptr(), v.data_ptr()) for k, v in kd], DEV)
+    plan = ck.decode_plan(np.array(lens), 8, 2, DEV, split_tokens=256)
+    lens_dev = torch.tensor(lens, dtype=torch.int64, device=DEV)
+    q = to_dev(q_st)
+    outs = []
+    for _ in range(4):
+        o, _ = ck.decode_attn(plan, q, table, lens_dev)
+        outs.append(o.clone())
+    torch.cuda.synchronize()
+    for o in outs[1:]:
+        assert torch.equal(o, outs[0])
+    o_ref, _ = O.decode_gqa(f64(q_st)[0], [(f64(k), f64(v)) for k, v in views])
+    assert_rows_close(outs[0].cpu().numpy()[0], o_ref, "bf16")
+
+
+# ---------------------------------------------------------------- selection
+
+def _small(name, **kw):
+    return synth.WORKLOADS[name].scaled(**kw)
+
+
+SEL_CASES = [
+    ("ctx4k_f32", dict()),                                    # the full 4K fp32 workload
+    ("ctx32k_bf16", dict(n=5000 + 64 + 3)),                   # ragged last tile and chunk
+    ("ctx32k_bf16", dict(n=64 + 40)),                         # shorter than one tile
+    ("ctx128k_bf16", dict(n=9000, hq=16, hkv=2)),            # G = 8 rows of 512
+]
+
+
+@pytest.mark.parametrize("name,kw", SEL_CASES)
+def test_select_and_compact(name, kw):
+    wl = _small(name, **kw)
+    seq = synth.make_sequence(wl)
+    heads = list(range(wl.hkv))[::-1][: max(1, wl.hkv // 2 + 1)]
+    say(f"select {wl.name} n={seq.n} hq={wl.hq} hkv={wl.hkv} heads={heads} b={wl.chunk_budget}")
+    q_obs, k, v = to_dev(seq.q_obs), to_dev(seq.k), to_dev(seq.v)
+    idx = ck.select_critical(q_obs, k, heads, wl.cs, wl.chunk_budget)
+    torch.cuda.synchronize()
+    idx = idx.cpu().numpy()
+    qf, kf = f64(seq.q_obs), f64(seq.k)
+    scale = 1 / math.sqrt(128)
+    for s, h in enumerate(heads):
+        sc = O.chunk_scores(qf, kf, h, wl.group, wl.l_obs, wl.cs, scale)
+        swaps = check_topk(idx[s], sc, wl.chunk_budget)
+        say(f"  head {h}: swaps inside the 1e-5 band: {swaps}")
+    # compaction, staged on the GPU's own indices: bitwise
+    lens = torch.full((wl.hkv,), -7, dtype=torch.int64, device=DEV)
+    idx_d = torch.from_numpy(idx).to(DEV)
+    k_c, v_c = ck.compact_kv(k, v, heads, idx_d, wl.cs, wl.l_obs, lens)
+    torch.cuda.synchronize()
+    lens = lens.cpu().numpy()
+    kc_h, vc_h = to_host_storage(k_c), to_host_storage(v_c)
+    for s, h in enumerate(heads):
+        sel = idx[s][idx[s] >= 0]
+        rows = O.compact_rows(seq.n, wl.l_obs, wl.cs, sel)
+        assert lens[h] == rows.size
+        assert np.array_equal(kc_h[s][:rows.size], seq.k[h][rows])
+        assert np.array_equal(vc_h[s][:rows.size], seq.v[h][rows])
+    for h in range(wl.hkv):
+        if h not in heads:
+            assert lens[h] == -7
+
+
+def test_select_budget_above_chunk_count_and_zero_keys():
+    wl = _small("ctx32k_bf16", n=64 + 8 * 20 + 5, hq=8, hkv=2)
+    seq = synth.make_sequence(wl)
+    k0 = np.zeros_like(seq.k)
+    say("select with zero keys and a budget above the chunk count")
+    idx = ck.select_critical(to_dev(seq.q_obs), to_dev(k0), [0, 1], wl.cs, 40).cpu().numpy()
+    nc = -(-(seq.n - 64) // 8)
+    for s in range(2):
+        assert idx[s][:nc].tolist() == list(range(nc))
+        assert (idx[s][nc:] == -1).all()
+    idx = ck.select_critical(to_dev(seq.q_obs), to_dev(k0), [1], wl.cs, 5).cpu().numpy()
+    assert idx[0].tolist() == [0, 1, 2, 3, 4]
+
+
+def test_full_budget_pipeline_equals_full_attention():
+    # budget >= chunk count: the compact cache is the full cache, and decoding
+    # over it reproduces full attention
+    wl = _small("ctx32k_bf16", n=2048 + 64 + 5, hq=8, hkv=2)
+    seq = synth.make_sequence(wl)
+    say("full-budget pipeline")
+    k, v = to_dev(seq.k), to_dev(seq.v)
+    nc = -(-(seq.n - 64) // 8)
+    idx = ck.select_critical(to_dev(seq.q_obs), k, [0, 1], 8, nc + 3)
+    lens = torch.zeros(2, dtype=torch.int64, device=DEV)
+    k_c, v_c = ck.compact_kv(k, v, [0, 1], idx, 8, 64, lens)
+    torch.cuda.synchronize()
+    assert lens.cpu().tolist() == [seq.n, seq.n]
+    assert torch.equal(k_c[:, :seq.n].view(torch.int16), k.view(torch.int16))
+    q_st = synth.decode_queries(wl, 0)
+    table = ck.kv_table([(k_c[h].data_ptr(), v_c[h].data_ptr()) for h in range(2)], DEV)
+    plan = ck.decode_plan(np.array([k_c.shape[1]] * 2), 8, 2, DEV)
+    out, _ = ck.decode_attn(plan, to_dev(q_st), table, lens)
+    o_ref, _ = O.decode_gqa(f64(q_st)[0], [(f64(seq.k[h]), f64(seq.v[h])) for h in range(2)])
+    assert_rows_close(out.cpu().numpy()[0], o_ref, "bf16")
+
+
+# ---------------------------------------------------------------- CV score
+
+CV_CASES = [
+    ("ctx4k_f32", dict(), True),
+    ("ctx32k_bf16", dict(n=6000), True),
+    ("ctx1m_bf16", dict(n=7000), True),          # decode-time calibration rows (mask is a no-op)
+    ("ctx32k_bf16", dict(n=3000, hq=16, hkv=2), False),
+]
+
+
+@pytest.mark.parametrize("name,kw,causal", CV_CASES)
+def test_score_heads(name, kw, causal):
+    wl = _small(name, **kw)
+    seq = synth.make_sequence(wl)
+    say(f"score_heads {wl.name} n={seq.n} rows={seq.q_cv.shape[1]} causal={causal}")
+    cv = ck.score_heads(to_dev(seq.q_cv), to_dev(seq.k), q_pos0=seq.q_cv_pos0, l_init=wl.l_init,
+                        l_rec=wl.l_rec, k_pct=wl.k_pct, alpha=wl.alpha, causal=causal)
+    torch.cuda.synchronize()
+    cv = cv.cpu().numpy().astype(np.float64)
+    ref = O.score_heads(f64(seq.q_cv), seq.q_cv_pos0, f64(seq.k), wl.l_init, wl.l_rec, wl.k_pct, wl.alpha,
+                        causal=causal)
+    say("  gpu", np.round(cv, 6), "\n  ref", np.round(ref, 6))
+    np.testing.assert_allclose(cv, ref, rtol=1e-4, atol=1e-6)
+
+
+def test_score_heads_toy_through_abi():
+    # the hand-worked 2 x 4 toy (cv = sqrt(3)) driven through the GPU path
+    A = np.array([[0.7, 0.1, 0.1, 0.1], [0.6, 0.2, 0.1, 0.1]])
+    q = np.zeros((1, 2, 128), dtype=np.float32)
+    q[0, 0, 0] = q[0, 1, 1] = 1.0
+    k = np.zeros((1, 4, 128), dtype=np.float32)
+    k[0, :, 0] = np.log(A[0]) * math.sqrt(128)
+    k[0, :, 1] = np.log(A[1]) * math.sqrt(128)
+    say("score_heads toy")
+    cv = ck.score_heads(to_dev(q), to_dev(k), q_pos0=10, l_init=0, l_rec=0, k_pct=0.75, alpha=1.0)
+    assert abs(float(cv.cpu()[0]) - math.sqrt(3)) < 1e-5
+
+
+# ----------------------------------------------------- whole pipeline (4K)
+
+def test_pipeline_ctx4k_f32():
+    """CV score -> Eq. 5 -> select -> compact -> one decode step on the 4K fp32
+    workload, against the oracle running the same steps."""
+    wl = synth.WORKLOADS["ctx4k_f32"]
+    seq = synth.make_sequence(wl)
+    say("pipeline ctx4k_f32")
+    k, v = to_dev(seq.k), to_dev(seq.v)
+    cv = ck.score_heads(to_dev(seq.q_cv), k, q_pos0=seq.q_cv_pos0, l_init=wl.l_init, l_rec=wl.l_rec,
+                        k_pct=wl.k_pct, alpha=wl.alpha).cpu().numpy()
+    cv_ref = O.score_heads(f64(seq.q_cv), seq.q_cv_pos0, f64(seq.k), wl.l_init, wl.l_rec, wl.k_pct, wl.alpha)
+    np.testing.assert_allclose(cv, cv_ref, rtol=1e-4)
+    cons = ck.classify_heads(cv[None], wl.r)
+    cons_ref = O.static_head_types(cv_ref[None], wl.r)
+    assert cons.tolist() == cons_ref.tolist()
+    heads = [h for h in range(wl.hkv) if cons[h]]
+    assert len(heads) == 4
+    idx = ck.select_critical(to_dev(seq.q_obs), k, heads, wl.cs, wl.chunk_budget)
+    idx_h = idx.cpu().numpy()
+    for s, h in enumerate(heads):
+        sc = O.chunk_scores(f64(seq.q_obs), f64(seq.k), h, wl.group, wl.l_obs, wl.cs, 1 / math.sqrt(128))
+        check_topk(idx_h[s], sc, wl.chunk_budget)
+    # downstream stages are compared on the GPU's own selection
+    idx_ref = [row[row >= 0] for row in idx_h]
+    lens = torch.tensor([seq.n] * wl.hkv, dtype=torch.int64, device=DEV)
+    k_c, v_c = ck.compact_kv(k, v, heads, idx, wl.cs, wl.l_obs, lens)
+    pairs, maxlen = [], []
+    for h in range(wl.hkv):
+        if h in heads:
+            s = heads.index(h)
+            pairs.append((k_c[s].data_ptr(), v_c[s].data_ptr()))
+            maxlen.append(k_c.shape[1])
+        else:
+            pairs.append((k[h].data_ptr(), v[h].data_ptr()))
+            maxlen.append(seq.n)
+    plan = ck.decode_plan(np.array(maxlen), wl.hq, wl.hkv, DEV)
+    q_st = synth.decode_queries(wl, 0)
+    out, lse = ck.decode_attn(plan, to_dev(q_st), ck.kv_table(pairs, DEV), lens)
+    kc_ref, vc_ref = O.compact_kv(f64(seq.k), f64(seq.v), heads, idx_ref, wl.cs, wl.l_obs)
+    views = [(kc_ref[heads.index(h)], vc_ref[heads.index(h)]) if h in heads else (f64(seq.k[h]), f64(seq.v[h]))
+             for h in range(wl.hkv)]
+    o_ref, l_ref = O.decode_gqa(f64(q_st)[0], views)
+    assert_rows_close(out.cpu().numpy()[0], o_ref, "f32")
+    np.testing.assert_allclose(lse.cpu().numpy()[0], l_ref, atol=1e-5)
