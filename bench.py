@@ -1,0 +1,322 @@
+"""Benchmark of the CateKV hybrid-KV decode path on one MI355X.
+
+Workload: one layer of Llama-3-8B-shaped attention (32 query heads, 8 KV
+heads, head dim 128) at 131072 tokens of bf16 context.  The prefill-side path
+runs first on the synthetic sequence -- CV head scores (64 window rows),
+Eq. 5 with adaptive ratio r = 0.4 (5 consistent heads), chunk selection with
+budget 2048 tokens (256 chunks of 8) and compaction -- and is timed on its
+own.  A timed step is then one hybrid decode step: every query head attends
+over its full cache (adaptive heads) or its 2112-row compact cache
+(consistent heads).  Steps rotate over several copies of the layer's caches so
+that the 256 MB Infinity Cache cannot serve a step from the previous one, as
+in a multi-layer model.
+
+Prints one JSON line: value = achieved HBM bandwidth on the algorithmic bytes
+of a decode step (K/V rows read + q + fp32 out), with the roofline of the
+decode kernel and the CPU oracle's rate on a bounded sample.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+BF16_MFMA_PEAK_TFLOPS = 2500.0
+METRIC = "hybrid decode-attn µs/step + achieved HBM GB/s (% peak) at 128K ctx, 1 GPU"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=100)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--workload", default="ctx128k_bf16")
+    p.add_argument("--layers", type=int, default=0, help="layer copies to rotate over (0: >= 1.2 GB of KV)")
+    p.add_argument("--split", type=int, default=0, help="decode split tokens (0: library default)")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=15.0)
+    p.add_argument("--no-graph", action="store_true", help="launch steps eagerly instead of a HIP graph")
+    return p.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: the hybrid decode path is built and timed on a single "
+              f"MI355X (requested --gpus {args.gpus}); run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2608_30295_amd as ck
+    import synth
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = synth.WORKLOADS[args.workload]
+    if wl.batch != 1:
+        raise SystemExit("bench.py times single-sequence workloads")
+    t_gen = time.time()
+    seq = synth.make_sequence(wl)
+    log(f"[bench] generated {wl.name}: n={seq.n} in {time.time() - t_gen:.1f}s")
+
+    def dev_t(st):
+        if st.dtype == np.uint16:
+            return torch.from_numpy(np.ascontiguousarray(st).view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(np.ascontiguousarray(st)).to(dev)
+
+    n, hq, hkv, d, G = seq.n, wl.hq, wl.hkv, wl.d, wl.group
+    k_full, v_full = dev_t(seq.k), dev_t(seq.v)
+    q_obs, q_cv = dev_t(seq.q_obs), dev_t(seq.q_cv)
+    esz = wl.itemsize
+
+    # ---------------- prefill-side path: CV -> Eq. 5 -> select -> compact ----------------
+    cv_ws = ck.workspace(ck.score_heads_workspace(hq, hkv, q_cv.shape[1], n, wl.l_init, wl.l_rec), dev)
+    cv = ck.score_heads(q_cv, k_full, q_pos0=seq.q_cv_pos0, l_init=wl.l_init, l_rec=wl.l_rec,
+                        k_pct=wl.k_pct, alpha=wl.alpha, ws=cv_ws)
+    cv_h = cv.cpu().numpy()
+    cons = ck.classify_heads(cv_h[None], wl.r)
+    heads = [h for h in range(hkv) if cons[h]]
+    adaptive = [h for h in range(hkv) if not cons[h]]
+    b = wl.chunk_budget
+    sel_ws = ck.workspace(ck.select_workspace(hq, hkv, wl.l_obs, n, wl.cs, len(heads)), dev)
+    idx = ck.select_critical(q_obs, k_full, heads, wl.cs, b, ws=sel_ws)
+    lens = torch.full((hkv,), n, dtype=torch.int64, device=dev)
+    k_c, v_c = ck.compact_kv(k_full, v_full, heads, idx, wl.cs, wl.l_obs, lens)
+    torch.cuda.synchronize()
+    lens_h = lens.cpu().numpy()
+    log(f"[bench] cv={np.round(cv_h, 3).tolist()} consistent={heads} lens={lens_h.tolist()}")
+
+    stream = torch.cuda.current_stream(dev)
+
+    def time_it(fn, reps):
+        fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        e1.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / reps     # us
+
+    reps = 5
+    t_cv = time_it(lambda: ck.score_heads(q_cv, k_full, q_pos0=seq.q_cv_pos0, l_init=wl.l_init, l_rec=wl.l_rec,
+                                          k_pct=wl.k_pct, alpha=wl.alpha, ws=cv_ws), reps)
+    idx_out = torch.empty_like(idx)
+    from paper_2608_30295_amd import _lib
+    from paper_2608_30295_amd._lib import check, lib
+    harr = (_lib.ctypes.c_int32 * len(heads))(*heads)
+
+    def run_select():
+        check(lib().catekv_select_critical(1 if wl.dtype == "bf16" else 0, q_obs.data_ptr(), k_full.data_ptr(),
+                                           hq, hkv, wl.l_obs, n, d, wl.cs, harr, len(heads), b, idx_out.data_ptr(),
+                                           sel_ws.data_ptr(), sel_ws.numel(), stream.cuda_stream))
+    t_sel = time_it(run_select, reps)
+    lens2 = lens.clone()
+    t_cmp = time_it(lambda: ck.compact_kv(k_full, v_full, heads, idx, wl.cs, wl.l_obs, lens2, out=(k_c, v_c)), reps)
+    n_keys = n - wl.l_obs
+    sel_flops = 2.0 * len(heads) * G * wl.l_obs * n_keys * d             # one Q K^T over the selection range
+    sel_bytes = len(heads) * n_keys * d * esz + 2 * int(sum(lens_h[h] for h in heads)) * d * esz * 2
+    sel_roof_us = max(sel_flops / (BF16_MFMA_PEAK_TFLOPS * 1e12), sel_bytes / (HBM_PEAK_GBS * 1e9)) * 1e6
+
+    # ---------------- decode: layer copies, plan, kv tables ----------------
+    view_len = [int(lens_h[h]) if h in heads else n for h in range(hkv)]
+    kv_bytes_layer = sum(view_len) * d * esz * 2
+    n_layers = args.layers or max(2, math.ceil(1.2e9 / kv_bytes_layer))
+    layers = []
+    for li in range(n_layers):
+        ka = k_full[adaptive].clone() if li else k_full[adaptive].contiguous()
+        va = v_full[adaptive].clone() if li else v_full[adaptive].contiguous()
+        kc = k_c.clone() if li else k_c
+        vc = v_c.clone() if li else v_c
+        pairs = []
+        for h in range(hkv):
+            if h in heads:
+                s = heads.index(h)
+                pairs.append((kc[s].data_ptr(), vc[s].data_ptr()))
+            else:
+                a = adaptive.index(h)
+                pairs.append((ka[a].data_ptr(), va[a].data_ptr()))
+        layers.append((ka, va, kc, vc, ck.kv_table(pairs, dev)))
+    del k_full, v_full
+    torch.cuda.empty_cache()
+    max_len = np.array([[view_len[h] for h in range(hkv)]], dtype=np.int64)
+    plan = ck.decode_plan(max_len, hq, hkv, dev, split_tokens=args.split)
+    nq = 16
+    qs = [dev_t(synth.decode_queries(wl, t)) for t in range(nq)]
+    out = torch.empty((1, hq, d), dtype=torch.float32, device=dev)
+    lse = torch.empty((1, hq), dtype=torch.float32, device=dev)
+    dtc = 1 if wl.dtype == "bf16" else 0
+    scale = 1.0 / math.sqrt(d)
+    pl = plan.plan
+    ws_ptr, ws_n = plan.ws.data_ptr(), plan.ws.numel()
+
+    def step(t):
+        _, _, _, _, table = layers[t % n_layers]
+        check(lib().catekv_decode_attn(dtc, _lib.ctypes.byref(pl), qs[t % nq].data_ptr(), table.data_ptr(),
+                                       lens.data_ptr(), 1, hq, hkv, d, scale, out.data_ptr(), lse.data_ptr(),
+                                       ws_ptr, ws_n, stream.cuda_stream))
+
+    algo_bytes = kv_bytes_layer + hq * d * esz + hq * d * 4
+    full_bytes = n * hkv * d * esz * 2 + hq * d * esz + hq * d * 4
+
+    for t in range(args.warmup):
+        step(t)
+    torch.cuda.synchronize()
+
+    mode = "eager"
+    graph = None
+    if not args.no_graph:
+        # one graph holds a full rotation of steps; replays are checked against eager results
+        try:
+            cap_steps = n_layers * nq // math.gcd(n_layers, nq)
+            cap_steps = min(cap_steps, 64)
+            ref = []
+            for t in range(cap_steps):
+                step(t)
+                ref.append(out.clone())
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            s2 = torch.cuda.Stream(device=dev)
+            s2.wait_stream(stream)
+
+            def step_on(t, st):
+                _, _, _, _, table = layers[t % n_layers]
+                check(lib().catekv_decode_attn(dtc, _lib.ctypes.byref(pl), qs[t % nq].data_ptr(),
+                                               table.data_ptr(), lens.data_ptr(), 1, hq, hkv, d, scale,
+                                               out.data_ptr(), lse.data_ptr(), ws_ptr, ws_n, st.cuda_stream))
+
+            with torch.cuda.stream(s2):
+                g.capture_begin()
+                for t in range(cap_steps):
+                    step_on(t, s2)
+                g.capture_end()
+            stream.wait_stream(s2)
+            torch.cuda.synchronize()
+            ok = True
+            for rep in range(3):
+                g.replay()
+                torch.cuda.synchronize()
+                ok = ok and torch.equal(out, ref[-1])
+                step(rep)                      # eager work between replays
+                torch.cuda.synchronize()
+                ok = ok and torch.equal(out, ref[rep])
+            if ok:
+                graph, mode = (g, cap_steps), "hip_graph"
+            else:
+                log("[bench] graph replay disagreed with eager launches; timing eagerly")
+        except Exception as e:   # graph capture unavailable: time eagerly
+            log(f"[bench] graph capture failed ({e}); timing eagerly")
+            graph = None
+
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    if graph is None:
+        e0.record(stream)
+        for t in range(args.steps):
+            step(t)
+        e1.record(stream)
+        timed_steps = args.steps
+    else:
+        g, cap_steps = graph
+        n_rep = max(1, round(args.steps / cap_steps))
+        e0.record(stream)
+        for _ in range(n_rep):
+            g.replay()
+        e1.record(stream)
+        timed_steps = n_rep * cap_steps
+    e1.synchronize()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / timed_steps
+    gbs = algo_bytes / (us * 1e-6) / 1e9
+    log(f"[bench] decode {mode}: {us:.2f} us/step over {timed_steps} steps, {gbs:.1f} GB/s "
+        f"({100 * gbs / HBM_PEAK_GBS:.1f}% of 8 TB/s), {n_layers} layer copies")
+
+    # ---------------- CPU oracle on a bounded sample ----------------
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle as O
+        f64 = synth.storage_to_f64
+        t0 = time.time()
+        views = []
+        kc_h = k_c.view(torch.int16).cpu().numpy().view(np.uint16) if wl.dtype == "bf16" else k_c.cpu().numpy()
+        vc_h = v_c.view(torch.int16).cpu().numpy().view(np.uint16) if wl.dtype == "bf16" else v_c.cpu().numpy()
+        for h in range(hkv):
+            if h in heads:
+                s = heads.index(h)
+                views.append((f64(kc_h[s][:view_len[h]]), f64(vc_h[s][:view_len[h]])))
+            else:
+                views.append((f64(seq.k[h]), f64(seq.v[h])))
+        log(f"[bench] oracle inputs widened in {time.time() - t0:.1f}s")
+        done, t_start = 0, time.perf_counter()
+        while True:
+            O.decode_gqa(f64(synth.decode_queries(wl, done))[0], views)
+            done += 1
+            if time.perf_counter() - t_start > args.cpu_seconds:
+                break
+        cpu_us = (time.perf_counter() - t_start) * 1e6 / done
+        try:
+            import threadpoolctl
+            blas = [(i.get("internal_api"), i.get("num_threads")) for i in threadpoolctl.threadpool_info()]
+        except Exception:
+            blas = []
+        threads = max([t for _, t in blas if t] or [1])
+        cpu = {"value": round(algo_bytes / (cpu_us * 1e-6) / 1e9, 3), "unit": "GB/s", "cores": threads,
+               "kind": "oracle", "us_per_step": round(cpu_us, 1),
+               "host_cores_available": len(os.sched_getaffinity(0)), "blas": blas,
+               "sample": f"{done} decode steps of the same 128K hybrid cache (fp64 NumPy oracle, "
+                         f"{args.cpu_seconds:.0f}s budget; inputs widened to fp64 outside the timing)"}
+
+    res = {
+        "metric": METRIC,
+        "value": round(gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": timed_steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(us / 1e3, 5),
+        "us_per_step": round(us, 2),
+        "hbm_peak_frac": round(gbs / HBM_PEAK_GBS, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded N(0,1) K/V/Q with 1% heavy-hitter keys scaled x3)",
+        "config": {
+            "workload": wl.name, "context": n, "batch": 1, "hq": hq, "hkv": hkv, "head_dim": d,
+            "consistent_heads": heads, "chunk_budget": b, "chunk_size": wl.cs, "l_obs": wl.l_obs,
+            "view_lengths": view_len, "layer_copies": n_layers, "launch": mode,
+            "split_tokens": int(plan.plan.split_tokens), "work_items": int(plan.plan.n_items),
+            "algorithmic_bytes_per_step": int(algo_bytes), "full_attention_bytes_per_step": int(full_bytes),
+            "kv_fraction_of_full": round(kv_bytes_layer / (n * hkv * d * esz * 2), 4),
+        },
+        "roofline": {
+            "kernel": "decode_kernel<bf16,G=4>", "bound": "hbm", "achieved": round(gbs, 2),
+            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+        },
+        "prefill": {
+            "score_heads_us": round(t_cv, 1),
+            "select_critical_us": round(t_sel, 1),
+            "compact_kv_us": round(t_cmp, 1),
+            "select_roofline_us": round(sel_roof_us, 1),
+            "select_plus_compact_vs_roofline": round((t_sel + t_cmp) / sel_roof_us, 3),
+            "select_tflops": round(sel_flops / (t_sel * 1e-6) / 1e12, 1),
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -68,8 +68,8 @@ typedef struct catekv_kv_ptrs {
 typedef struct catekv_decode_plan_t {
   uint64_t magic;
   int32_t batch, hq, hkv, split_tokens;
-  int32_t n_items, n_slots, reserved0, reserved1;
-  uint64_t items_off, bh_off, counters_off, partials_off, ws_bytes;
+  int32_t n_items, n_slots, n_multi, reserved1;
+  uint64_t items_off, views_off, reserved2, partials_off, ws_bytes;
   int64_t max_len_total;
 } catekv_decode_plan_t;
 

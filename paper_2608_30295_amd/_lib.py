@@ -29,9 +29,9 @@ class DecodePlanT(ctypes.Structure):
         ("batch", ctypes.c_int32), ("hq", ctypes.c_int32), ("hkv", ctypes.c_int32),
         ("split_tokens", ctypes.c_int32),
         ("n_items", ctypes.c_int32), ("n_slots", ctypes.c_int32),
-        ("reserved0", ctypes.c_int32), ("reserved1", ctypes.c_int32),
-        ("items_off", ctypes.c_uint64), ("bh_off", ctypes.c_uint64),
-        ("counters_off", ctypes.c_uint64), ("partials_off", ctypes.c_uint64),
+        ("n_multi", ctypes.c_int32), ("reserved1", ctypes.c_int32),
+        ("items_off", ctypes.c_uint64), ("views_off", ctypes.c_uint64),
+        ("reserved2", ctypes.c_uint64), ("partials_off", ctypes.c_uint64),
         ("ws_bytes", ctypes.c_uint64),
         ("max_len_total", ctypes.c_int64),
     ]

@@ -12,7 +12,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/catekv.h"
+#include "catekv.h"
 #include "internal.h"
 
 namespace {
@@ -82,9 +82,25 @@ int default_split(const int64_t* max_len, int n_views) {
   return (int)std::max<int64_t>(256, std::min<int64_t>(s, 1 << 20));
 }
 
+// Split of one view: the requested split, raised so that no view needs more
+// partials than the combine kernel merges.
+int64_t view_split(int64_t L, int split) {
+  const int64_t maxp = catekv::decode_max_parts();
+  int64_t s = split;
+  if ((L + s - 1) / s > maxp) {
+    s = (L + maxp - 1) / maxp;
+    s = ((s + kSplitQuantum - 1) / kSplitQuantum) * kSplitQuantum;
+  }
+  return s;
+}
+
+int view_parts(int64_t L, int split) {
+  return L <= 0 ? 1 : (int)((L + view_split(L, split) - 1) / view_split(L, split));
+}
+
 struct PlanShape {
-  int n_items = 0, n_slots = 0, n_gslots = 0, n_gcounters = 0;
-  size_t items_off = 0, views_off = 0, counters_off = 0, slots_off = 0, gslots_off = 0, total = 0;
+  int n_items = 0, n_slots = 0, n_multi = 0;
+  size_t items_off = 0, views_off = 0, slots_off = 0, total = 0;
 };
 
 size_t a256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -92,23 +108,16 @@ size_t a256(size_t x) { return (x + 255) & ~(size_t)255; }
 PlanShape plan_shape(const int64_t* max_len, int n_views, int G, int split) {
   PlanShape P;
   for (int v = 0; v < n_views; ++v) {
-    const int64_t L = max_len[v];
-    const int parts = L <= 0 ? 1 : (int)((L + split - 1) / split);
-    const int groups = (parts + catekv::kMergeGroup - 1) / catekv::kMergeGroup;
+    const int parts = view_parts(max_len[v], split);
     P.n_items += parts;
     P.n_slots += parts;
-    if (groups > 1) {
-      P.n_gslots += groups;
-      P.n_gcounters += groups;
-    }
+    P.n_multi += parts > 1;
   }
   const size_t sf = catekv::decode_slot_floats(G) * sizeof(float);
   size_t o = 0;
   P.items_off = o; o += a256((size_t)P.n_items * sizeof(catekv::DecodeItem));
   P.views_off = o; o += a256((size_t)n_views * sizeof(catekv::ViewInfo));
-  P.counters_off = o; o += a256((size_t)(n_views + P.n_gcounters) * sizeof(int32_t));
   P.slots_off = o; o += a256((size_t)P.n_slots * sf);
-  P.gslots_off = o; o += a256((size_t)std::max(P.n_gslots, 1) * sf);
   P.total = o;
   return P;
 }
@@ -312,30 +321,21 @@ int catekv_decode_plan(const int64_t* max_len_host, int batch, int hq, int hkv, 
   std::vector<catekv::DecodeItem> items;
   items.reserve(P.n_items);
   std::vector<catekv::ViewInfo> views(nv);
-  int slot = 0, gslot = 0, gctr = 0;
+  int slot = 0;
   int64_t total = 0;
   for (int v = 0; v < nv; ++v) {
     const int64_t L = max_len_host[v];
     total += L;
-    const int parts = L <= 0 ? 1 : (int)((L + split - 1) / split);
-    const int groups = (parts + catekv::kMergeGroup - 1) / catekv::kMergeGroup;
-    catekv::ViewInfo& vi = views[v];
-    std::memset(&vi, 0, sizeof vi);
-    vi.first_slot = slot;
-    vi.n_parts = parts;
-    vi.n_groups = groups;
-    vi.first_gslot = groups > 1 ? gslot : -1;
-    vi.gcounter = groups > 1 ? gctr : -1;
+    const int parts = view_parts(L, split);
+    const int64_t vs = view_split(L, split);
+    views[v].first_slot = slot;
+    views[v].n_parts = parts;
     for (int p = 0; p < parts; ++p) {
-      const int64_t t0 = (int64_t)p * split;
-      const int64_t t1 = std::min<int64_t>(L, t0 + split);
+      const int64_t t0 = (int64_t)p * vs;
+      const int64_t t1 = std::min<int64_t>(L, t0 + vs);
       items.push_back({v, p, (int32_t)t0, (int32_t)std::max<int64_t>(t0, t1)});
     }
     slot += parts;
-    if (groups > 1) {
-      gslot += groups;
-      gctr += groups;
-    }
   }
   // largest items first so that short consistent-head items fill the tail
   std::stable_sort(items.begin(), items.end(), [](const catekv::DecodeItem& a, const catekv::DecodeItem& b) {
@@ -345,7 +345,6 @@ int catekv_decode_plan(const int64_t* max_len_host, int batch, int hq, int hkv, 
   std::vector<unsigned char> host(P.slots_off, 0);
   std::memcpy(host.data() + P.items_off, items.data(), items.size() * sizeof(catekv::DecodeItem));
   std::memcpy(host.data() + P.views_off, views.data(), views.size() * sizeof(catekv::ViewInfo));
-  // counters stay zero
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   hipError_t e = hipMemcpyAsync(ws, host.data(), host.size(), hipMemcpyHostToDevice, s);
   if (e != hipSuccess) return hip_fail(e, "decode_plan upload");
@@ -360,15 +359,14 @@ int catekv_decode_plan(const int64_t* max_len_host, int batch, int hq, int hkv, 
   plan->split_tokens = split;
   plan->n_items = P.n_items;
   plan->n_slots = P.n_slots;
-  plan->reserved0 = P.n_gslots;
-  plan->reserved1 = P.n_gcounters;
+  plan->n_multi = P.n_multi;
+  plan->reserved1 = 0;
   plan->items_off = P.items_off;
-  plan->bh_off = P.views_off;
-  plan->counters_off = P.counters_off;
+  plan->views_off = P.views_off;
+  plan->reserved2 = 0;
   plan->partials_off = P.slots_off;
   plan->ws_bytes = P.total;
   plan->max_len_total = total;
-  (void)P.gslots_off;
   return ok();
 }
 
@@ -392,18 +390,15 @@ int catekv_decode_attn(int dtype, const catekv_decode_plan_t* plan, const void* 
   a.kv = kv;
   a.lens = lens;
   a.items = reinterpret_cast<const catekv::DecodeItem*>(w + plan->items_off);
-  a.views = reinterpret_cast<const catekv::ViewInfo*>(w + plan->bh_off);
-  a.counters = reinterpret_cast<int*>(w + plan->counters_off);
+  a.views = reinterpret_cast<const catekv::ViewInfo*>(w + plan->views_off);
   a.slots = reinterpret_cast<float*>(w + plan->partials_off);
-  const size_t sf = catekv::decode_slot_floats(hq / hkv) * sizeof(float);
-  a.gslots = reinterpret_cast<float*>(w + plan->partials_off + a256((size_t)plan->n_slots * sf));
   a.n_items = plan->n_items;
   a.n_views = batch * hkv;
   a.hkv = hkv;
   a.scale = scale;
   a.out = out;
   a.lse = lse;
-  hipError_t e = catekv::launch_decode(dtype, hq / hkv, a, reinterpret_cast<hipStream_t>(stream));
+  hipError_t e = catekv::launch_decode(dtype, hq / hkv, a, plan->n_multi > 0, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "decode_attn launch");
   return ok();
 }

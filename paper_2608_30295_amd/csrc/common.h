@@ -58,7 +58,15 @@ __device__ __forceinline__ float shfl_xor(float x, int mask) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// 16-byte global load that the compiler keeps as one dwordx4.
+// 16-byte load that the compiler keeps as one dwordx4.
 __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+
+// 16-byte load through the global address space (a global_load_dwordx4, not a
+// flat load), for pointers the compiler cannot prove global by itself.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 ldg16(const void* p) {
+  const u32x4_t v = *(const __attribute__((address_space(1))) u32x4_t*)(p);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
 
 }  // namespace catekv

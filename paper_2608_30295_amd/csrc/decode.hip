@@ -5,13 +5,15 @@
 // the host plan.  One workgroup handles one item for all G query heads of
 // the group, so each K/V row is read from HBM exactly once per step.
 //
-// Layout inside a wave: 8 lanes share one token row (each lane owns 16 of the
-// 128 dims, fetched as 16-byte loads), so a wave covers 8 tokens per load
-// instruction.  q.k partial sums are reduced over the 8 lanes with DPP.  Each
-// group of 8 lanes keeps its own online-softmax state (running max m, sum l,
-// unnormalised o); the states are merged across groups and waves at the end,
-// and across items by the last-arriving workgroup of the view (atomic
-// counter), which writes the normalised output and its log-sum-exp.
+// Streaming kernel: 8 lanes share one token row (each lane owns 16 of the 128
+// dims, fetched as 16-byte loads), so one wave covers 8 tokens per load
+// instruction.  Loads run NS stages ahead of use in a register ring.  q.k
+// partial sums are reduced over the 8 lanes with DPP; each group of 8 lanes
+// keeps its own online-softmax state (running max m, sum l, unnormalised o),
+// merged across groups and waves at the end.  An item that covers its whole
+// view writes the normalised output directly; otherwise it writes a partial
+// (o, m, l) that the combine kernel merges with the view's other partials
+// (log-sum-exp weighting).  No cross-workgroup synchronisation is needed.
 #include "common.h"
 #include "internal.h"
 
@@ -33,7 +35,7 @@ struct Row {
 template <typename T>
 __device__ __forceinline__ void load_row(Row<T>& r, const T* row, int j) {
 #pragma unroll
-  for (int p = 0; p < Row<T>::NP; ++p) r.w[p] = ld16(row + (p * 8 + j) * Row<T>::NV);
+  for (int p = 0; p < Row<T>::NP; ++p) r.w[p] = ldg16(row + (p * 8 + j) * Row<T>::NV);
 }
 
 // 16 fp32 values of the row owned by this lane.
@@ -119,44 +121,11 @@ __device__ __forceinline__ int dim_of(int j, int e) {
   return ((e / NV) * 8 + j) * NV + (e % NV);
 }
 
-// Merge `cnt` partial slots (stride SF floats) for output element (g, e):
-// returns the merged unnormalised o, the sum l and the max m (natural-log units).
-template <int G>
-__device__ __forceinline__ void merge_slots(const float* src, int cnt, int g, int e, float& M,
-                                            float& L, float& Ov) {
-  constexpr int SF = G * kD + 2 * G;
-  M = -INFINITY;
-  for (int s = 0; s < cnt; ++s) M = fmaxf(M, src[s * SF + G * kD + g]);
-  L = 0.f;
-  Ov = 0.f;
-  for (int s = 0; s < cnt; ++s) {
-    const float ms = src[s * SF + G * kD + g];
-    const float cw = ms == -INFINITY ? 0.f : fast_exp2((ms - M) * kLog2e);
-    L += src[s * SF + G * kD + G + g] * cw;
-    Ov += src[s * SF + g * kD + e] * cw;
-  }
-}
-
-template <int G>
-__device__ __forceinline__ void emit(float* out, float* lse, size_t row, int e, float M, float L, float Ov) {
-  out[row * kD + e] = L > 0.f ? Ov / L : 0.f;
-  if (lse && e == 0) lse[row] = L > 0.f ? M + logf(L) : -INFINITY;
-}
-
-template <int G>
-__device__ __forceinline__ void put_slot(float* slot, int g, int e, float M, float L, float Ov) {
-  slot[g * kD + e] = Ov;
-  if (e == 0) {
-    slot[G * kD + g] = L > 0.f ? M : -INFINITY;
-    slot[G * kD + G + g] = L;
-  }
-}
-
-template <typename T, int G, int WAVES, int U>
-__global__ __launch_bounds__(WAVES * 64) void decode_kernel(DecodeArgs a) {
-  constexpr int TOK_IT = 8 * U;                 // tokens per wave iteration
+template <typename T, int G, int WAVES, int NS>
+__global__ __launch_bounds__(WAVES * 64) void decode_split_kernel(DecodeArgs a) {
   constexpr int SF = G * kD + 2 * G;            // floats per partial slot
   constexpr int NT = WAVES * 64;
+  constexpr int TPW = 8;                        // tokens per wave per stage
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int j = lane & 7;                       // lane within the token group
@@ -168,6 +137,7 @@ __global__ __launch_bounds__(WAVES * 64) void decode_kernel(DecodeArgs a) {
   const int b = bh / hkv, h = bh - b * hkv;
   const catekv_kv_ptrs view = a.kv[bh];
   int64_t len = a.lens[bh];
+  const ViewInfo vi = a.views[bh];
   len = len < 0 ? 0 : len;
   const int t0 = it.t0;
   const int t_end = (int)((int64_t)it.t1 < len ? (int64_t)it.t1 : len);
@@ -191,47 +161,33 @@ __global__ __launch_bounds__(WAVES * 64) void decode_kernel(DecodeArgs a) {
     for (int e = 0; e < 16; ++e) o[g][e] = 0.f;
   }
 
+  // stage s of wave w covers tokens t0 + (s * WAVES + w) * 8 + [0, 8)
   const int ntok = t_end > t0 ? t_end - t0 : 0;
-  const int n_it = (ntok + TOK_IT * WAVES - 1) / (TOK_IT * WAVES);
-  // raw-unit slack before the running max is refreshed (2^8 headroom in p)
-  const float thr = 8.0f / c;
+  const int n_st = (ntok + TPW * WAVES - 1) / (TPW * WAVES);
+  const float thr = 8.0f / c;                   // raw-unit slack before the running max is refreshed
 
-  Row<T> kb[2][U], vb[2][U];
-  auto issue = [&](int buf, int iter) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      int tok = t0 + (iter * WAVES + wave) * TOK_IT + u * 8 + gi;
-      tok = tok < t_end ? tok : t0;               // masked rows re-read a valid row
-      load_row(kb[buf][u], kbase + (size_t)tok * kD, j);
-      load_row(vb[buf][u], vbase + (size_t)tok * kD, j);
-    }
+  Row<T> kb[NS], vb[NS];
+  auto issue = [&](int buf, int st) {
+    int tok = t0 + (st * WAVES + wave) * TPW + gi;
+    tok = tok < t_end ? tok : t0;               // rows past the end re-read a valid row
+    load_row(kb[buf], kbase + (size_t)tok * kD, j);
+    load_row(vb[buf], vbase + (size_t)tok * kD, j);
   };
-  auto consume = [&](int buf, int iter) {
-    float s[U][G];
-    bool valid[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int tok = t0 + (iter * WAVES + wave) * TOK_IT + u * 8 + gi;
-      valid[u] = tok < t_end;
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        const float x = sum8(qf[g].dot(kb[buf][u]));
-        s[u][g] = valid[u] ? x : -INFINITY;
-      }
-    }
+  auto consume = [&](int buf, int st) {
+    const int tok = t0 + (st * WAVES + wave) * TPW + gi;
+    const bool valid = tok < t_end;
+    float s[G];
     bool need = false;
-    float mt[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      mt[g] = s[0][g];
-#pragma unroll
-      for (int u = 1; u < U; ++u) mt[g] = fmaxf(mt[g], s[u][g]);
-      need |= mt[g] > m[g] + thr;
+      const float x = sum8(qf[g].dot(kb[buf]));
+      s[g] = valid ? x : -INFINITY;
+      need |= s[g] > m[g] + thr;
     }
     if (__builtin_amdgcn_ballot_w64(need)) {
 #pragma unroll
       for (int g = 0; g < G; ++g) {
-        const float nm = fmaxf(m[g], mt[g]);
+        const float nm = fmaxf(m[g], s[g]);
         if (nm > m[g]) {
           const float corr = m[g] == -INFINITY ? 0.f : fast_exp2((m[g] - nm) * c);
           l[g] *= corr;
@@ -241,28 +197,29 @@ __global__ __launch_bounds__(WAVES * 64) void decode_kernel(DecodeArgs a) {
         }
       }
     }
+    float vf[16];
+    row_to_f32(vb[buf], vf);
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      float vf[16];
-      row_to_f32(vb[buf][u], vf);
+    for (int g = 0; g < G; ++g) {
+      const float p = valid ? fast_exp2(__builtin_fmaf(s[g], c, -m[g] * c)) : 0.f;
+      l[g] += p;
 #pragma unroll
-      for (int g = 0; g < G; ++g) {
-        const float p = valid[u] ? fast_exp2(__builtin_fmaf(s[u][g], c, -m[g] * c)) : 0.f;
-        l[g] += p;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) o[g][e] = __builtin_fmaf(p, vf[e], o[g][e]);
-      }
+      for (int e = 0; e < 16; ++e) o[g][e] = __builtin_fmaf(p, vf[e], o[g][e]);
     }
   };
 
-  if (n_it > 0) {
-    issue(0, 0);
-    for (int iter = 0; iter < n_it; iter += 2) {
-      if (iter + 1 < n_it) issue(1, iter + 1);
-      consume(0, iter);
-      if (iter + 1 < n_it) {
-        if (iter + 2 < n_it) issue(0, iter + 2);
-        consume(1, iter + 1);
+  if (n_st > 0) {
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s)
+      if (s < n_st) issue(s, s);
+    for (int base = 0; base < n_st; base += NS) {
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        const int st = base + s;
+        if (st < n_st) {
+          if (st + NS - 1 < n_st) issue((s + NS - 1) % NS, st + NS - 1);
+          consume(s, st);
+        }
       }
     }
   }
@@ -294,7 +251,6 @@ __global__ __launch_bounds__(WAVES * 64) void decode_kernel(DecodeArgs a) {
   // ---- merge the waves through LDS -----------------------------------------
   __shared__ float s_o[WAVES][G][kD];
   __shared__ float s_m[WAVES][G], s_l[WAVES][G];
-  __shared__ int s_flag;
   if (gi == 0) {
 #pragma unroll
     for (int g = 0; g < G; ++g) {
@@ -308,7 +264,6 @@ __global__ __launch_bounds__(WAVES * 64) void decode_kernel(DecodeArgs a) {
   }
   __syncthreads();
 
-  const ViewInfo vi = a.views[bh];
   const size_t row0 = (size_t)b * hq + (size_t)h * G;
   float* slot = a.slots + (size_t)(vi.first_slot + it.part) * SF;
   for (int t = threadIdx.x; t < G * kD; t += NT) {
@@ -324,67 +279,112 @@ __global__ __launch_bounds__(WAVES * 64) void decode_kernel(DecodeArgs a) {
       Ov += s_o[w][g][e] * cw;
     }
     const float Mn = M * scale;                 // natural-log units of the scaled score
-    if (vi.n_parts == 1) emit<G>(a.out, a.lse, row0 + g, e, Mn, L, Ov);
-    else put_slot<G>(slot, g, e, Mn, L, Ov);
+    if (vi.n_parts == 1) {
+      a.out[(row0 + g) * kD + e] = L > 0.f ? Ov / L : 0.f;
+      if (a.lse && e == 0) a.lse[row0 + g] = L > 0.f ? Mn + logf(L) : -INFINITY;
+    } else {
+      slot[g * kD + e] = Ov;
+      if (e == 0) {
+        slot[G * kD + g] = L > 0.f ? Mn : -INFINITY;
+        slot[G * kD + G + g] = L;
+      }
+    }
   }
-  if (vi.n_parts == 1) return;
+}
 
-  // ---- level 1: the last item of a merge group merges the group -----------
-  const int grp = it.part / kMergeGroup;
-  const int g_first = grp * kMergeGroup;
-  const int g_cnt = min(kMergeGroup, vi.n_parts - g_first);
-  const bool single_group = vi.n_groups == 1;
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int* ctr = single_group ? &a.counters[bh] : &a.counters[a.n_views + vi.gcounter + grp];
-    s_flag = atomicAdd(ctr, 1) == g_cnt - 1;
-    if (s_flag) *ctr = 0;                       // every member has arrived: reset for the next step
-  }
-  __syncthreads();
-  if (!s_flag) return;
-  __threadfence();
-  const float* gsrc = a.slots + (size_t)(vi.first_slot + g_first) * SF;
-  float* gdst = single_group ? nullptr : a.gslots + (size_t)(vi.first_gslot + grp) * SF;
-  for (int t = threadIdx.x; t < G * kD; t += NT) {
-    const int g = t / kD, e = t - g * kD;
-    float M, L, Ov;
-    merge_slots<G>(gsrc, g_cnt, g, e, M, L, Ov);
-    if (single_group) emit<G>(a.out, a.lse, row0 + g, e, M, L, Ov);
-    else put_slot<G>(gdst, g, e, M, L, Ov);
-  }
-  if (single_group) return;
+// Merges the partials of every view cut into more than one item.  One
+// workgroup per (view, query head of the group): all (m, l) pairs go to LDS,
+// then 8 lanes of parts x 128 dims accumulate the weighted o.
+constexpr int kCombineThreads = 1024;
+constexpr int kCombineLanes = kCombineThreads / kD;   // parts handled in parallel per dim
+constexpr int kCombineMaxParts = 4096;
 
-  // ---- level 2: the last group of the view merges the group results -------
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    int* ctr = &a.counters[bh];
-    s_flag = atomicAdd(ctr, 1) == vi.n_groups - 1;
-    if (s_flag) *ctr = 0;
+template <int G>
+__global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(DecodeArgs a) {
+  constexpr int SF = G * kD + 2 * G;
+  const int bh = blockIdx.x / G, g = blockIdx.x - (blockIdx.x / G) * G;
+  const ViewInfo vi = a.views[bh];
+  const int P = vi.n_parts;
+  if (P <= 1) return;
+  __shared__ float s_w[kCombineMaxParts];
+  __shared__ float s_red[kCombineThreads / 64];
+  __shared__ float s_acc[kCombineLanes][kD];
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const float* base = a.slots + (size_t)vi.first_slot * SF;
+
+  // global max of the parts' m
+  float M = -INFINITY;
+  for (int s = t; s < P; s += kCombineThreads) {
+    const float ms = base[(size_t)s * SF + G * kD + g];
+    s_w[s] = ms;
+    M = fmaxf(M, ms);
   }
+  for (int off = 32; off > 0; off >>= 1) M = fmaxf(M, shfl_xor(M, off));
+  if (lane == 0) s_red[wave] = M;
   __syncthreads();
-  if (!s_flag) return;
-  __threadfence();
-  const float* vsrc = a.gslots + (size_t)vi.first_gslot * SF;
-  for (int t = threadIdx.x; t < G * kD; t += NT) {
-    const int g = t / kD, e = t - g * kD;
-    float M, L, Ov;
-    merge_slots<G>(vsrc, vi.n_groups, g, e, M, L, Ov);
-    emit<G>(a.out, a.lse, row0 + g, e, M, L, Ov);
+  M = s_red[0];
+#pragma unroll
+  for (int w = 1; w < kCombineThreads / 64; ++w) M = fmaxf(M, s_red[w]);
+  __syncthreads();
+  // weights w_s = exp(m_s - M) and L = sum w_s l_s
+  float L = 0.f;
+  for (int s = t; s < P; s += kCombineThreads) {
+    const float ms = s_w[s];
+    const float w = ms == -INFINITY ? 0.f : fast_exp2((ms - M) * kLog2e);
+    s_w[s] = w;
+    L += w * base[(size_t)s * SF + G * kD + G + g];
+  }
+  for (int off = 32; off > 0; off >>= 1) L += shfl_xor(L, off);
+  if (lane == 0) s_red[wave] = L;
+  __syncthreads();
+  L = 0.f;
+#pragma unroll
+  for (int w = 0; w < kCombineThreads / 64; ++w) L += s_red[w];
+
+  // o = sum_s w_s o_s
+  const int e = t % kD, pl = t / kD;
+  float acc = 0.f;
+  constexpr int UNR = 8;
+  for (int s0 = pl; s0 < P; s0 += kCombineLanes * UNR) {
+    float v[UNR];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int s = s0 + u * kCombineLanes;
+      v[u] = s < P ? base[(size_t)s * SF + g * kD + e] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int s = s0 + u * kCombineLanes;
+      acc += s < P ? s_w[s] * v[u] : 0.f;
+    }
+  }
+  s_acc[pl][e] = acc;
+  __syncthreads();
+  if (t < kD) {
+    float o = 0.f;
+#pragma unroll
+    for (int p = 0; p < kCombineLanes; ++p) o += s_acc[p][t];
+    const int hkv = a.hkv, b = bh / hkv, h = bh - b * hkv;
+    const size_t row = (size_t)b * hkv * G + (size_t)h * G + g;
+    a.out[row * kD + t] = L > 0.f ? o / L : 0.f;
+    if (a.lse && t == 0) a.lse[row] = L > 0.f ? M + logf(L) : -INFINITY;
   }
 }
 
 template <typename T, int G>
-static hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
-  constexpr int WAVES = 4, U = 2;
-  hipLaunchKernelGGL((decode_kernel<T, G, WAVES, U>), dim3(a.n_items), dim3(WAVES * 64), 0, stream, a);
+static hipError_t launch_t(const DecodeArgs& a, bool combine, hipStream_t stream) {
+  constexpr int WAVES = 4, NS = 4;
+  hipLaunchKernelGGL((decode_split_kernel<T, G, WAVES, NS>), dim3(a.n_items), dim3(WAVES * 64), 0, stream, a);
+  if (combine)
+    hipLaunchKernelGGL((decode_combine_kernel<G>), dim3(a.n_views * G), dim3(kCombineThreads), 0, stream, a);
   return hipGetLastError();
 }
 
-hipError_t launch_decode(int dtype, int G, const DecodeArgs& a, hipStream_t stream) {
+int decode_max_parts() { return kCombineMaxParts; }
+
+hipError_t launch_decode(int dtype, int G, const DecodeArgs& a, bool combine, hipStream_t stream) {
 #define CATEKV_DEC(T, GG) \
-  if (G == GG) return launch_t<T, GG>(a, stream);
+  if (G == GG) return launch_t<T, GG>(a, combine, stream);
   if (dtype == CATEKV_BF16) {
     CATEKV_DEC(uint16_t, 1) CATEKV_DEC(uint16_t, 2) CATEKV_DEC(uint16_t, 4) CATEKV_DEC(uint16_t, 8)
   } else {

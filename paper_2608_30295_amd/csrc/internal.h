@@ -6,7 +6,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
-#include "../../include/catekv.h"
+#include "catekv.h"
 
 namespace catekv {
 
@@ -21,18 +21,10 @@ struct DecodeItem {
   int32_t t1;
 };
 
-// Partials of a view are merged in groups of kMergeGroup by the last item of
-// each group to finish, then the group results by the last group.
-constexpr int kMergeGroup = 16;
-
-// Per view: where its partial slots, group slots and group counters live.
+// Per view: where its partial slots live and how many items cover it.
 struct ViewInfo {
   int32_t first_slot;     // slot of part 0
   int32_t n_parts;
-  int32_t first_gslot;    // group slot of group 0 (views with more than one group)
-  int32_t n_groups;
-  int32_t gcounter;       // index of group 0's counter in the counter array
-  int32_t pad[3];
 };
 
 // Floats per decode partial slot for a group of G query heads: o[G][128],
@@ -45,16 +37,15 @@ struct DecodeArgs {
   const int64_t* lens;
   const DecodeItem* items;
   const ViewInfo* views;
-  int* counters;          // [n_views] view counters, then group counters
   float* slots;           // partial slots
-  float* gslots;          // group slots
   int n_items, n_views, hkv;
   float scale;
   float* out;
   float* lse;
 };
 
-hipError_t launch_decode(int dtype, int G, const DecodeArgs& a, hipStream_t stream);
+int decode_max_parts();
+hipError_t launch_decode(int dtype, int G, const DecodeArgs& a, bool combine, hipStream_t stream);
 
 // ---- critical-token selection ------------------------------------------
 struct SelectGeom {
