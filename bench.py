@@ -297,7 +297,7 @@ def main():
             "workload": wl.name, "context": n, "batch": 1, "hq": hq, "hkv": hkv, "head_dim": d,
             "consistent_heads": heads, "chunk_budget": b, "chunk_size": wl.cs, "l_obs": wl.l_obs,
             "view_lengths": view_len, "layer_copies": n_layers, "launch": mode,
-            "split_tokens": int(plan.plan.split_tokens), "work_items": int(plan.plan.n_items),
+            "workgroups": int(plan.plan.n_workers), "segments": int(plan.plan.n_segments),
             "algorithmic_bytes_per_step": int(algo_bytes), "full_attention_bytes_per_step": int(full_bytes),
             "kv_fraction_of_full": round(kv_bytes_layer / (n * hkv * d * esz * 2), 4),
         },

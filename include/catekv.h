@@ -68,8 +68,8 @@ typedef struct catekv_kv_ptrs {
 typedef struct catekv_decode_plan_t {
   uint64_t magic;
   int32_t batch, hq, hkv, split_tokens;
-  int32_t n_items, n_slots, n_multi, reserved1;
-  uint64_t items_off, views_off, reserved2, partials_off, ws_bytes;
+  int32_t n_workers, n_segments, n_slots, n_multi;
+  uint64_t segs_off, workers_off, views_off, slots_off, ws_bytes;
   int64_t max_len_total;
 } catekv_decode_plan_t;
 
@@ -164,15 +164,20 @@ int catekv_compact_kv(int dtype, const void* k, const void* v, int hkv, int64_t 
 /* ------------------------------------------------------------------------ */
 
 /* Workspace bytes for a decode plan over max_len_host [batch][hkv].
- * split_tokens <= 0 picks the default split. */
+ * split_tokens is the number of tokens each decode workgroup streams; <= 0
+ * spreads all tokens over the workgroups the device holds at once. */
 size_t catekv_decode_workspace(const int64_t* max_len_host, int batch, int hq, int hkv,
                                int split_tokens);
 
 /* Builds the split-KV work list for upper-bound cache lengths
  * max_len_host [batch][hkv] (full length for adaptive heads, b cs + l_obs for
- * consistent heads), writes it into ws and fills *plan.  Blocks until the
- * upload has completed, so max_len_host may be reused on return.  The plan and
- * ws serve every later catekv_decode_attn call with the same shapes.
+ * consistent heads), writes it into ws and fills *plan.  All views are laid
+ * end to end and cut into equal shares, one per decode workgroup (by default
+ * the number of workgroups the current device runs at once), so long and
+ * short views balance across compute units.  Blocks until the upload has
+ * completed, so max_len_host may be reused on return.  The plan and ws serve
+ * every later catekv_decode_attn call with the same shapes; calls sharing a
+ * ws must not overlap in time.
  * Errors: INVALID_ARG for null pointers, batch < 1, negative lengths or a
  * length above 2^31 - 1; WORKSPACE if ws is too small; HIP on upload failure. */
 int catekv_decode_plan(const int64_t* max_len_host, int batch, int hq, int hkv,

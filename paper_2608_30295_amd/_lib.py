@@ -28,10 +28,10 @@ class DecodePlanT(ctypes.Structure):
         ("magic", ctypes.c_uint64),
         ("batch", ctypes.c_int32), ("hq", ctypes.c_int32), ("hkv", ctypes.c_int32),
         ("split_tokens", ctypes.c_int32),
-        ("n_items", ctypes.c_int32), ("n_slots", ctypes.c_int32),
-        ("n_multi", ctypes.c_int32), ("reserved1", ctypes.c_int32),
-        ("items_off", ctypes.c_uint64), ("views_off", ctypes.c_uint64),
-        ("reserved2", ctypes.c_uint64), ("partials_off", ctypes.c_uint64),
+        ("n_workers", ctypes.c_int32), ("n_segments", ctypes.c_int32), ("n_slots", ctypes.c_int32),
+        ("n_multi", ctypes.c_int32),
+        ("segs_off", ctypes.c_uint64), ("workers_off", ctypes.c_uint64), ("views_off", ctypes.c_uint64),
+        ("slots_off", ctypes.c_uint64),
         ("ws_bytes", ctypes.c_uint64),
         ("max_len_total", ctypes.c_int64),
     ]

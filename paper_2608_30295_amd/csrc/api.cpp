@@ -71,53 +71,73 @@ double quantile_linear(std::vector<double> x, double p) {
   return x[lo] + (h - (double)lo) * (x[hi] - x[lo]);
 }
 
-constexpr int kDefaultItems = 1024;   // aim for ~4 work items per compute unit
-constexpr int kSplitQuantum = 64;     // tokens one workgroup covers per loop trip
+// ---- decode plan: stream-K shares of the concatenated views ---------------
 
-int default_split(const int64_t* max_len, int n_views) {
-  int64_t tot = 0;
-  for (int i = 0; i < n_views; ++i) tot += max_len[i];
-  int64_t s = (tot + kDefaultItems - 1) / kDefaultItems;
-  s = ((s + kSplitQuantum - 1) / kSplitQuantum) * kSplitQuantum;
-  return (int)std::max<int64_t>(256, std::min<int64_t>(s, 1 << 20));
-}
+struct Segment {
+  int view, worker;
+  int64_t t0, t1;
+};
 
-// Split of one view: the requested split, raised so that no view needs more
-// partials than the combine kernel merges.
-int64_t view_split(int64_t L, int split) {
-  const int64_t maxp = catekv::decode_max_parts();
-  int64_t s = split;
-  if ((L + s - 1) / s > maxp) {
-    s = (L + maxp - 1) / maxp;
-    s = ((s + kSplitQuantum - 1) / kSplitQuantum) * kSplitQuantum;
-  }
-  return s;
-}
-
-int view_parts(int64_t L, int split) {
-  return L <= 0 ? 1 : (int)((L + view_split(L, split) - 1) / view_split(L, split));
-}
-
-struct PlanShape {
-  int n_items = 0, n_slots = 0, n_multi = 0;
-  size_t items_off = 0, views_off = 0, slots_off = 0, total = 0;
+struct PlanLayout {
+  int n_workers = 0, n_segments = 0, n_slots = 0, n_multi = 0;
+  size_t segs_off = 0, workers_off = 0, views_off = 0, slots_off = 0, total = 0;
+  std::vector<Segment> segs;   // grouped by worker
 };
 
 size_t a256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-PlanShape plan_shape(const int64_t* max_len, int n_views, int G, int split) {
-  PlanShape P;
+int device_workers(int G) {
+  int dev = 0, n_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n_cu < 1)
+    n_cu = 256;
+  return n_cu * catekv::decode_blocks_per_cu(CATEKV_BF16, G);
+}
+
+// Cuts the views (in index order, laid end to end in units of
+// kDecodeQuantum tokens) into n_workers near-equal shares.
+PlanLayout plan_layout(const int64_t* max_len, int n_views, int G, int split, int workers_hint) {
+  PlanLayout P;
+  const int64_t Q = catekv::kDecodeQuantum;
+  std::vector<int64_t> units(n_views);
+  int64_t U = 0;
   for (int v = 0; v < n_views; ++v) {
-    const int parts = view_parts(max_len[v], split);
-    P.n_items += parts;
-    P.n_slots += parts;
-    P.n_multi += parts > 1;
+    units[v] = (max_len[v] + Q - 1) / Q;
+    U += units[v];
+  }
+  int64_t W = split > 0 ? (U * Q + split - 1) / split : workers_hint;
+  W = std::max<int64_t>(1, std::min<int64_t>(W, std::max<int64_t>(U, 1)));
+  P.n_workers = (int)W;
+  int v = 0;
+  int64_t off = 0;   // units consumed of view v
+  for (int64_t w = 0; w < W; ++w) {
+    int64_t need = (w + 1) * U / W - w * U / W;
+    while (need > 0 && v < n_views) {
+      if (units[v] == 0) { ++v; off = 0; continue; }
+      const int64_t take = std::min(need, units[v] - off);
+      P.segs.push_back({v, (int)w, off * Q, std::min(max_len[v], (off + take) * Q)});
+      need -= take;
+      off += take;
+      if (off == units[v]) { ++v; off = 0; }
+    }
+  }
+  // empty views still produce an output (zeros and -inf): one empty segment each
+  for (int e = 0; e < n_views; ++e)
+    if (units[e] == 0) P.segs.push_back({e, (int)(e % W), 0, 0});
+  std::stable_sort(P.segs.begin(), P.segs.end(), [](const Segment& x, const Segment& y) { return x.worker < y.worker; });
+  P.n_segments = (int)P.segs.size();
+  std::vector<int> parts(n_views, 0);
+  for (const Segment& s : P.segs) parts[s.view]++;
+  for (int i = 0; i < n_views; ++i) {
+    P.n_slots += parts[i];
+    P.n_multi += parts[i] > 1;
   }
   const size_t sf = catekv::decode_slot_floats(G) * sizeof(float);
   size_t o = 0;
-  P.items_off = o; o += a256((size_t)P.n_items * sizeof(catekv::DecodeItem));
+  P.segs_off = o; o += a256((size_t)P.n_segments * sizeof(catekv::DecodeItem));
+  P.workers_off = o; o += a256((size_t)(P.n_workers + 1) * sizeof(int32_t));
   P.views_off = o; o += a256((size_t)n_views * sizeof(catekv::ViewInfo));
-  P.slots_off = o; o += a256((size_t)P.n_slots * sf);
+  P.slots_off = o; o += a256((size_t)std::max(P.n_slots, 1) * sf);
   P.total = o;
   return P;
 }
@@ -299,8 +319,7 @@ size_t catekv_decode_workspace(const int64_t* max_len_host, int batch, int hq, i
   const int nv = batch * hkv;
   for (int i = 0; i < nv; ++i)
     if (max_len_host[i] < 0 || max_len_host[i] > INT32_MAX) return 0;
-  const int split = split_tokens > 0 ? split_tokens : default_split(max_len_host, nv);
-  return plan_shape(max_len_host, nv, hq / hkv, split).total;
+  return plan_layout(max_len_host, nv, hq / hkv, split_tokens, device_workers(hq / hkv)).total;
 }
 
 int catekv_decode_plan(const int64_t* max_len_host, int batch, int hq, int hkv, int split_tokens,
@@ -312,38 +331,36 @@ int catekv_decode_plan(const int64_t* max_len_host, int batch, int hq, int hkv, 
   const int nv = batch * hkv;
   rc = check_lengths(max_len_host, nv);
   if (rc) return rc;
-  const int split = split_tokens > 0 ? split_tokens : default_split(max_len_host, nv);
+  if (!ws) return fail(CATEKV_ERR_WORKSPACE, "workspace pointer is null");
   const int G = hq / hkv;
-  const PlanShape P = plan_shape(max_len_host, nv, G, split);
+  const PlanLayout P = plan_layout(max_len_host, nv, G, split_tokens, device_workers(G));
   rc = check_ws(ws, ws_bytes, P.total);
   if (rc) return rc;
 
-  std::vector<catekv::DecodeItem> items;
-  items.reserve(P.n_items);
+  std::vector<catekv::DecodeItem> segs(P.n_segments);
+  std::vector<int32_t> wseg(P.n_workers + 1, 0);
   std::vector<catekv::ViewInfo> views(nv);
+  std::vector<int> parts(nv, 0);
+  for (const Segment& s : P.segs) parts[s.view]++;
   int slot = 0;
   int64_t total = 0;
   for (int v = 0; v < nv; ++v) {
-    const int64_t L = max_len_host[v];
-    total += L;
-    const int parts = view_parts(L, split);
-    const int64_t vs = view_split(L, split);
+    total += max_len_host[v];
     views[v].first_slot = slot;
-    views[v].n_parts = parts;
-    for (int p = 0; p < parts; ++p) {
-      const int64_t t0 = (int64_t)p * vs;
-      const int64_t t1 = std::min<int64_t>(L, t0 + vs);
-      items.push_back({v, p, (int32_t)t0, (int32_t)std::max<int64_t>(t0, t1)});
-    }
-    slot += parts;
+    views[v].n_parts = parts[v];
+    slot += parts[v];
   }
-  // largest items first so that short consistent-head items fill the tail
-  std::stable_sort(items.begin(), items.end(), [](const catekv::DecodeItem& a, const catekv::DecodeItem& b) {
-    return (a.t1 - a.t0) > (b.t1 - b.t0);
-  });
+  std::vector<int> next_part(nv, 0);
+  for (int i = 0; i < P.n_segments; ++i) {
+    const Segment& s = P.segs[i];
+    segs[i] = {s.view, next_part[s.view]++, (int32_t)s.t0, (int32_t)s.t1};
+    wseg[s.worker + 1] = i + 1;
+  }
+  for (int w = 1; w <= P.n_workers; ++w) wseg[w] = std::max(wseg[w], wseg[w - 1]);
 
   std::vector<unsigned char> host(P.slots_off, 0);
-  std::memcpy(host.data() + P.items_off, items.data(), items.size() * sizeof(catekv::DecodeItem));
+  std::memcpy(host.data() + P.segs_off, segs.data(), segs.size() * sizeof(catekv::DecodeItem));
+  std::memcpy(host.data() + P.workers_off, wseg.data(), wseg.size() * sizeof(int32_t));
   std::memcpy(host.data() + P.views_off, views.data(), views.size() * sizeof(catekv::ViewInfo));
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   hipError_t e = hipMemcpyAsync(ws, host.data(), host.size(), hipMemcpyHostToDevice, s);
@@ -356,15 +373,15 @@ int catekv_decode_plan(const int64_t* max_len_host, int batch, int hq, int hkv, 
   plan->batch = batch;
   plan->hq = hq;
   plan->hkv = hkv;
-  plan->split_tokens = split;
-  plan->n_items = P.n_items;
+  plan->split_tokens = split_tokens;
+  plan->n_workers = P.n_workers;
+  plan->n_segments = P.n_segments;
   plan->n_slots = P.n_slots;
   plan->n_multi = P.n_multi;
-  plan->reserved1 = 0;
-  plan->items_off = P.items_off;
+  plan->segs_off = P.segs_off;
+  plan->workers_off = P.workers_off;
   plan->views_off = P.views_off;
-  plan->reserved2 = 0;
-  plan->partials_off = P.slots_off;
+  plan->slots_off = P.slots_off;
   plan->ws_bytes = P.total;
   plan->max_len_total = total;
   return ok();
@@ -389,16 +406,18 @@ int catekv_decode_attn(int dtype, const catekv_decode_plan_t* plan, const void* 
   a.q = q;
   a.kv = kv;
   a.lens = lens;
-  a.items = reinterpret_cast<const catekv::DecodeItem*>(w + plan->items_off);
+  a.items = reinterpret_cast<const catekv::DecodeItem*>(w + plan->segs_off);
+  a.worker_seg = reinterpret_cast<const int32_t*>(w + plan->workers_off);
   a.views = reinterpret_cast<const catekv::ViewInfo*>(w + plan->views_off);
-  a.slots = reinterpret_cast<float*>(w + plan->partials_off);
-  a.n_items = plan->n_items;
+  a.slots = reinterpret_cast<float*>(w + plan->slots_off);
+  a.n_workers = plan->n_workers;
+  a.n_multi = plan->n_multi;
   a.n_views = batch * hkv;
   a.hkv = hkv;
   a.scale = scale;
   a.out = out;
   a.lse = lse;
-  hipError_t e = catekv::launch_decode(dtype, hq / hkv, a, plan->n_multi > 0, reinterpret_cast<hipStream_t>(stream));
+  hipError_t e = catekv::launch_decode(dtype, hq / hkv, a, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "decode_attn launch");
   return ok();
 }

@@ -1,21 +1,26 @@
 // Hybrid-KV GQA decode attention (CateKV, Algorithm 1, decoding stage).
 //
 // Every (sequence, KV head) view -- a full cache for adaptive heads, a
-// compact cache for consistent heads -- is cut into split-KV work items by
-// the host plan.  One workgroup handles one item for all G query heads of
-// the group, so each K/V row is read from HBM exactly once per step.
+// compact cache for consistent heads -- is a run of tokens.  The host plan
+// lays all views end to end and cuts the run into equal shares, one per
+// persistent workgroup (stream-K), so long adaptive views and short
+// consistent views balance across CUs.  A workgroup streams the 1-3
+// segments of its share for all G query heads of the group, so each K/V row
+// is read from HBM exactly once per step.
 //
-// Streaming kernel: 8 lanes share one token row (each lane owns 16 of the 128
-// dims, fetched as 16-byte loads), so one wave covers 8 tokens per load
-// instruction.  Loads run NS stages ahead of use in a register ring.  q.k
+// Streaming: 8 lanes share one token row (each lane owns 16 of the 128 dims,
+// fetched as 16-byte global loads), so one wave covers 8 tokens per load
+// instruction; loads run NS stages ahead of use in a register ring.  q.k
 // partial sums are reduced over the 8 lanes with DPP; each group of 8 lanes
 // keeps its own online-softmax state (running max m, sum l, unnormalised o),
-// merged across groups and waves at the end.  An item that covers its whole
-// view writes the normalised output directly; otherwise it writes a partial
-// (o, m, l) that the combine kernel merges with the view's other partials
-// (log-sum-exp weighting).  No cross-workgroup synchronisation is needed.
+// merged across groups and waves at the end of a segment.  A segment that
+// covers its whole view writes the normalised output and log-sum-exp;
+// otherwise it writes a partial (o, m, l), and the combine kernel merges the
+// partials of each such view (log-sum-exp weighting) right after.
 #include "common.h"
 #include "internal.h"
+
+#include <type_traits>
 
 namespace catekv {
 
@@ -121,8 +126,28 @@ __device__ __forceinline__ int dim_of(int j, int e) {
   return ((e / NV) * 8 + j) * NV + (e % NV);
 }
 
+// ---- partials ----------------------------------------------------------------
+// A segment that does not cover its whole view stores (o, m, l) in its slot
+// with plain stores; the combine kernel, launched right after on the same
+// stream, sees them complete at the kernel boundary.
+template <int G>
+__device__ __forceinline__ void put_slot(float* slot, int g, int e, float M, float L, float Ov) {
+  slot[g * kD + e] = Ov;
+  if (e == 0) {
+    slot[G * kD + g] = L > 0.f ? M : -INFINITY;
+    slot[G * kD + G + g] = L;
+  }
+}
+
+__device__ __forceinline__ void emit(float* out, float* lse, size_t row, int e, float M, float L, float Ov) {
+  out[row * kD + e] = L > 0.f ? Ov / L : 0.f;
+  if (lse && e == 0) lse[row] = L > 0.f ? M + logf(L) : -INFINITY;
+}
+
+// Persistent stream-K worker: workgroup w streams segments
+// [worker_seg[w], worker_seg[w + 1]) of the plan, each a token range of one view.
 template <typename T, int G, int WAVES, int NS>
-__global__ __launch_bounds__(WAVES * 64) void decode_split_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(WAVES * 64) void decode_stream_kernel(DecodeArgs a) {
   constexpr int SF = G * kD + 2 * G;            // floats per partial slot
   constexpr int NT = WAVES * 64;
   constexpr int TPW = 8;                        // tokens per wave per stage
@@ -130,174 +155,376 @@ __global__ __launch_bounds__(WAVES * 64) void decode_split_kernel(DecodeArgs a) 
   const int wave = threadIdx.x >> 6;
   const int j = lane & 7;                       // lane within the token group
   const int gi = lane >> 3;                     // token group within the wave
-
-  const DecodeItem it = a.items[blockIdx.x];
-  const int bh = it.bh;
-  const int hkv = a.hkv;
-  const int b = bh / hkv, h = bh - b * hkv;
-  const catekv_kv_ptrs view = a.kv[bh];
-  int64_t len = a.lens[bh];
-  const ViewInfo vi = a.views[bh];
-  len = len < 0 ? 0 : len;
-  const int t0 = it.t0;
-  const int t_end = (int)((int64_t)it.t1 < len ? (int64_t)it.t1 : len);
-  const T* kbase = reinterpret_cast<const T*>(view.k);
-  const T* vbase = reinterpret_cast<const T*>(view.v);
+  const int hkv = a.hkv, hq = hkv * G;
   const float scale = a.scale;
   const float c = scale * kLog2e;               // raw dot -> log2 units
-
-  QFrag<T> qf[G];
-  const int hq = hkv * G;
-  const T* qb = reinterpret_cast<const T*>(a.q);
-#pragma unroll
-  for (int g = 0; g < G; ++g) qf[g].load(qb + ((size_t)b * hq + (size_t)h * G + g) * kD, j);
-
-  float m[G], l[G], o[G][16];
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    m[g] = -INFINITY;
-    l[g] = 0.f;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) o[g][e] = 0.f;
-  }
-
-  // stage s of wave w covers tokens t0 + (s * WAVES + w) * 8 + [0, 8)
-  const int ntok = t_end > t0 ? t_end - t0 : 0;
-  const int n_st = (ntok + TPW * WAVES - 1) / (TPW * WAVES);
   const float thr = 8.0f / c;                   // raw-unit slack before the running max is refreshed
 
-  Row<T> kb[NS], vb[NS];
-  auto issue = [&](int buf, int st) {
-    int tok = t0 + (st * WAVES + wave) * TPW + gi;
-    tok = tok < t_end ? tok : t0;               // rows past the end re-read a valid row
-    load_row(kb[buf], kbase + (size_t)tok * kD, j);
-    load_row(vb[buf], vbase + (size_t)tok * kD, j);
-  };
-  auto consume = [&](int buf, int st) {
-    const int tok = t0 + (st * WAVES + wave) * TPW + gi;
-    const bool valid = tok < t_end;
-    float s[G];
-    bool need = false;
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      const float x = sum8(qf[g].dot(kb[buf]));
-      s[g] = valid ? x : -INFINITY;
-      need |= s[g] > m[g] + thr;
-    }
-    if (__builtin_amdgcn_ballot_w64(need)) {
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        const float nm = fmaxf(m[g], s[g]);
-        if (nm > m[g]) {
-          const float corr = m[g] == -INFINITY ? 0.f : fast_exp2((m[g] - nm) * c);
-          l[g] *= corr;
-#pragma unroll
-          for (int e = 0; e < 16; ++e) o[g][e] *= corr;
-          m[g] = nm;
-        }
-      }
-    }
-    float vf[16];
-    row_to_f32(vb[buf], vf);
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      const float p = valid ? fast_exp2(__builtin_fmaf(s[g], c, -m[g] * c)) : 0.f;
-      l[g] += p;
-#pragma unroll
-      for (int e = 0; e < 16; ++e) o[g][e] = __builtin_fmaf(p, vf[e], o[g][e]);
-    }
-  };
-
-  if (n_st > 0) {
-#pragma unroll
-    for (int s = 0; s < NS - 1; ++s)
-      if (s < n_st) issue(s, s);
-    for (int base = 0; base < n_st; base += NS) {
-#pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        const int st = base + s;
-        if (st < n_st) {
-          if (st + NS - 1 < n_st) issue((s + NS - 1) % NS, st + NS - 1);
-          consume(s, st);
-        }
-      }
-    }
-  }
-
-  // ---- merge the 8 token groups of the wave (lanes l, l^8, l^16, l^32) ----
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    float M = m[g];
-    M = fmaxf(M, shfl_xor(M, 8));
-    M = fmaxf(M, shfl_xor(M, 16));
-    M = fmaxf(M, shfl_xor(M, 32));
-    const float corr = m[g] == -INFINITY ? 0.f : fast_exp2((m[g] - M) * c);
-    float lg = l[g] * corr;
-    lg += shfl_xor(lg, 8);
-    lg += shfl_xor(lg, 16);
-    lg += shfl_xor(lg, 32);
-    l[g] = lg;
-    m[g] = M;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      float x = o[g][e] * corr;
-      x += shfl_xor(x, 8);
-      x += shfl_xor(x, 16);
-      x += shfl_xor(x, 32);
-      o[g][e] = x;
-    }
-  }
-
-  // ---- merge the waves through LDS -----------------------------------------
   __shared__ float s_o[WAVES][G][kD];
   __shared__ float s_m[WAVES][G], s_l[WAVES][G];
-  if (gi == 0) {
+
+  const int seg_lo = a.worker_seg[blockIdx.x], seg_hi = a.worker_seg[blockIdx.x + 1];
+  for (int sg = seg_lo; sg < seg_hi; ++sg) {
+    const DecodeItem it = a.items[sg];
+    const int bh = it.bh;
+    const int b = bh / hkv, h = bh - b * hkv;
+    const catekv_kv_ptrs view = a.kv[bh];
+    int64_t len = a.lens[bh];
+    const ViewInfo vi = a.views[bh];
+    len = len < 0 ? 0 : len;
+    const int t0 = it.t0;
+    const int t_end = (int)((int64_t)it.t1 < len ? (int64_t)it.t1 : len);
+    const T* kbase = reinterpret_cast<const T*>(view.k);
+    const T* vbase = reinterpret_cast<const T*>(view.v);
+
+    QFrag<T> qf[G];
+    const T* qb = reinterpret_cast<const T*>(a.q);
+#pragma unroll
+    for (int g = 0; g < G; ++g) qf[g].load(qb + ((size_t)b * hq + (size_t)h * G + g) * kD, j);
+
+    float m[G], l[G], o[G][16];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
+      m[g] = -INFINITY;
+      l[g] = 0.f;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) s_o[wave][g][dim_of<T>(j, e)] = o[g][e];
-      if (j == 0) {
-        s_m[wave][g] = m[g];
-        s_l[wave][g] = l[g];
-      }
+      for (int e = 0; e < 16; ++e) o[g][e] = 0.f;
     }
-  }
-  __syncthreads();
 
-  const size_t row0 = (size_t)b * hq + (size_t)h * G;
-  float* slot = a.slots + (size_t)(vi.first_slot + it.part) * SF;
-  for (int t = threadIdx.x; t < G * kD; t += NT) {
-    const int g = t / kD, e = t - g * kD;
-    float M = -INFINITY;
+    // stage s of wave w covers tokens t0 + (s * WAVES + w) * 8 + [0, 8)
+    const int ntok = t_end > t0 ? t_end - t0 : 0;
+    const int n_st = (ntok + TPW * WAVES - 1) / (TPW * WAVES);
+
+    Row<T> kb[NS], vb[NS];
+    auto issue = [&](int buf, int st) {
+      int tok = t0 + (st * WAVES + wave) * TPW + gi;
+      tok = tok < t_end ? tok : t0;             // rows past the end re-read a valid row
+      load_row(kb[buf], kbase + (size_t)tok * kD, j);
+      load_row(vb[buf], vbase + (size_t)tok * kD, j);
+    };
+    auto consume = [&](int buf, int st) {
+      const int tok = t0 + (st * WAVES + wave) * TPW + gi;
+      const bool valid = tok < t_end;
+      float s[G];
+      bool need = false;
 #pragma unroll
-    for (int w = 0; w < WAVES; ++w) M = fmaxf(M, s_m[w][g]);
-    float L = 0.f, Ov = 0.f;
-#pragma unroll
-    for (int w = 0; w < WAVES; ++w) {
-      const float cw = s_m[w][g] == -INFINITY ? 0.f : fast_exp2((s_m[w][g] - M) * c);
-      L += s_l[w][g] * cw;
-      Ov += s_o[w][g][e] * cw;
-    }
-    const float Mn = M * scale;                 // natural-log units of the scaled score
-    if (vi.n_parts == 1) {
-      a.out[(row0 + g) * kD + e] = L > 0.f ? Ov / L : 0.f;
-      if (a.lse && e == 0) a.lse[row0 + g] = L > 0.f ? Mn + logf(L) : -INFINITY;
-    } else {
-      slot[g * kD + e] = Ov;
-      if (e == 0) {
-        slot[G * kD + g] = L > 0.f ? Mn : -INFINITY;
-        slot[G * kD + G + g] = L;
+      for (int g = 0; g < G; ++g) {
+        const float x = sum8(qf[g].dot(kb[buf]));
+        s[g] = valid ? x : -INFINITY;
+        need |= s[g] > m[g] + thr;
       }
+      if (__builtin_amdgcn_ballot_w64(need)) {
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          const float nm = fmaxf(m[g], s[g]);
+          if (nm > m[g]) {
+            const float corr = m[g] == -INFINITY ? 0.f : fast_exp2((m[g] - nm) * c);
+            l[g] *= corr;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) o[g][e] *= corr;
+            m[g] = nm;
+          }
+        }
+      }
+      float vf[16];
+      row_to_f32(vb[buf], vf);
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const float p = valid ? fast_exp2(__builtin_fmaf(s[g], c, -m[g] * c)) : 0.f;
+        l[g] += p;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[g][e] = __builtin_fmaf(p, vf[e], o[g][e]);
+      }
+    };
+
+    // Loads are issued unconditionally (stages past the end re-read row t0,
+    // which is cached) so that every wait in the ring is a static count and
+    // the NS - 1 stages ahead stay in flight.
+    if (n_st > 0) {
+      const int n_pad = (n_st + NS - 1) / NS * NS;
+#pragma unroll
+      for (int s = 0; s < NS - 1; ++s) issue(s, s);
+      for (int base = 0; base < n_pad; base += NS) {
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+          issue((s + NS - 1) % NS, base + s + NS - 1);
+          consume(s, base + s);
+        }
+      }
+    }
+
+    // ---- merge the 8 token groups of the wave (lanes l, l^8, l^16, l^32) ----
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      float M = m[g];
+      M = fmaxf(M, shfl_xor(M, 8));
+      M = fmaxf(M, shfl_xor(M, 16));
+      M = fmaxf(M, shfl_xor(M, 32));
+      const float corr = m[g] == -INFINITY ? 0.f : fast_exp2((m[g] - M) * c);
+      float lg = l[g] * corr;
+      lg += shfl_xor(lg, 8);
+      lg += shfl_xor(lg, 16);
+      lg += shfl_xor(lg, 32);
+      l[g] = lg;
+      m[g] = M;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        float x = o[g][e] * corr;
+        x += shfl_xor(x, 8);
+        x += shfl_xor(x, 16);
+        x += shfl_xor(x, 32);
+        o[g][e] = x;
+      }
+    }
+
+    // ---- merge the waves through LDS ---------------------------------------
+    __syncthreads();                            // LDS of the previous segment is free
+    if (gi == 0) {
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) s_o[wave][g][dim_of<T>(j, e)] = o[g][e];
+        if (j == 0) {
+          s_m[wave][g] = m[g];
+          s_l[wave][g] = l[g];
+        }
+      }
+    }
+    __syncthreads();
+
+    const size_t row0 = (size_t)b * hq + (size_t)h * G;
+    float* slot = a.slots + (size_t)(vi.first_slot + it.part) * SF;
+    for (int t = threadIdx.x; t < G * kD; t += NT) {
+      const int g = t / kD, e = t - g * kD;
+      float M = -INFINITY;
+#pragma unroll
+      for (int w = 0; w < WAVES; ++w) M = fmaxf(M, s_m[w][g]);
+      float L = 0.f, Ov = 0.f;
+#pragma unroll
+      for (int w = 0; w < WAVES; ++w) {
+        const float cw = s_m[w][g] == -INFINITY ? 0.f : fast_exp2((s_m[w][g] - M) * c);
+        L += s_l[w][g] * cw;
+        Ov += s_o[w][g][e] * cw;
+      }
+      const float Mn = M * scale;               // natural-log units of the scaled score
+      if (vi.n_parts == 1) emit(a.out, a.lse, row0 + g, e, Mn, L, Ov);
+      else put_slot<G>(slot, g, e, Mn, L, Ov);
     }
   }
 }
 
-// Merges the partials of every view cut into more than one item.  One
-// workgroup per (view, query head of the group): all (m, l) pairs go to LDS,
-// then 8 lanes of parts x 128 dims accumulate the weighted o.
-constexpr int kCombineThreads = 1024;
-constexpr int kCombineLanes = kCombineThreads / kD;   // parts handled in parallel per dim
-constexpr int kCombineMaxParts = 4096;
+// ---- bf16 storage: the contraction runs on MFMA -----------------------------
+// Per wave and stage, a tile of 16 tokens:
+//  * S^T = K Q^T with v_mfma_f32_16x16x32_bf16: A = the K tile (lane l holds
+//    token l % 16, dims [32 ks + 8 (l / 16), +8) for k-step ks), B = Q^T with
+//    the G heads as columns (zero columns past G).  The result puts the score
+//    of token 4 k + r and head j in lane j + 16 k, register r.
+//  * Those lanes and registers are exactly the A operand of
+//    v_mfma_f32_16x16x4_f32 for the token group {4 k + r : k < 4} (A[head][k]),
+//    so P = exp(S - m) needs no data movement.  B is V in its natural row
+//    layout: lane l holds token 4 (l / 16) + r, dims [8 (l % 16), +8), and
+//    register e of that row feeds the product for dims 8 n + e.
+//  * O accumulates in 8 tiles (one per e): head i, dim 8 n + e sits in lane
+//    n + 16 (i / 4), register i % 4.
+// The running max of a head is kept equal across the four lanes that hold
+// its tokens, so every product that accumulates into O uses the same scale.
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+constexpr float kDecodeMFloor = -1e30f;
+
+template <int G, int WAVES, int NS>
+__global__ __launch_bounds__(WAVES * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void decode_stream_mfma_kernel(DecodeArgs a) {
+  static_assert(G <= 16, "heads of a group must fit the 16 MFMA columns");
+  constexpr int SF = G * kD + 2 * G;
+  constexpr int NT = WAVES * 64;
+  constexpr int TPW = 16;                       // tokens per wave per stage
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int n16 = lane & 15, k4 = lane >> 4;
+  const int hkv = a.hkv, hq = hkv * G;
+  const float scale = a.scale;
+  const float c = scale * kLog2e;
+  const float thr = 8.0f / c;
+  const bool head_lane = n16 < G;               // lanes whose column is a real head
+
+  __shared__ float s_o[WAVES][G][kD];
+  __shared__ float s_m[WAVES][G], s_l[WAVES][G];
+
+  const int seg_lo = a.worker_seg[blockIdx.x], seg_hi = a.worker_seg[blockIdx.x + 1];
+  for (int sg = seg_lo; sg < seg_hi; ++sg) {
+    const DecodeItem it = a.items[sg];
+    const int bh = it.bh;
+    const int b = bh / hkv, h = bh - b * hkv;
+    const catekv_kv_ptrs view = a.kv[bh];
+    int64_t len = a.lens[bh];
+    const ViewInfo vi = a.views[bh];
+    len = len < 0 ? 0 : len;
+    const int t0 = it.t0;
+    const int t_end = (int)((int64_t)it.t1 < len ? (int64_t)it.t1 : len);
+    const char* kbase = reinterpret_cast<const char*>(view.k);
+    const char* vbase = reinterpret_cast<const char*>(view.v);
+
+    // B operand of S^T: head n16's dims [32 ks + 8 k4, +8)
+    uint4 qb[4];
+    {
+      const char* qrow = reinterpret_cast<const char*>(a.q) +
+                         ((size_t)b * hq + (size_t)h * G + (head_lane ? n16 : 0)) * kD * 2;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const uint4 v = ldg16(qrow + ks * 64 + k4 * 16);
+        qb[ks] = head_lane ? v : make_uint4(0, 0, 0, 0);
+      }
+    }
+
+    f32x4_t O[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) O[e] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    // a finite floor keeps exp2(s c - m c) = 0 for masked tokens (s = -inf) even
+    // before the first valid token; +inf makes p = 0 on padding columns
+    float m = head_lane ? kDecodeMFloor : INFINITY;
+    float l = 0.f;
+
+    const int ntok = t_end > t0 ? t_end - t0 : 0;
+    const int n_units = (ntok + TPW - 1) / TPW;   // 16-token units of the segment
+
+    // wave w takes units w, w + WAVES, w + 2 WAVES, ... (unit numbers ride
+    // along the prefetch ring)
+    int st_ctr = 0;
+    auto grab = [&]() -> int { return (st_ctr++) * WAVES + wave; };
+    int unit[NS];
+
+    uint4 kb[NS][4], vb[NS][4];
+    auto issue = [&](int buf, int un) {
+      const int tile = t0 + un * TPW;
+      int tk = tile + n16;
+      tk = tk < t_end ? tk : t0;                  // rows past the end re-read row t0
+      const char* kr = kbase + (size_t)tk * (kD * 2) + k4 * 16;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) kb[buf][ks] = ldg16(kr + ks * 64);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        int tv = tile + 4 * k4 + r;
+        tv = tv < t_end ? tv : t0;
+        vb[buf][r] = ldg16(vbase + (size_t)tv * (kD * 2) + n16 * 16);
+      }
+    };
+    auto consume = [&](int buf, int un) {
+      const int tile = t0 + un * TPW;
+      f32x4_t S = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks)
+        S = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kb[buf][ks]),
+                                                    __builtin_bit_cast(bf16x8_t, qb[ks]), S, 0, 0, 0);
+      float sv[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sv[r] = tile + 4 * k4 + r < t_end ? S[r] : -INFINITY;
+      float mx = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+      mx = fmaxf(mx, shfl_xor(mx, 16));
+      mx = fmaxf(mx, shfl_xor(mx, 32));
+      const bool need = head_lane && mx > m + thr;
+      if (__builtin_amdgcn_ballot_w64(need)) {
+        // refresh the running max of every head that needs it; rescale l and O
+        float corr = 1.f;
+        if (head_lane && mx > m) {
+          corr = fast_exp2((m - mx) * c);       // 0 while m is still the floor
+          m = mx;
+        }
+        l *= corr;
+        // O register r of lane L belongs to head 4 (L / 16) + r: fetch that head's corr
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int src = (4 * k4 + r) & 15;
+          const float cr = __int_as_float(__builtin_amdgcn_ds_bpermute(src << 2, __float_as_int(corr)));
+#pragma unroll
+          for (int e = 0; e < 8; ++e) O[e][r] *= cr;
+        }
+      }
+      const float mc = m * c;
+      f32x4_t P;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        P[r] = fast_exp2(__builtin_fmaf(sv[r], c, -mc));
+        l += P[r];
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const uint32_t w[4] = {vb[buf][r].x, vb[buf][r].y, vb[buf][r].z, vb[buf][r].w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          O[2 * i] = __builtin_amdgcn_mfma_f32_16x16x4f32(P[r], bf16_lo(w[i]), O[2 * i], 0, 0, 0);
+          O[2 * i + 1] = __builtin_amdgcn_mfma_f32_16x16x4f32(P[r], bf16_hi(w[i]), O[2 * i + 1], 0, 0, 0);
+        }
+      }
+    };
+
+    if (n_units > 0) {
+      // units past the end re-read row t0 (cached) and contribute nothing
+#pragma unroll
+      for (int s = 0; s < NS - 1; ++s) {
+        unit[s] = grab();
+        issue(s, unit[s]);
+      }
+      bool more = true;
+      while (more) {
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+          const int nb = (s + NS - 1) % NS;
+          unit[nb] = grab();
+          issue(nb, unit[nb]);
+          if (unit[s] < n_units) consume(s, unit[s]);
+          else more = false;
+        }
+      }
+    }
+
+    // l of a head is spread over its four lanes (one per token quarter)
+    l += shfl_xor(l, 16);
+    l += shfl_xor(l, 32);
+
+    __syncthreads();                            // LDS of the previous segment is free
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int head = 4 * k4 + r;
+      if (head < G) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s_o[wave][head][8 * n16 + e] = O[e][r];
+      }
+    }
+    if (lane < G) {
+      s_m[wave][lane] = m;
+      s_l[wave][lane] = l;
+    }
+    __syncthreads();
+
+    const size_t row0 = (size_t)b * hq + (size_t)h * G;
+    float* slot = a.slots + (size_t)(vi.first_slot + it.part) * SF;
+    for (int t = threadIdx.x; t < G * kD; t += NT) {
+      const int g = t / kD, e = t - g * kD;
+      float M = -INFINITY;
+#pragma unroll
+      for (int w = 0; w < WAVES; ++w) M = fmaxf(M, s_m[w][g]);
+      float L = 0.f, Ov = 0.f;
+#pragma unroll
+      for (int w = 0; w < WAVES; ++w) {
+        const float cw = s_m[w][g] == -INFINITY ? 0.f : fast_exp2((s_m[w][g] - M) * c);
+        L += s_l[w][g] * cw;
+        Ov += s_o[w][g][e] * cw;
+      }
+      const float Mn = M * scale;
+      if (vi.n_parts == 1) emit(a.out, a.lse, row0 + g, e, Mn, L, Ov);
+      else put_slot<G>(slot, g, e, Mn, L, Ov);
+    }
+  }
+}
+
+// Merges the partials of every view covered by more than one segment: one
+// workgroup per (view, query head).  Thread (part lane pl, dim quad dq) loads
+// the float4 o of parts pl, pl + 8, ... together with their (m, l) in one
+// round of independent loads; the max and the weights are reduced in LDS.
+constexpr int kCombineThreads = 512;
+constexpr int kCombineLanes = kCombineThreads / 32;    // parts handled side by side
+constexpr int kCombineBatch = 16;                      // parts per thread per round
 
 template <int G>
 __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(DecodeArgs a) {
@@ -306,85 +533,116 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(DecodeA
   const ViewInfo vi = a.views[bh];
   const int P = vi.n_parts;
   if (P <= 1) return;
-  __shared__ float s_w[kCombineMaxParts];
   __shared__ float s_red[kCombineThreads / 64];
-  __shared__ float s_acc[kCombineLanes][kD];
+  __shared__ float4 s_acc[kCombineLanes][32];
+  __shared__ float s_l[kCombineLanes][32];
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int pl = t >> 5, dq = t & 31;
   const float* base = a.slots + (size_t)vi.first_slot * SF;
 
-  // global max of the parts' m
-  float M = -INFINITY;
-  for (int s = t; s < P; s += kCombineThreads) {
-    const float ms = base[(size_t)s * SF + G * kD + g];
-    s_w[s] = ms;
-    M = fmaxf(M, ms);
-  }
-  for (int off = 32; off > 0; off >>= 1) M = fmaxf(M, shfl_xor(M, off));
-  if (lane == 0) s_red[wave] = M;
-  __syncthreads();
-  M = s_red[0];
+  float M = -INFINITY, L = 0.f;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int s0 = pl; s0 < P; s0 += kCombineLanes * kCombineBatch) {
+    float ms[kCombineBatch], ls[kCombineBatch];
+    float4 os[kCombineBatch];
 #pragma unroll
-  for (int w = 1; w < kCombineThreads / 64; ++w) M = fmaxf(M, s_red[w]);
-  __syncthreads();
-  // weights w_s = exp(m_s - M) and L = sum w_s l_s
-  float L = 0.f;
-  for (int s = t; s < P; s += kCombineThreads) {
-    const float ms = s_w[s];
-    const float w = ms == -INFINITY ? 0.f : fast_exp2((ms - M) * kLog2e);
-    s_w[s] = w;
-    L += w * base[(size_t)s * SF + G * kD + G + g];
-  }
-  for (int off = 32; off > 0; off >>= 1) L += shfl_xor(L, off);
-  if (lane == 0) s_red[wave] = L;
-  __syncthreads();
-  L = 0.f;
-#pragma unroll
-  for (int w = 0; w < kCombineThreads / 64; ++w) L += s_red[w];
-
-  // o = sum_s w_s o_s
-  const int e = t % kD, pl = t / kD;
-  float acc = 0.f;
-  constexpr int UNR = 8;
-  for (int s0 = pl; s0 < P; s0 += kCombineLanes * UNR) {
-    float v[UNR];
-#pragma unroll
-    for (int u = 0; u < UNR; ++u) {
+    for (int u = 0; u < kCombineBatch; ++u) {
       const int s = s0 + u * kCombineLanes;
-      v[u] = s < P ? base[(size_t)s * SF + g * kD + e] : 0.f;
+      if (s < P) {
+        const float* sl = base + (size_t)s * SF;
+        ms[u] = sl[G * kD + g];
+        ls[u] = sl[G * kD + G + g];
+        os[u] = *reinterpret_cast<const float4*>(sl + g * kD + 4 * dq);
+      } else {
+        ms[u] = -INFINITY;
+        ls[u] = 0.f;
+        os[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
     }
+    float mb = M;
 #pragma unroll
-    for (int u = 0; u < UNR; ++u) {
-      const int s = s0 + u * kCombineLanes;
-      acc += s < P ? s_w[s] * v[u] : 0.f;
+    for (int u = 0; u < kCombineBatch; ++u) mb = fmaxf(mb, ms[u]);
+    const float ca = M == -INFINITY ? 0.f : fast_exp2((M - mb) * kLog2e);
+    L *= ca;
+    acc.x *= ca; acc.y *= ca; acc.z *= ca; acc.w *= ca;
+#pragma unroll
+    for (int u = 0; u < kCombineBatch; ++u) {
+      const float w = ms[u] == -INFINITY ? 0.f : fast_exp2((ms[u] - mb) * kLog2e);
+      L += w * ls[u];
+      acc.x += w * os[u].x; acc.y += w * os[u].y; acc.z += w * os[u].z; acc.w += w * os[u].w;
     }
+    M = mb;
   }
-  s_acc[pl][e] = acc;
+  // global max over the part lanes, then rescale each lane's sums to it
+  float Mx = M;
+  for (int off = 32; off > 0; off >>= 1) Mx = fmaxf(Mx, shfl_xor(Mx, off));
+  if (lane == 0) s_red[wave] = Mx;
   __syncthreads();
-  if (t < kD) {
-    float o = 0.f;
+  Mx = s_red[0];
 #pragma unroll
-    for (int p = 0; p < kCombineLanes; ++p) o += s_acc[p][t];
+  for (int w = 1; w < kCombineThreads / 64; ++w) Mx = fmaxf(Mx, s_red[w]);
+  const float cs = M == -INFINITY ? 0.f : fast_exp2((M - Mx) * kLog2e);
+  s_acc[pl][dq] = make_float4(acc.x * cs, acc.y * cs, acc.z * cs, acc.w * cs);
+  s_l[pl][dq] = L * cs;
+  __syncthreads();
+  if (t < 32) {
+    float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+    float Lt = 0.f;
+#pragma unroll
+    for (int p = 0; p < kCombineLanes; ++p) {
+      o.x += s_acc[p][t].x; o.y += s_acc[p][t].y; o.z += s_acc[p][t].z; o.w += s_acc[p][t].w;
+      Lt += s_l[p][t];
+    }
     const int hkv = a.hkv, b = bh / hkv, h = bh - b * hkv;
     const size_t row = (size_t)b * hkv * G + (size_t)h * G + g;
-    a.out[row * kD + t] = L > 0.f ? o / L : 0.f;
-    if (a.lse && t == 0) a.lse[row] = L > 0.f ? M + logf(L) : -INFINITY;
+    const float inv = Lt > 0.f ? 1.f / Lt : 0.f;
+    *reinterpret_cast<float4*>(a.out + row * kD + 4 * t) = make_float4(o.x * inv, o.y * inv, o.z * inv, o.w * inv);
+    if (a.lse && t == 0) a.lse[row] = Lt > 0.f ? Mx + logf(Lt) : -INFINITY;
   }
 }
 
 template <typename T, int G>
-static hipError_t launch_t(const DecodeArgs& a, bool combine, hipStream_t stream) {
-  constexpr int WAVES = 4, NS = 4;
-  hipLaunchKernelGGL((decode_split_kernel<T, G, WAVES, NS>), dim3(a.n_items), dim3(WAVES * 64), 0, stream, a);
-  if (combine)
+static hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
+  if constexpr (std::is_same<T, uint16_t>::value)
+    hipLaunchKernelGGL((decode_stream_mfma_kernel<G, kDecodeWaves, kDecodeStagesMfma>), dim3(a.n_workers),
+                       dim3(kDecodeWaves * 64), 0, stream, a);
+  else
+    hipLaunchKernelGGL((decode_stream_kernel<T, G, kDecodeWaves, kDecodeStages>), dim3(a.n_workers),
+                       dim3(kDecodeWaves * 64), 0, stream, a);
+  if (a.n_multi > 0)
     hipLaunchKernelGGL((decode_combine_kernel<G>), dim3(a.n_views * G), dim3(kCombineThreads), 0, stream, a);
   return hipGetLastError();
 }
 
-int decode_max_parts() { return kCombineMaxParts; }
+template <typename T, int G>
+static int occupancy_t() {
+  int n = 0;
+  hipError_t e;
+  if constexpr (std::is_same<T, uint16_t>::value)
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, decode_stream_mfma_kernel<G, kDecodeWaves, kDecodeStagesMfma>,
+                                                     kDecodeWaves * 64, 0);
+  else
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, decode_stream_kernel<T, G, kDecodeWaves, kDecodeStages>,
+                                                     kDecodeWaves * 64, 0);
+  if (e != hipSuccess) return 1;
+  return n < 1 ? 1 : n;
+}
 
-hipError_t launch_decode(int dtype, int G, const DecodeArgs& a, bool combine, hipStream_t stream) {
+int decode_blocks_per_cu(int dtype, int G) {
+#define CATEKV_OCC(T, GG) \
+  if (G == GG) return occupancy_t<T, GG>();
+  if (dtype == CATEKV_BF16) {
+    CATEKV_OCC(uint16_t, 1) CATEKV_OCC(uint16_t, 2) CATEKV_OCC(uint16_t, 4) CATEKV_OCC(uint16_t, 8)
+  } else {
+    CATEKV_OCC(float, 1) CATEKV_OCC(float, 2) CATEKV_OCC(float, 4) CATEKV_OCC(float, 8)
+  }
+#undef CATEKV_OCC
+  return 1;
+}
+
+hipError_t launch_decode(int dtype, int G, const DecodeArgs& a, hipStream_t stream) {
 #define CATEKV_DEC(T, GG) \
-  if (G == GG) return launch_t<T, GG>(a, combine, stream);
+  if (G == GG) return launch_t<T, GG>(a, stream);
   if (dtype == CATEKV_BF16) {
     CATEKV_DEC(uint16_t, 1) CATEKV_DEC(uint16_t, 2) CATEKV_DEC(uint16_t, 4) CATEKV_DEC(uint16_t, 8)
   } else {

@@ -21,10 +21,15 @@ struct DecodeItem {
   int32_t t1;
 };
 
-// Per view: where its partial slots live and how many items cover it.
+constexpr int kDecodeWaves = 8;    // waves per decode workgroup
+constexpr int kDecodeStages = 4;   // register prefetch depth (fp32 path)
+constexpr int kDecodeStagesMfma = 3;   // register prefetch depth (bf16 MFMA path, 16-token stages)
+constexpr int kDecodeQuantum = 64; // tokens per workgroup load stage (16 per wave)
+
+// Per view: where its partial slots live and how many segments cover it.
 struct ViewInfo {
   int32_t first_slot;     // slot of part 0
-  int32_t n_parts;
+  int32_t n_parts;        // segments covering the view
 };
 
 // Floats per decode partial slot for a group of G query heads: o[G][128],
@@ -35,17 +40,19 @@ struct DecodeArgs {
   const void* q;
   const catekv_kv_ptrs* kv;
   const int64_t* lens;
-  const DecodeItem* items;
+  const DecodeItem* items;      // segments, grouped by worker
+  const int32_t* worker_seg;    // [n_workers + 1] first segment of each worker
   const ViewInfo* views;
-  float* slots;           // partial slots
-  int n_items, n_views, hkv;
+  float* slots;                 // partial slots
+  int n_workers, n_views, n_multi, hkv;
   float scale;
   float* out;
   float* lse;
 };
 
-int decode_max_parts();
-hipError_t launch_decode(int dtype, int G, const DecodeArgs& a, bool combine, hipStream_t stream);
+// Decode workgroups one CU holds at once (occupancy of the stream kernel).
+int decode_blocks_per_cu(int dtype, int G);
+hipError_t launch_decode(int dtype, int G, const DecodeArgs& a, hipStream_t stream);
 
 // ---- critical-token selection ------------------------------------------
 struct SelectGeom {

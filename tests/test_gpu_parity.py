@@ -59,7 +59,7 @@ def test_decode_ragged_views(dtype):
     q_st = synth.f32_to_bf16_bits(q) if dtype == "bf16" else q
     say(f"decode ragged {dtype} lens={lens}")
     out, lse, _, plan = run_decode(views, B, hq, hkv, dtype, q_st, split=256)
-    assert plan.plan.n_multi > 0            # views split over several items
+    assert plan.plan.n_multi > 0            # views merged from several partials
     qq = f64(q_st)
     for b in range(B):
         vv = [(f64(views[b * hkv + h][0])[:lens[b * hkv + h]], f64(views[b * hkv + h][1])[:lens[b * hkv + h]])
