@@ -50,6 +50,39 @@ __device__ __forceinline__ float max16(float x) {
   return x;
 }
 
+// x combined with x of lane ^ 16 (or ^ 32) on every lane, through the gfx950
+// row-swap instructions (VALU; no LDS traffic).  Swapping a register with
+// itself leaves one half of each lane pair in each result, so the two results
+// of the swap hold x[lane] and x[lane ^ 16] in some order.
+__device__ __forceinline__ float add_xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float add_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float max_xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float max_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// Maximum over each aligned group of g lanes (g a power of two up to 64, the
+// same on every lane); every lane of a group gets the group's maximum.
+__device__ __forceinline__ float max_in_group(float x, int g) {
+  if (g >= 2) x = fmaxf(x, dpp<kDppXor1>(x));
+  if (g >= 4) x = fmaxf(x, dpp<kDppXor2>(x));
+  if (g >= 8) x = fmaxf(x, dpp<kDppHalfMirror>(x));
+  if (g >= 16) x = fmaxf(x, dpp<kDppMirror>(x));
+  if (g >= 32) x = max_xor16(x);
+  if (g >= 64) x = max_xor32(x);
+  return x;
+}
+
 // Cross-row exchange through the LDS crossbar (no LDS storage used).
 __device__ __forceinline__ float shfl_xor(float x, int mask) {
   int lane = __lane_id();
@@ -57,6 +90,20 @@ __device__ __forceinline__ float shfl_xor(float x, int mask) {
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Compiler-only memory barrier: keeps LDS accesses on their side of a
+// hand-placed s_waitcnt / s_barrier pair.
+__device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
+
+// Workgroup barrier that waits only for this wave's LDS operations, so that
+// global-to-LDS loads still in flight keep flowing across it.
+// s_waitcnt immediate: lgkmcnt(0), vmcnt and expcnt not waited on.
+__device__ __forceinline__ void barrier_lds_only() {
+  compiler_fence();
+  __builtin_amdgcn_s_waitcnt(0xC07F);
+  __builtin_amdgcn_s_barrier();
+  compiler_fence();
+}
 
 // 16-byte load that the compiler keeps as one dwordx4.
 __device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }

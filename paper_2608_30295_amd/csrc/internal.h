@@ -59,11 +59,13 @@ struct SelectGeom {
   int hq, hkv, G, l_obs, cs, n_sel, b;
   int64_t n, n_keys;       // n_keys = n - l_obs
   int64_t n_chunks;
+  int64_t cb_tokens;       // key columns per score workgroup
   int n_colblk;            // column blocks of the score passes
   int heads[128];
 };
 
-int64_t score_colblocks(int64_t n_keys);
+// Key columns per score workgroup for n_keys columns of n_heads KV heads.
+int64_t score_block_tokens(int64_t n_keys, int n_heads);
 size_t select_workspace_bytes(const SelectGeom& g);
 hipError_t launch_select(int dtype, const SelectGeom& g, const void* q_obs, const void* k,
                          int32_t* idx_out, void* ws, hipStream_t stream);
@@ -78,6 +80,7 @@ struct ScoreGeom {
   int64_t q_pos0;
   int causal;
   double k_pct, alpha;
+  int64_t cb_tokens;
   int n_colblk;
 };
 

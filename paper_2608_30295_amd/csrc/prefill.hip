@@ -17,11 +17,13 @@
 #include "internal.h"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace catekv {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int kTileTok = 64;     // tokens per LDS tile (4 MFMA column tiles)
 constexpr int kSWaves = 4;       // waves per score workgroup
@@ -73,20 +75,31 @@ struct ScoreArgs {
   int64_t q_pos0;         // absolute position of query row i = 0 (causal mask)
   float c;                // log2(e) / sqrt(d)
   int32_t heads[128];     // KV head per blockIdx.y
-  float2* rowpart;        // kRowStats out: [n_sel][n_colblk][R_pad] (m, l)
+  float2* rowpart;        // kRowStats out: [n_sel][n_colblk][R_pad] (max * c, sum)
   const float* rowoff;    // kColMass / kObsMatrix in: [n_sel][R_pad]
-  float* colmass;         // kColMass out: [n_sel][n_keys]
+  float* colmass;         // kColMass out: [n_sel][n_keys] (when cs_fused == 0)
+  float* chunks;          // kColMass out: [n_sel][n_chunks] chunk maxima (when cs_fused > 0)
+  int cs_fused;           // chunk size when it divides the 64-column tile, else 0
+  int64_t n_chunks;
   float* obs;             // kObsMatrix out: [n_sel][lq][n_keys]
 };
 
 template <typename T, int MT, int MODE, int G, bool CAUSAL>
-__global__ __launch_bounds__(kSWaves * 64) void score_kernel(ScoreArgs a) {
+__device__ __forceinline__ void score_body(const ScoreArgs& a) {
   using F = Frag<T>;
   constexpr int KG = F::KG, SEG = F::SEG;
   constexpr int RPAD = kSWaves * MT * 16;
   constexpr int NSTAGE = kTileTok * SEG / (kSWaves * 64);   // 16-byte loads per thread per tile
-  __shared__ uint4 s_tile[2][kTileTok * SEG];
-  __shared__ float s_col[kSWaves][kTileTok];
+  constexpr int NRING = sizeof(T) == 2 ? 4 : 2;               // LDS stages (16 KB bf16, 32 KB fp32 each)
+  // s_waitcnt immediate: vmcnt <= NSTAGE * (NRING - 2), expcnt not waited on;
+  // lgkmcnt(0) in column-mass mode, whose column partials in LDS the barrier publishes
+  constexpr int VM = NSTAGE * (NRING - 2);
+  constexpr int LGKM = MODE == kColMass ? 0 : 0xF;
+  constexpr int kWaitRing = (VM & 0xF) | ((VM >> 4) << 14) | (0x7 << 4) | (LGKM << 8);
+  // one LDS array per ring stage: stages chosen at compile time do not alias,
+  // so the compiler adds no waits of its own between the loads and the reads
+  __shared__ uint4 s_r0[kTileTok * SEG], s_r1[kTileTok * SEG], s_r2[kTileTok * SEG], s_r3[kTileTok * SEG];
+  __shared__ float s_col[2][kSWaves][kTileTok];   // per-wave column partials, by tile parity
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int sel = blockIdx.y, cb = blockIdx.x;
@@ -113,177 +126,239 @@ __global__ __launch_bounds__(kSWaves * 64) void score_kernel(ScoreArgs a) {
   }
 
   // rows owned by this lane's accumulator registers: (mt, r) -> row
-  float st_m[MT][4], st_l[MT][4];      // kRowStats
-  float off[MT][4];                    // kColMass / kObsMatrix
+  float st_mc[MT][4], st_l[MT][4];   // kRowStats: running max in log2 units (max * c), sum
+  float off[MT][4];                                // kColMass / kObsMatrix
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      st_m[mt][r] = kMInit;
+      st_mc[mt][r] = kMInit;
       st_l[mt][r] = 0.f;
+      off[mt][r] = 0.f;
       if (MODE != kRowStats) {
         const int row = (wave * MT + mt) * 16 + 4 * (lane >> 4) + r;
         off[mt][r] = a.rowoff[(size_t)sel * RPAD + row];
       }
     }
-  const float thr = 8.0f / a.c;
 
-  uint4 stage[NSTAGE];
-  auto stage_load = [&](int tile) {
+  // K tiles arrive through a ring of NRING LDS stages filled by direct
+  // global-to-LDS loads (no staging registers).  Thread x's load i lands in
+  // slot i * 256 + x; the slot's (token, position) picks which 16-byte
+  // segment of which row it fetches, so the ring holds the XOR-swizzled
+  // layout that tile_slot() reads.
+  const int full_tiles = (int)((col_end - col0) / kTileTok);   // tiles with no column past the end
+  const char* kbase = reinterpret_cast<const char*>(kh + (size_t)(a.key_off + col0) * kD);
+  int src_off[NSTAGE];   // byte offset of each of this thread's loads inside a tile
 #pragma unroll
-    for (int i = 0; i < NSTAGE; ++i) {
-      const int flat = i * kSWaves * 64 + threadIdx.x;
-      const int tok = flat / SEG, seg = flat - (flat / SEG) * SEG;
-      int64_t col = col0 + (int64_t)tile * kTileTok + tok;
-      col = col < col_end ? col : col0;
-      stage[i] = ld16(reinterpret_cast<const char*>(kh + (size_t)(a.key_off + col) * kD) + seg * 16);
-    }
-  };
-  auto stage_store = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < NSTAGE; ++i) {
-      const int flat = i * kSWaves * 64 + threadIdx.x;
-      const int tok = flat / SEG, seg = flat - (flat / SEG) * SEG;
-      s_tile[buf][tile_slot<T>(tok, seg)] = stage[i];
-    }
-  };
-
-  if (n_tiles > 0) {
-    stage_load(0);
-    stage_store(0);
+  for (int i = 0; i < NSTAGE; ++i) {
+    const int slot = i * kSWaves * 64 + threadIdx.x;
+    const int tok = slot / SEG, pos = slot - (slot / SEG) * SEG;
+    src_off[i] = tok * (kD * (int)sizeof(T)) + (pos ^ (tok & 15)) * 16;
   }
-  __syncthreads();
-
-  for (int tile = 0; tile < n_tiles; ++tile) {
-    const int buf = tile & 1;
-    if (tile + 1 < n_tiles) stage_load(tile + 1);
-    uint4 bf[4][KG];
+  auto issue = [&](uint4* stage, int tile) {
+    if (tile < full_tiles) {
+      const char* tb = kbase + (size_t)tile * (kTileTok * kD * sizeof(T));
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt)
+      for (int i = 0; i < NSTAGE; ++i)
+        __builtin_amdgcn_global_load_lds(tb + src_off[i], (lds_void*)&stage[i * kSWaves * 64 + wave * 64], 16, 0, 0);
+    } else {
 #pragma unroll
-      for (int kg = 0; kg < KG; ++kg)
-        bf[nt][kg] = s_tile[buf][tile_slot<T>(nt * 16 + (lane & 15), kg * 4 + (lane >> 4))];
+      for (int i = 0; i < NSTAGE; ++i) {
+        const int slot = i * kSWaves * 64 + threadIdx.x;
+        const int tok = slot / SEG;
+        int64_t col = (int64_t)tile * kTileTok + tok;
+        // rows past the end (and tiles past the last) re-read row 0 of the block
+        const int64_t rowoff = col < col_end - col0 ? col * (kD * (int64_t)sizeof(T)) : 0;
+        __builtin_amdgcn_global_load_lds(kbase + rowoff + (src_off[i] - tok * (kD * (int)sizeof(T))),
+                                         (lds_void*)&stage[i * kSWaves * 64 + wave * 64], 16, 0, 0);
+      }
+    }
+  };
+  auto ring = [&](int k) -> uint4* { return k == 0 ? s_r0 : k == 1 ? s_r1 : k == 2 ? s_r2 : s_r3; };
 
+  // Column mass of tile t: the four waves' partials are summed by one wave
+  // (t mod 4) during tile t + 1, after the barrier that published them, so no
+  // wave waits for this step and no barrier of its own is needed.  With cs
+  // dividing 64 a chunk never straddles a tile and BlockMax is taken here.
+  auto finish_cols = [&](int t) {
+    const int p = t & 1;
+    float v = 0.f;
+#pragma unroll
+    for (int w = 0; w < kSWaves; ++w) v += s_col[p][w][lane];
+    v *= 1.0f / (float)G;
+    const int64_t col = col0 + (int64_t)t * kTileTok + lane;
+    if (a.cs_fused > 0) {
+      const float mx = max_in_group(col < col_end ? v : -INFINITY, a.cs_fused);
+      if ((lane & (a.cs_fused - 1)) == 0 && col < col_end)
+        a.chunks[(size_t)sel * a.n_chunks + col / a.cs_fused] = mx;
+    } else if (col < col_end) {
+      a.colmass[(size_t)sel * a.n_keys + col] = v;
+    }
+  };
+#pragma unroll
+  for (int t = 0; t < NRING - 1; ++t) issue(ring(t), t);
+
+  const int64_t qpos_min = a.q_pos0;   // position of query row 0: the smallest row position
+  for (int base = 0; base < n_tiles; base += NRING) {
+#pragma unroll
+  for (int u = 0; u < NRING; ++u) {
+    const int tile = base + u;
+    if (tile >= n_tiles) break;
+    uint4* cur = ring(u);
+    const int par = tile & 1;
+    // this tile's loads are done once at most NRING - 2 later groups are outstanding
+    // (vector memory operations retire in order); the barrier makes every wave's
+    // part of the tile visible and frees the stage the next issue overwrites
+    compiler_fence();
+    __builtin_amdgcn_s_waitcnt(kWaitRing);
+    __builtin_amdgcn_s_barrier();
+    compiler_fence();
+    issue(ring((u + NRING - 1) % NRING), tile + NRING - 1);
+    if (MODE == kColMass && tile > 0 && wave == ((tile - 1) & (kSWaves - 1))) finish_cols(tile - 1);
     const int64_t tcol0 = col0 + (int64_t)tile * kTileTok;
-    bool colok[4];
-#pragma unroll
-    for (int nt = 0; nt < 4; ++nt) colok[nt] = tcol0 + nt * 16 + (lane & 15) < col_end;
     float cmass[4] = {0.f, 0.f, 0.f, 0.f};
 
+    // one tile: the whole 64-column score block of this wave first (MFMA), then
+    // the softmax arithmetic on it (VALU); without branches inside, the
+    // scheduler overlaps the two.  Masks are needed only on a ragged last tile
+    // or where keys can lie past a row's position.
+    auto tile_body = [&](auto mask_tag) {
+      constexpr bool MASK = decltype(mask_tag)::value;
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      floatx4 acc[4];
+      for (int hh = 0; hh < 2; ++hh) {
+      floatx4 acc[2][MT];
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) acc[nt] = floatx4{0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < 2; ++j) {
+        uint4 bf[KG];
 #pragma unroll
-      for (int kg = 0; kg < KG; ++kg)
+        for (int kg = 0; kg < KG; ++kg) bf[kg] = cur[tile_slot<T>((2 * hh + j) * 16 + (lane & 15), kg * 4 + (lane >> 4))];
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) acc[nt] = F::mma(qf[mt][kg], bf[nt][kg], acc[nt]);
-
-      // scores with the column and causal masks applied
-      float s[4][4];
+        for (int mt = 0; mt < MT; ++mt) {
+          floatx4 x = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int row = (wave * MT + mt) * 16 + 4 * (lane >> 4) + r;
-        const int64_t qpos = a.q_pos0 + row / G;
+          for (int kg = 0; kg < KG; ++kg) x = F::mma(qf[mt][kg], bf[kg], x);
+          acc[j][mt] = x;
+        }
+      }
+      if (MASK) {
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) {
-          bool ok = colok[nt];
-          if (CAUSAL) ok = ok && (a.key_off + tcol0 + nt * 16 + (lane & 15) <= qpos);
-          s[r][nt] = ok ? acc[nt][r] : -INFINITY;
+        for (int j = 0; j < 2; ++j) {
+          const int64_t col = tcol0 + (2 * hh + j) * 16 + (lane & 15);
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int row = (wave * MT + mt) * 16 + 4 * (lane >> 4) + r;
+              bool ok = col < col_end;
+              if (CAUSAL) ok = ok && (a.key_off + col <= a.q_pos0 + row / G);
+              acc[j][mt][r] = ok ? acc[j][mt][r] : -INFINITY;
+            }
         }
       }
 
       if (MODE == kRowStats) {
+        // lazy running maximum: move it only when the half-tile maximum exceeds
+        // it by more than 8 in log2 units (terms stay below 2^8)
+        float tmc[MT][4];
+        bool upd = false;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float mx = fmaxf(fmaxf(s[r][0], s[r][1]), fmaxf(s[r][2], s[r][3]));
-          float m = st_m[mt][r];
-          if (mx > m + thr) {
-            st_l[mt][r] *= fast_exp2((m - mx) * a.c);
-            m = mx;
-            st_m[mt][r] = m;
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            tmc[mt][r] = fmaxf(acc[0][mt][r], acc[1][mt][r]) * a.c;
+            upd |= tmc[mt][r] - st_mc[mt][r] > 8.0f;
           }
-          const float mc = m * a.c;
-          float add = 0.f;
+        if (__builtin_amdgcn_ballot_w64(upd)) {
 #pragma unroll
-          for (int nt = 0; nt < 4; ++nt) add += fast_exp2(__builtin_fmaf(s[r][nt], a.c, -mc));
-          st_l[mt][r] += add;
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (tmc[mt][r] - st_mc[mt][r] > 8.0f) {
+                st_l[mt][r] *= fast_exp2(st_mc[mt][r] - tmc[mt][r]);
+                st_mc[mt][r] = tmc[mt][r];
+              }
         }
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              st_l[mt][r] += fast_exp2(__builtin_fmaf(acc[j][mt][r], a.c, -st_mc[mt][r]));
       } else if (MODE == kColMass) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
+        for (int j = 0; j < 2; ++j)
 #pragma unroll
-          for (int nt = 0; nt < 4; ++nt)
-            cmass[nt] += fast_exp2(__builtin_fmaf(s[r][nt], a.c, -off[mt][r]));
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              cmass[2 * hh + j] += fast_exp2(__builtin_fmaf(acc[j][mt][r], a.c, -off[mt][r]));
       } else {  // kObsMatrix: group mean over the G rows of each query i
-        float p[4][4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-#pragma unroll
-          for (int nt = 0; nt < 4; ++nt) p[r][nt] = fast_exp2(__builtin_fmaf(s[r][nt], a.c, -off[mt][r]));
         const float invG = 1.0f / (float)G;
-        const int rbase = (wave * MT + mt) * 16 + 4 * (lane >> 4);
-        if (G == 1 || G == 2 || G == 4) {
 #pragma unroll
-          for (int r0 = 0; r0 < 4; r0 += G) {
-            const int i = (rbase + r0) / G;
+        for (int j = 0; j < 2; ++j) {
+          const int64_t col = tcol0 + (2 * hh + j) * 16 + (lane & 15);
+          const bool colok = col < col_end;
 #pragma unroll
-            for (int nt = 0; nt < 4; ++nt) {
-              float v = 0.f;
+          for (int mt = 0; mt < MT; ++mt) {
+            float p[4];
 #pragma unroll
-              for (int r = 0; r < G; ++r) v += p[r0 + r][nt];
-              const int64_t col = tcol0 + nt * 16 + (lane & 15);
-              if (i < a.lq && colok[nt]) a.obs[((size_t)sel * a.lq + i) * a.n_keys + col] = v * invG;
+            for (int r = 0; r < 4; ++r) p[r] = fast_exp2(__builtin_fmaf(acc[j][mt][r], a.c, -off[mt][r]));
+            const int rbase = (wave * MT + mt) * 16 + 4 * (lane >> 4);
+            if (G == 1 || G == 2 || G == 4) {
+#pragma unroll
+              for (int r0 = 0; r0 < 4; r0 += G) {
+                const int i = (rbase + r0) / G;
+                float v = 0.f;
+#pragma unroll
+                for (int r = 0; r < G; ++r) v += p[r0 + r];
+                if (i < a.lq && colok) a.obs[((size_t)sel * a.lq + i) * a.n_keys + col] = v * invG;
+              }
+            } else {  // G == 8: the 8 rows of a query span lane groups 2k and 2k + 1
+              const float v = add_xor16(p[0] + p[1] + p[2] + p[3]);
+              const int i = rbase / 8;
+              if (((lane >> 4) & 1) == 0 && i < a.lq && colok)
+                a.obs[((size_t)sel * a.lq + i) * a.n_keys + col] = v * invG;
             }
-          }
-        } else {  // G == 8: the 8 rows of a query span lane groups 2k and 2k + 1
-#pragma unroll
-          for (int nt = 0; nt < 4; ++nt) {
-            float v = p[0][nt] + p[1][nt] + p[2][nt] + p[3][nt];
-            v += shfl_xor(v, 16);
-            const int i = rbase / 8;
-            const int64_t col = tcol0 + nt * 16 + (lane & 15);
-            if (((lane >> 4) & 1) == 0 && i < a.lq && colok[nt])
-              a.obs[((size_t)sel * a.lq + i) * a.n_keys + col] = v * invG;
           }
         }
       }
-    }
+      }
+    };
+
+    const bool need_mask = tcol0 + kTileTok > col_end || (CAUSAL && a.key_off + tcol0 + kTileTok - 1 > qpos_min);
+    if (need_mask) tile_body(std::true_type{});
+    else tile_body(std::false_type{});
 
     if (MODE == kColMass) {
+      // sum over the four row groups of lanes; each wave leaves its partial in LDS
 #pragma unroll
       for (int nt = 0; nt < 4; ++nt) {
-        float v = cmass[nt];
-        v += shfl_xor(v, 16);
-        v += shfl_xor(v, 32);
-        if (lane < 16) s_col[wave][nt * 16 + lane] = v;
+        const float v = add_xor32(add_xor16(cmass[nt]));
+        if (lane < 16) s_col[par][wave][nt * 16 + lane] = v;
       }
-    }
-    if (tile + 1 < n_tiles) stage_store(buf ^ 1);
-    __syncthreads();
-    if (MODE == kColMass) {
-      if (threadIdx.x < kTileTok) {
-        const int t = threadIdx.x;
-        float v = 0.f;
-#pragma unroll
-        for (int w = 0; w < kSWaves; ++w) v += s_col[w][t];
-        const int64_t col = tcol0 + t;
-        if (col < col_end) a.colmass[(size_t)sel * a.n_keys + col] = v * (1.0f / (float)G);
-      }
-      // s_col is rewritten only after the next tile's barrier
     }
   }
+  }
+
+  if (MODE == kColMass) {
+    barrier_lds_only();
+    if (n_tiles > 0 && wave == ((n_tiles - 1) & (kSWaves - 1))) finish_cols(n_tiles - 1);
+  }
+
+  // the ring's trailing loads must land before the workgroup's LDS is released
+  __builtin_amdgcn_s_waitcnt(0);
+  compiler_fence();
 
   if (MODE == kRowStats) {
-    // merge the 16 lanes that share each row
+    // merge the 16 lanes that share each row (maxima in log2 units)
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const float m = st_m[mt][r];
+        const float m = st_mc[mt][r];
         const float M = max16(m);
-        const float lsum = sum16(st_l[mt][r] * fast_exp2((m - M) * a.c));
+        const float lsum = sum16(st_l[mt][r] * fast_exp2(m - M));
         const int row = (wave * MT + mt) * 16 + 4 * (lane >> 4) + r;
         if ((lane & 15) == 0)
           a.rowpart[((size_t)sel * a.n_colblk + cb) * RPAD + row] = make_float2(M, lsum);
@@ -291,26 +366,49 @@ __global__ __launch_bounds__(kSWaves * 64) void score_kernel(ScoreArgs a) {
   }
 }
 
+// Up to 256 query rows the body fits two waves per SIMD; 512 rows (MT = 8)
+// keep the compiler's own register budget rather than spill.
+template <typename T, int MT, int MODE, int G, bool CAUSAL>
+__global__ __launch_bounds__(kSWaves * 64) __attribute__((amdgpu_waves_per_eu(2)))
+void score_kernel(ScoreArgs a) {
+  score_body<T, MT, MODE, G, CAUSAL>(a);
+}
+template <typename T, int MODE, int G, bool CAUSAL>
+__global__ __launch_bounds__(kSWaves * 64) void score_kernel_wide(ScoreArgs a) {
+  score_body<T, 8, MODE, G, CAUSAL>(a);
+}
+
 // Merge the per-column-block row statistics: offset = m c + log2(l), +inf
-// for rows with no visible key and for padding rows.
-__global__ void rowstats_merge_kernel(const float2* __restrict__ part, int n_colblk, int R, int rpad,
-                                      float c, float* __restrict__ off) {
+// for rows with no visible key and for padding rows.  16 lanes share a row
+// and walk its column blocks with independent loads, then reduce over DPP.
+constexpr int kMergeRows = 16;    // rows per 256-thread workgroup
+__global__ __launch_bounds__(256) void rowstats_merge_kernel(const float2* __restrict__ part, int n_colblk,
+                                                             int R, int rpad, float* __restrict__ off) {
   const int sel = blockIdx.y;
-  const int row = blockIdx.x * blockDim.x + threadIdx.x;
-  if (row >= rpad) return;
-  float res = INFINITY;
-  if (row < R) {
-    const float2* p = part + (size_t)sel * n_colblk * rpad + row;
-    float M = kMInit;
-    for (int b = 0; b < n_colblk; ++b) M = fmaxf(M, p[(size_t)b * rpad].x);
-    float L = 0.f;
-    for (int b = 0; b < n_colblk; ++b) {
-      const float2 v = p[(size_t)b * rpad];
-      L += v.y * fast_exp2((v.x - M) * c);
+  const int row = blockIdx.x * kMergeRows + (threadIdx.x >> 4);
+  const int ln = threadIdx.x & 15;
+  const bool ok = row < R;
+  const float2* p = part + (size_t)sel * n_colblk * rpad + (ok ? row : 0);
+  float M = kMInit, L = 0.f;
+  constexpr int UNR = 8;
+  for (int b0 = ln; b0 < n_colblk; b0 += 16 * UNR) {
+    float2 v[UNR];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int b = b0 + 16 * u;
+      v[u] = (ok && b < n_colblk) ? p[(size_t)b * rpad] : make_float2(kMInit, 0.f);
     }
-    if (L > 0.f) res = M * c + __log2f(L);
+    float mb = M;
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) mb = fmaxf(mb, v[u].x);
+    L *= fast_exp2(M - mb);
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) L += v[u].y * fast_exp2(v[u].x - mb);
+    M = mb;
   }
-  off[(size_t)sel * rpad + row] = res;
+  const float M16 = max16(M);
+  L = sum16(L * fast_exp2(M - M16));
+  if (ln == 0 && row < rpad) off[(size_t)sel * rpad + row] = (ok && L > 0.f) ? M16 + __log2f(L) : INFINITY;
 }
 
 // ---------------------------------------------------------------------------
@@ -425,6 +523,105 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(const float* __restr
   for (int i = k + t; i < b; i += kTopkThreads) out[i] = -1;
 }
 
+
+// Same selection with the scores held in registers: thread t owns the
+// contiguous chunks [t * PER, (t + 1) * PER), loaded once; the four radix
+// passes only touch LDS (histogram) and registers.
+template <int PER>
+__global__ __launch_bounds__(kTopkThreads) void topk_reg_kernel(const float* __restrict__ S, int64_t n_chunks,
+                                                                 int k, int b, int32_t* __restrict__ idx_out) {
+  constexpr int NCOPY = 16;                // histogram copies (lane & 15): hot bins spread 16 ways
+  __shared__ int s_histc[NCOPY][256];
+  __shared__ int s_hist[256];
+  __shared__ int s_scan[kTopkThreads];
+  __shared__ uint32_t s_prefix;
+  __shared__ int s_remaining;
+  const int sel = blockIdx.x;
+  const float* Ss = S + (size_t)sel * n_chunks;
+  const int t = threadIdx.x;
+  const int64_t lo = (int64_t)t * PER;
+  uint32_t key[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) key[i] = lo + i < n_chunks ? ord_key(Ss[lo + i]) : 0u;   // 0: below every score
+  const int n_valid = (int)max<int64_t>(0, min<int64_t>(PER, n_chunks - lo));
+
+  uint32_t prefix = 0, mask = 0;
+  int remaining = k;
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    for (int i = t; i < NCOPY * 256; i += kTopkThreads) (&s_histc[0][0])[i] = 0;
+    __syncthreads();
+    const int cp = t & (NCOPY - 1);
+#pragma unroll
+    for (int i = 0; i < PER; ++i)
+      if (i < n_valid && (key[i] & mask) == prefix) atomicAdd(&s_histc[cp][(key[i] >> shift) & 255], 1);
+    __syncthreads();
+    if (t < 256) {
+      int v = 0;
+#pragma unroll
+      for (int c2 = 0; c2 < NCOPY; ++c2) v += s_histc[c2][t];
+      s_hist[t] = v;
+    }
+    __syncthreads();
+    if (t < 64) {
+      // wave 0 finds, from the top bin down, the bin where the count reaches `remaining`
+      int h[4], c4 = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) { h[i] = s_hist[255 - (4 * t + i)]; c4 += h[i]; }
+      // inclusive scan of c4 over the 64 lanes (bins 255 .. 0)
+      int incl = c4;
+      for (int off = 1; off < 64; off <<= 1) {
+        const int y = __shfl_up(incl, off);
+        if (t >= off) incl += y;
+      }
+      const int excl = incl - c4;
+      if (excl < remaining && incl >= remaining) {
+        int cum = excl, i = 0;
+        for (i = 0; i < 3; ++i) {
+          if (cum + h[i] >= remaining) break;
+          cum += h[i];
+        }
+        s_prefix = prefix | ((uint32_t)(255 - (4 * t + i)) << shift);
+        s_remaining = remaining - cum;
+      }
+    }
+    __syncthreads();
+    prefix = s_prefix;
+    remaining = s_remaining;
+    mask |= 255u << shift;
+    __syncthreads();
+  }
+  const uint32_t tau = prefix;
+  int n_eq = 0;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) n_eq += (i < n_valid && key[i] == tau);
+  int tot;
+  const int eq_before = block_exclusive_scan(n_eq, s_scan, &tot);
+  int n_take = 0;
+  {
+    int eb = eq_before;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      if (i >= n_valid) continue;
+      if (key[i] > tau) ++n_take;
+      else if (key[i] == tau) { if (eb < remaining) ++n_take; ++eb; }
+    }
+  }
+  int pos = block_exclusive_scan(n_take, s_scan, &tot);
+  int32_t* out = idx_out + (size_t)sel * b;
+  {
+    int eb = eq_before;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      if (i >= n_valid) continue;
+      bool take = false;
+      if (key[i] > tau) take = true;
+      else if (key[i] == tau) { take = eb < remaining; ++eb; }
+      if (take && pos < k) out[pos++] = (int32_t)(lo + i);
+    }
+  }
+  for (int i = k + t; i < b; i += kTopkThreads) out[i] = -1;
+}
 
 struct CompactArgs {
   const void* k;
@@ -636,9 +833,17 @@ static inline int rows_pad(int R) {
   const int mt = (R + 63) / 64;
   return (mt <= 1 ? 1 : mt <= 2 ? 2 : mt <= 4 ? 4 : 8) * 64;
 }
-constexpr int64_t kColBlockTokens = 512;
+// Score workgroups run in a single round: at most kScoreSlots of them (two per
+// compute unit, the residency their registers and LDS allow), each over whole
+// 64-column tiles and at least four of them.
+constexpr int64_t kScoreSlots = 512;
 
-int64_t score_colblocks(int64_t n_keys) { return (n_keys + kColBlockTokens - 1) / kColBlockTokens; }
+int64_t score_block_tokens(int64_t n_keys, int n_heads) {
+  const int64_t per_head = std::max<int64_t>(1, kScoreSlots / std::max(1, n_heads));
+  int64_t cb = (std::max<int64_t>(n_keys, 1) + per_head - 1) / per_head;
+  cb = (cb + kTileTok - 1) / kTileTok * kTileTok;
+  return std::max<int64_t>(cb, 4 * kTileTok);
+}
 
 struct SelectLayout {
   size_t rowpart, rowoff, colmass, chunks, total;
@@ -663,7 +868,7 @@ static hipError_t launch_score_mt(int mt, dim3 grid, hipStream_t s, const ScoreA
     case 1: hipLaunchKernelGGL((score_kernel<T, 1, MODE, G, CAUSAL>), grid, dim3(kSWaves * 64), 0, s, a); break;
     case 2: hipLaunchKernelGGL((score_kernel<T, 2, MODE, G, CAUSAL>), grid, dim3(kSWaves * 64), 0, s, a); break;
     case 4: hipLaunchKernelGGL((score_kernel<T, 4, MODE, G, CAUSAL>), grid, dim3(kSWaves * 64), 0, s, a); break;
-    case 8: hipLaunchKernelGGL((score_kernel<T, 8, MODE, G, CAUSAL>), grid, dim3(kSWaves * 64), 0, s, a); break;
+    case 8: hipLaunchKernelGGL((score_kernel_wide<T, MODE, G, CAUSAL>), grid, dim3(kSWaves * 64), 0, s, a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -691,7 +896,7 @@ hipError_t launch_select(int dtype, const SelectGeom& g, const void* q_obs, cons
   const int mt = rp / 64;
   ScoreArgs a{};
   a.q = q_obs; a.k = k; a.hkv = g.hkv; a.lq = g.l_obs; a.G = g.G; a.R = R; a.n = g.n;
-  a.key_off = 0; a.n_keys = g.n_keys; a.cb_tokens = kColBlockTokens; a.n_colblk = g.n_colblk;
+  a.key_off = 0; a.n_keys = g.n_keys; a.cb_tokens = g.cb_tokens; a.n_colblk = g.n_colblk;
   a.q_pos0 = g.n - g.l_obs; a.c = kLog2e / sqrtf((float)kD);
   for (int i = 0; i < g.n_sel; ++i) a.heads[i] = g.heads[i];
   a.rowpart = reinterpret_cast<float2*>(w + L.rowpart);
@@ -700,16 +905,27 @@ hipError_t launch_select(int dtype, const SelectGeom& g, const void* q_obs, cons
   const dim3 grid(g.n_colblk, g.n_sel);
   hipError_t e = launch_score_any<kRowStats, false>(dtype, g.G, mt, grid, stream, a);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(rowstats_merge_kernel, dim3((rp + 255) / 256, g.n_sel), dim3(256), 0, stream,
-                     a.rowpart, g.n_colblk, R, rp, a.c, reinterpret_cast<float*>(w + L.rowoff));
+  hipLaunchKernelGGL(rowstats_merge_kernel, dim3((rp + kMergeRows - 1) / kMergeRows, g.n_sel), dim3(256), 0, stream,
+                     a.rowpart, g.n_colblk, R, rp, reinterpret_cast<float*>(w + L.rowoff));
+  float* S = reinterpret_cast<float*>(w + L.chunks);
+  a.chunks = S;
+  a.n_chunks = g.n_chunks;
+  a.cs_fused = (kTileTok % g.cs == 0) ? g.cs : 0;
   e = launch_score_any<kColMass, false>(dtype, g.G, mt, grid, stream, a);
   if (e != hipSuccess) return e;
-  float* S = reinterpret_cast<float*>(w + L.chunks);
-  hipLaunchKernelGGL(chunk_max_kernel, dim3((unsigned)((g.n_chunks + 255) / 256), g.n_sel), dim3(256), 0,
-                     stream, a.colmass, g.n_keys, g.cs, g.n_chunks, S);
+  if (!a.cs_fused)
+    hipLaunchKernelGGL(chunk_max_kernel, dim3((unsigned)((g.n_chunks + 255) / 256), g.n_sel), dim3(256), 0,
+                       stream, a.colmass, g.n_keys, g.cs, g.n_chunks, S);
   const int k_eff = (int)(g.b < g.n_chunks ? g.b : g.n_chunks);
-  hipLaunchKernelGGL(topk_kernel, dim3(g.n_sel), dim3(kTopkThreads), 0, stream, S, g.n_chunks, k_eff,
-                     g.b, idx_out);
+  if (g.n_chunks <= 16 * kTopkThreads)
+    hipLaunchKernelGGL(topk_reg_kernel<16>, dim3(g.n_sel), dim3(kTopkThreads), 0, stream, S, g.n_chunks, k_eff,
+                       g.b, idx_out);
+  else if (g.n_chunks <= 32 * kTopkThreads)
+    hipLaunchKernelGGL(topk_reg_kernel<32>, dim3(g.n_sel), dim3(kTopkThreads), 0, stream, S, g.n_chunks, k_eff,
+                       g.b, idx_out);
+  else
+    hipLaunchKernelGGL(topk_kernel, dim3(g.n_sel), dim3(kTopkThreads), 0, stream, S, g.n_chunks, k_eff,
+                       g.b, idx_out);
   return hipGetLastError();
 }
 
@@ -763,7 +979,7 @@ hipError_t launch_score(int dtype, const ScoreGeom& g, const void* q_rows, const
   const int mt = rp / 64;
   ScoreArgs a{};
   a.q = q_rows; a.k = k; a.hkv = g.hkv; a.lq = g.lq; a.G = g.G; a.R = R; a.n = g.n;
-  a.key_off = g.l_init; a.n_keys = g.n_keys; a.cb_tokens = kColBlockTokens; a.n_colblk = g.n_colblk;
+  a.key_off = g.l_init; a.n_keys = g.n_keys; a.cb_tokens = g.cb_tokens; a.n_colblk = g.n_colblk;
   a.q_pos0 = g.q_pos0; a.c = kLog2e / sqrtf((float)kD);
   for (int i = 0; i < g.hkv; ++i) a.heads[i] = i;
   a.rowpart = reinterpret_cast<float2*>(w + L.rowpart);
@@ -773,8 +989,8 @@ hipError_t launch_score(int dtype, const ScoreGeom& g, const void* q_rows, const
   hipError_t e = g.causal ? launch_score_any<kRowStats, true>(dtype, g.G, mt, grid, stream, a)
                           : launch_score_any<kRowStats, false>(dtype, g.G, mt, grid, stream, a);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(rowstats_merge_kernel, dim3((rp + 255) / 256, g.hkv), dim3(256), 0, stream,
-                     a.rowpart, g.n_colblk, R, rp, a.c, reinterpret_cast<float*>(w + L.rowoff));
+  hipLaunchKernelGGL(rowstats_merge_kernel, dim3((rp + kMergeRows - 1) / kMergeRows, g.hkv), dim3(256), 0, stream,
+                     a.rowpart, g.n_colblk, R, rp, reinterpret_cast<float*>(w + L.rowoff));
   e = g.causal ? launch_score_any<kObsMatrix, true>(dtype, g.G, mt, grid, stream, a)
                : launch_score_any<kObsMatrix, false>(dtype, g.G, mt, grid, stream, a);
   if (e != hipSuccess) return e;
