@@ -16,6 +16,8 @@ of a decode step (K/V rows read + q + fp32 out), with the roofline of the
 decode kernel and the CPU oracle's rate on a bounded sample.
 """
 import argparse
+import csv
+import hashlib
 import json
 import math
 import os
@@ -30,6 +32,90 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 BF16_MFMA_PEAK_TFLOPS = 2500.0
 METRIC = "hybrid decode-attn µs/step + achieved HBM GB/s (% peak) at 128K ctx, 1 GPU"
+
+# HBM traffic of a decode step, from two rocprofv3 counter runs (FETCH_SIZE,
+# WRITE_SIZE) of this script, scaled by what the same counters read for a
+# streaming kernel of known size; valid only while the decode sources are the
+# ones the counters were taken on.
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_traffic_ctx128k_bf16.md")
+DECODE_SOURCES = ["paper_2608_30295_amd/csrc/decode.hip", "paper_2608_30295_amd/csrc/common.h",
+                  "paper_2608_30295_amd/csrc/internal.h", "paper_2608_30295_amd/csrc/api.cpp"]
+COPY_PROBE_BYTES = 1 << 30
+DECODE_KERNELS = ("decode_stream_mfma_kernel", "decode_combine_kernel")
+COPY_KERNEL = "bitwise_not"
+
+
+def decode_sources_sha256() -> str:
+    h = hashlib.sha256()
+    for rel in DECODE_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def recorded_traffic():
+    """Bytes per decode step from the committed counter summary, or None when
+    it is missing or was taken on other decode sources."""
+    try:
+        lines = open(TRAFFIC_SUMMARY).read().splitlines()
+    except OSError:
+        return None
+    kv = {}
+    for ln in lines:
+        if ln.startswith("- `") and "`: " in ln:
+            k, v = ln[3:].split("`: ", 1)
+            kv[k] = v.strip()
+    if kv.get("decode_sources_sha256") != decode_sources_sha256():
+        return None
+    try:
+        return int(kv["traffic_bytes_per_step"])
+    except (KeyError, ValueError):
+        return None
+
+
+def pmc_summary(fetch_dir: str, write_dir: str, algo_bytes: int, cmds) -> str:
+    """Markdown summary of the two counter runs (run on their CSV output)."""
+    def per_kernel(d, counter):
+        path = None
+        for root, _, files in os.walk(d):
+            for f in files:
+                if f.endswith("counter_collection.csv"):
+                    path = os.path.join(root, f)
+        if path is None:
+            raise SystemExit(f"no counter_collection.csv under {d}")
+        vals = {}
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            name = r["Kernel_Name"]
+            key = next((k for k in DECODE_KERNELS + (COPY_KERNEL,) if k in name), None)
+            if key is None:
+                continue
+            vals.setdefault(key, []).append(float(r["Counter_Value"]))
+        return {k: (len(v), sum(v) / len(v)) for k, v in vals.items()}
+
+    fetch = per_kernel(fetch_dir, "FETCH_SIZE")
+    write = per_kernel(write_dir, "WRITE_SIZE")
+    f_copy = COPY_PROBE_BYTES / (fetch[COPY_KERNEL][1] * 1024)
+    w_copy = COPY_PROBE_BYTES / (write[COPY_KERNEL][1] * 1024)
+    rd = sum(fetch[k][1] for k in DECODE_KERNELS if k in fetch) * 1024 * f_copy
+    wr = sum(write[k][1] for k in DECODE_KERNELS if k in write) * 1024 * w_copy
+    out = ["# HBM traffic of one decode step, ctx128k_bf16", "",
+           "Two counter runs of the benchmark (eager launches), one counter each:", ""]
+    out += [f"    {c}" for c in cmds]
+    out += ["", "| kernel | dispatches | FETCH_SIZE KiB (avg) | WRITE_SIZE KiB (avg) |", "|---|---|---|---|"]
+    for k in DECODE_KERNELS + (COPY_KERNEL,):
+        out.append(f"| {k} | {fetch.get(k, (0, 0))[0]} | {fetch.get(k, (0, 0))[1]:.1f} | {write.get(k, (0, 0))[1]:.1f} |")
+    out += ["", f"Streaming probe: `torch.bitwise_not` over {COPY_PROBE_BYTES} bytes (reads and writes that many);",
+            f"scale factors: read {f_copy:.4f}, write {w_copy:.4f} (bytes per counted byte).", "",
+            f"Decode step (stream + combine kernels): {rd / 1e6:.2f} MB read, {wr / 1e6:.3f} MB written; "
+            f"algorithmic bytes {algo_bytes / 1e6:.2f} MB; ratio {(rd + wr) / algo_bytes:.4f}.", "",
+            f"- `traffic_bytes_per_step`: {int(round(rd + wr))}",
+            f"- `read_bytes_per_step`: {int(round(rd))}",
+            f"- `write_bytes_per_step`: {int(round(wr))}",
+            f"- `algorithmic_bytes_per_step`: {algo_bytes}",
+            f"- `decode_sources_sha256`: {decode_sources_sha256()}", ""]
+    return "\n".join(out)
 
 
 def log(*a):
@@ -47,11 +133,20 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
     p.add_argument("--no-graph", action="store_true", help="launch steps eagerly instead of a HIP graph")
+    p.add_argument("--copy-probe", action="store_true",
+                   help=f"after timing, run a streaming kernel over {COPY_PROBE_BYTES} bytes (counter scale)")
+    p.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                   help="print the traffic summary of two rocprofv3 counter runs and exit (no GPU)")
+    p.add_argument("--pmc-cmd", action="append", default=[], help="command lines quoted in the summary")
+    p.add_argument("--algo-bytes", type=int, default=206757888, help="algorithmic bytes per step for the summary")
     return p.parse_args()
 
 
 def main():
     args = parse()
+    if args.pmc_summary:
+        print(pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.algo_bytes, args.pmc_cmd))
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the hybrid decode path is built and timed on a single "
               f"MI355X (requested --gpus {args.gpus}); run with --gpus 1.", file=sys.stderr)
@@ -242,6 +337,13 @@ def main():
     gbs = algo_bytes / (us * 1e-6) / 1e9
     log(f"[bench] decode {mode}: {us:.2f} us/step over {timed_steps} steps, {gbs:.1f} GB/s "
         f"({100 * gbs / HBM_PEAK_GBS:.1f}% of 8 TB/s), {n_layers} layer copies")
+    if args.copy_probe:
+        src = torch.empty(COPY_PROBE_BYTES // 2, dtype=torch.int16, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.bitwise_not(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
 
     # ---------------- CPU oracle on a bounded sample ----------------
     cpu = None
@@ -302,8 +404,10 @@ def main():
             "kv_fraction_of_full": round(kv_bytes_layer / (n * hkv * d * esz * 2), 4),
         },
         "roofline": {
-            "kernel": "decode_kernel<bf16,G=4>", "bound": "hbm", "achieved": round(gbs, 2),
-            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+            "kernel": "decode step: decode_stream_mfma_kernel<G=4> + decode_combine_kernel<G=4>",
+            "bound": "hbm", "achieved": round(gbs, 2),
+            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+            "traffic": recorded_traffic(),
         },
         "prefill": {
             "score_heads_us": round(t_cv, 1),

@@ -21,7 +21,7 @@ struct DecodeItem {
   int32_t t1;
 };
 
-constexpr int kDecodeWaves = 8;    // waves per decode workgroup
+constexpr int kDecodeWaves = 4;    // waves per decode workgroup
 constexpr int kDecodeStages = 4;   // register prefetch depth (fp32 path)
 constexpr int kDecodeStagesMfma = 3;   // register prefetch depth (bf16 MFMA path, 16-token stages)
 constexpr int kDecodeQuantum = 64; // tokens per workgroup load stage (16 per wave)
