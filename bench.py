@@ -133,6 +133,9 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
     p.add_argument("--no-graph", action="store_true", help="launch steps eagerly instead of a HIP graph")
+    p.add_argument("--no-next", action="store_true",
+                   help="skip the decode-time append timing and the retention sweep")
+    p.add_argument("--etas", default="0.5,0.25,0.1", help="retention ratios of the adaptive heads to sweep")
     p.add_argument("--copy-probe", action="store_true",
                    help=f"after timing, run a streaming kernel over {COPY_PROBE_BYTES} bytes (counter scale)")
     p.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -194,6 +197,24 @@ def main():
     log(f"[bench] cv={np.round(cv_h, 3).tolist()} consistent={heads} lens={lens_h.tolist()}")
 
     stream = torch.cuda.current_stream(dev)
+
+    # ------ retention below 1 in the adaptive heads: argtopk(C_chunk, n eta) of Algorithm 1 ------
+    eta_caches = []
+    if not args.no_next and adaptive:
+        ws_a = ck.workspace(ck.select_workspace(hq, hkv, wl.l_obs, n, wl.cs, len(adaptive)), dev)
+        for eta in [float(x) for x in args.etas.split(",") if x]:
+            ba = ck.adaptive_budget(n, wl.l_obs, wl.cs, eta)
+            idx_a = ck.select_critical(q_obs, k_full, adaptive, wl.cs, ba, ws=ws_a)
+            lens_a = lens.clone()
+            k_a, v_a = ck.compact_kv(k_full, v_full, adaptive, idx_a, wl.cs, wl.l_obs, lens_a)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(3):
+                ck.select_critical(q_obs, k_full, adaptive, wl.cs, ba, ws=ws_a)
+            e1.record(stream)
+            e1.synchronize()
+            eta_caches.append((eta, ba, k_a, v_a, lens_a.cpu().numpy(), e0.elapsed_time(e1) * 1e3 / 3))
 
     def time_it(fn, reps):
         fn()
@@ -345,6 +366,89 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    # ---------------- decode-time append and the retention sweep ----------------
+    next_res = None
+    if not args.no_next:
+        next_res = {}
+        # one token appended to all 8 views (capacity: 128 rows of headroom per view)
+        room = 128
+        bufs = [torch.empty((L + room, d), dtype=k_c.dtype, device=dev) for L in view_len for _ in (0, 1)]
+        tab = ck.kv_table([(bufs[2 * i].data_ptr(), bufs[2 * i + 1].data_ptr()) for i in range(hkv)], dev)
+        capa = torch.tensor([L + room for L in view_len], dtype=torch.int64, device=dev)
+        lens_g = torch.tensor(view_len, dtype=torch.int64, device=dev)
+        row = torch.zeros((1, hkv, d), dtype=k_c.dtype, device=dev)
+        flag = torch.zeros(1, dtype=torch.int32, device=dev)
+        ck.append_kv(tab, capa, lens_g, row, row, flag)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(100):
+            ck.append_kv(tab, capa, lens_g, row, row, flag)
+        e1.record(stream)
+        e1.synchronize()
+        assert int(flag.item()) == 0 and lens_g.cpu().tolist() == [L + 101 for L in view_len]
+        next_res["append_kv_us"] = round(e0.elapsed_time(e1) * 1e3 / 100, 2)
+        del bufs, tab
+        # decode steps with the adaptive heads compacted to eta of their chunks (graph replays)
+        sweep = []
+        for eta, ba, k_a, v_a, lens_a, sel_us in eta_caches:
+            vl = [int(lens_a[h]) for h in range(hkv)]
+            bytes_step = sum(vl) * d * esz * 2 + hq * d * esz + hq * d * 4
+            n_cp = max(4, math.ceil(1.0e9 / (sum(vl) * d * esz * 2)))
+            cps = []
+            for li in range(n_cp):
+                ka_e, va_e = k_a.clone(), v_a.clone()
+                kc_e, vc_e = layers[li % n_layers][2], layers[li % n_layers][3]
+                pairs = []
+                for h in range(hkv):
+                    t_ = (kc_e[heads.index(h)], vc_e[heads.index(h)]) if h in heads else \
+                        (ka_e[adaptive.index(h)], va_e[adaptive.index(h)])
+                    pairs.append((t_[0].data_ptr(), t_[1].data_ptr()))
+                cps.append((ka_e, va_e, ck.kv_table(pairs, dev)))
+            plan_e = ck.decode_plan(np.array([vl], dtype=np.int64), hq, hkv, dev)
+            lens_e = torch.from_numpy(lens_a).to(dev)
+            out_e = torch.empty_like(out)
+
+            def step_e(t, st):
+                check(lib().catekv_decode_attn(dtc, _lib.ctypes.byref(plan_e.plan), qs[t % nq].data_ptr(),
+                                               cps[t % n_cp][2].data_ptr(), lens_e.data_ptr(), 1, hq, hkv, d,
+                                               scale, out_e.data_ptr(), None, plan_e.ws.data_ptr(),
+                                               plan_e.ws.numel(), st.cuda_stream))
+            for t in range(5):
+                step_e(t, stream)
+            torch.cuda.synchronize()
+            cyc = min(64, n_cp * nq // math.gcd(n_cp, nq))
+            s3 = torch.cuda.Stream(device=dev)
+            s3.wait_stream(stream)
+            ge = torch.cuda.CUDAGraph()
+            with torch.cuda.stream(s3):
+                ge.capture_begin()
+                for t in range(cyc):
+                    step_e(t, s3)
+                ge.capture_end()
+            stream.wait_stream(s3)
+            step_e(cyc - 1, stream)
+            torch.cuda.synchronize()
+            ref_e = out_e.clone()
+            ge.replay()
+            torch.cuda.synchronize()
+            same = torch.equal(out_e, ref_e)
+            reps = max(1, round(args.steps / cyc))
+            e0.record(stream)
+            for _ in range(reps):
+                ge.replay()
+            e1.record(stream)
+            e1.synchronize()
+            us_e = e0.elapsed_time(e1) * 1e3 / (reps * cyc)
+            sweep.append({"eta": eta, "adaptive_chunks": ba, "view_lengths": vl, "bytes_per_step": int(bytes_step),
+                          "us_per_step": round(us_e, 2), "gbs": round(bytes_step / (us_e * 1e-6) / 1e9, 1),
+                          "layer_copies": n_cp, "select_adaptive_us": round(sel_us, 1),
+                          "graph_matches_eager": bool(same)})
+            log(f"[bench] eta {eta}: {ba} chunks per adaptive head, {us_e:.2f} us/step "
+                f"({bytes_step / 1e6:.1f} MB), adaptive selection {sel_us:.1f} us")
+            del cps, ge
+        next_res["retention_sweep"] = sweep
+
     # ---------------- CPU oracle on a bounded sample ----------------
     cpu = None
     if not args.no_cpu_baseline:
@@ -418,6 +522,7 @@ def main():
             "select_tflops": round(sel_flops / (t_sel * 1e-6) / 1e12, 1),
         },
         "cpu_baseline": cpu,
+        "next": next_res,
     }
     print(json.dumps(res), flush=True)
 

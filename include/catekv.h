@@ -202,6 +202,35 @@ int catekv_decode_attn(int dtype, const catekv_decode_plan_t* plan, const void* 
                        int batch, int hq, int hkv, int d, float scale,
                        float* out, float* lse, void* ws, size_t ws_bytes, void* stream);
 
+/* ------------------------------------------------------------------------ */
+/* Decode-time KV append -- the generation loop around Algorithm 1's decoding */
+/* stage.                                                                     */
+/* ------------------------------------------------------------------------ */
+
+/* Appends the newest token's key and value to every (sequence, KV head)
+ * view.  For each view bh with L = lens[bh] and 0 <= L < capacity[bh]:
+ *   K_bh[L] = k_new[bh],  V_bh[L] = v_new[bh],  lens[bh] = L + 1.
+ * The token enters the compact cache of a consistent head and the full cache
+ * of an adaptive head alike (the decoding stage attends over every token
+ * generated so far, and no stage of Algorithm 1 drops one).  A view with
+ * L >= capacity[bh] or L < 0 is left unchanged and sets *overflow = 1 when
+ * overflow is not NULL; the library never clears *overflow.
+ * A decode plan built once with max_len = capacity serves every step of the
+ * growing cache: catekv_decode_attn reads lens on the device and never looks
+ * past them.  Run on the stream of the decode steps, so that each step sees
+ * the tokens appended before it.
+ * kv        [batch][hkv] catekv_kv_ptrs, device; each view's rows must be
+ *           writable and number capacity[bh]
+ * capacity  [batch][hkv] int64, device: rows allocated per view
+ * lens      [batch][hkv] int64, device: read and bumped on the device
+ * k_new, v_new  [batch][hkv][d] (dtype)
+ * overflow  int32, device, or NULL
+ * Errors: INVALID_ARG for null pointers, batch < 1, hkv < 1 or d != 128;
+ * UNSUPPORTED for an unknown dtype. */
+int catekv_append_kv(int dtype, const catekv_kv_ptrs* kv, const int64_t* capacity, int64_t* lens,
+                     const void* k_new, const void* v_new, int batch, int hkv, int d,
+                     int32_t* overflow, void* stream);
+
 /* Message describing the last failure on the calling host thread. */
 const char* catekv_last_error(void);
 

@@ -26,6 +26,12 @@ Passages followed
 * Section 3.2, Eq. 5 and the reference-based static identification paragraph:
   consistent iff ``S > Gamma(r)``; model-wise head types from the frequency
   with which a head is classified consistent across reference samples.
+* Algorithm 1, adaptive branch: ``argtopk(C_chunk, n eta)`` (retention
+  below 1) and ``Retrieval(q, cache_k, cache_v)``, "all or query-aware";
+  Section 4 integrates page-based query-aware retrieval (Quest) in the
+  adaptive heads.
+* Figure 4 and its discussion: attention recall of the consistent,
+  streaming, query-aware and top-k patterns under one sparse budget.
 
 Readings where the paper is silent or ambiguous
 -----------------------------------------------
@@ -49,6 +55,15 @@ Readings where the paper is silent or ambiguous
   sample with distinct scores, ``H - 1 - floor((H - 1) r)``: the heads with
   the highest consistency frequency, ties broken by the higher mean score and
   then the lower head index.
+* New tokens of the generation loop join every view, compact or full; the
+  paper does not say where a token generated after prefill goes.
+* ``argtopk(C_chunk, n eta)`` counts chunks: ``ceil(eta * ceil((n - L_obs) / cs))``.
+* Query-aware retrieval uses chunks of cs rows as pages with per-page
+  elementwise key minima and maxima (the Quest bound); with GQA a page's score
+  is the largest bound over the group's query heads.
+* Attention recall is the share of the full softmax mass of a decode query
+  that falls on the kept rows; the streaming pattern keeps a few initial
+  rows plus the most recent ones.
 
 Parity status
 -------------
@@ -309,3 +324,91 @@ def static_head_types(scores: np.ndarray, r: float) -> np.ndarray:
     out = np.zeros(H, dtype=bool)
     out[order[:n_cons]] = True
     return out
+
+
+# --------------------------------------------------------------------------
+# Around Algorithm 1's decoding stage: the generation loop, adaptive
+# retention below 1, query-aware retrieval in adaptive heads (the
+# "CateKV + Quest" integration of Section 4) and the attention-recall
+# comparison of Figure 4.
+# --------------------------------------------------------------------------
+
+def append_token(k_view: np.ndarray, v_view: np.ndarray, k_new: np.ndarray, v_new: np.ndarray,
+                 capacity: int) -> Tuple[np.ndarray, np.ndarray, bool]:
+    """One generated token joins a cache view (compact or full alike) while
+    the view holds fewer than ``capacity`` rows.  Returns (k, v, appended)."""
+    if k_view.shape[0] >= capacity:
+        return k_view, v_view, False
+    return (np.concatenate([k_view, k_new[None, :]]), np.concatenate([v_view, v_new[None, :]]), True)
+
+
+def adaptive_budget(n: int, l_obs: int, cs: int, eta: float) -> int:
+    """Chunk budget of an adaptive head, ``argtopk(C_chunk, n eta)`` of
+    Algorithm 1 read as a chunk count: ``ceil(eta * ceil((n - l_obs) / cs))``.
+    eta = 1 keeps every chunk (the whole cache)."""
+    nc = -(-(n - l_obs) // cs)
+    return int(math.ceil(eta * nc - 1e-12))
+
+
+def page_bounds(k: np.ndarray, cs: int) -> Tuple[np.ndarray, np.ndarray]:
+    """Per chunk of cs rows (aligned at 0, last one partial): elementwise
+    minimum and maximum of the keys, the page metadata of query-aware
+    retrieval."""
+    n, d = k.shape
+    nc = -(-n // cs)
+    kmin = np.zeros((nc, d))
+    kmax = np.zeros((nc, d))
+    for c in range(nc):
+        rows = k[c * cs:min((c + 1) * cs, n)]
+        kmin[c] = rows.min(axis=0)
+        kmax[c] = rows.max(axis=0)
+    return kmin, kmax
+
+
+def page_scores(q_group: np.ndarray, kmin: np.ndarray, kmax: np.ndarray) -> np.ndarray:
+    """Upper bound of q . k over each page, ``sum_d max(q_d kmin_d, q_d kmax_d)``,
+    for each query head of the group; a page's score is the largest bound
+    over the group's heads (it may matter to any of them)."""
+    best = np.full(kmin.shape[0], -np.inf)
+    for q in q_group:
+        ub = np.maximum(kmin * q[None, :], kmax * q[None, :]).sum(axis=1)
+        best = np.maximum(best, ub)
+    return best
+
+
+def retrieve_pages(q_group: np.ndarray, k: np.ndarray, cs: int, n_pages: int) -> np.ndarray:
+    """The n_pages pages with the highest scores (ties to the lower index),
+    ascending: the query-aware Retrieval(q, cache_k, cache_v) of an adaptive
+    head."""
+    kmin, kmax = page_bounds(k, cs)
+    return argtopk_ascending(page_scores(q_group, kmin, kmax), n_pages)
+
+
+def attention_recall(q: np.ndarray, k: np.ndarray, keep: np.ndarray, scale: float) -> float:
+    """Share of the full attention mass of query q that falls on the kept
+    rows."""
+    w = softmax_rows(((k @ q) * scale)[None, :])[0]
+    return float(w[np.asarray(keep, dtype=np.int64)].sum())
+
+
+def streaming_keep(n: int, budget: int, n_sink: int) -> np.ndarray:
+    """Rows of the streaming pattern: the first n_sink rows and the most
+    recent ones, budget rows in all."""
+    if budget >= n:
+        return np.arange(n)
+    return np.concatenate([np.arange(min(n_sink, budget)), np.arange(n - (budget - min(n_sink, budget)), n)])
+
+
+def topk_keep(q: np.ndarray, k: np.ndarray, budget: int, scale: float) -> np.ndarray:
+    """Rows of the upper-bound pattern: the budget rows with the largest
+    attention weights for this query."""
+    s = (k @ q) * scale
+    order = np.lexsort((np.arange(s.shape[0]), -s))
+    return np.sort(order[:min(budget, s.shape[0])])
+
+
+def chunk_rows(n: int, cs: int, pages: np.ndarray) -> np.ndarray:
+    """Rows of the given chunks, ascending."""
+    pages = np.sort(np.asarray(pages, dtype=np.int64))
+    return np.concatenate([np.arange(c * cs, min((c + 1) * cs, n)) for c in pages]) if pages.size else \
+        np.zeros(0, dtype=np.int64)

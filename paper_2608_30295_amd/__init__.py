@@ -6,6 +6,8 @@ The compute lives in ``libcatekv.so`` (HIP kernels behind the C ABI of
 from ._lib import CateKVError, LIB_PATH, lib  # noqa: F401
 from .binding import (  # noqa: F401
     DecodePlan,
+    adaptive_budget,
+    append_kv,
     classify_heads,
     compact_kv,
     decode_attn,

@@ -55,6 +55,8 @@ SIGNATURES = {
     "catekv_decode_attn": (c_int, [c_int, ctypes.POINTER(DecodePlanT), c_void_p, c_void_p, c_void_p, c_int,
                                    c_int, c_int, c_int, c_float, c_void_p, c_void_p, c_void_p, c_size,
                                    c_void_p]),
+    "catekv_append_kv": (c_int, [c_int, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_int, c_int, c_int,
+                                 c_void_p, c_void_p]),
     "catekv_last_error": (ctypes.c_char_p, []),
     "catekv_version": (ctypes.c_char_p, []),
 }

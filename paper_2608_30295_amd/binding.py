@@ -185,3 +185,29 @@ def decode_attn(plan: DecodePlan, q: torch.Tensor, kv: torch.Tensor, lens: torch
                                    lse.data_ptr() if lse is not None else None, plan.ws.data_ptr(),
                                    plan.ws.numel(), _stream(q.device)))
     return out, lse
+
+
+def append_kv(kv: torch.Tensor, capacity: torch.Tensor, lens: torch.Tensor, k_new: torch.Tensor,
+              v_new: torch.Tensor, overflow: Optional[torch.Tensor] = None) -> None:
+    """Appends the newest token's K/V rows to every view of the kv table and
+    bumps lens on the device.  capacity, lens: int64 [B][Hkv] on the GPU;
+    k_new, v_new [B][Hkv][d]; overflow: int32 [1] on the GPU (set to 1 when a
+    view is full) or None."""
+    _need_cuda(kv, capacity, lens, k_new, v_new)
+    B, hkv, d = k_new.shape
+    if v_new.shape != k_new.shape or v_new.dtype != k_new.dtype:
+        raise ValueError("k_new and v_new must have the same shape and dtype")
+    if capacity.numel() != B * hkv or lens.numel() != B * hkv or kv.shape[0] != B * hkv:
+        raise ValueError("kv, capacity and lens must have B * Hkv entries")
+    check(lib().catekv_append_kv(_dtype_code(k_new), kv.data_ptr(), capacity.data_ptr(), lens.data_ptr(),
+                                 k_new.data_ptr(), v_new.data_ptr(), B, hkv, d,
+                                 overflow.data_ptr() if overflow is not None else None,
+                                 _stream(k_new.device)))
+
+
+def adaptive_budget(n: int, l_obs: int, cs: int, eta: float) -> int:
+    """Chunk budget of an adaptive head for retention ratio eta (Algorithm 1,
+    argtopk(C_chunk, n eta) counted in chunks): ceil(eta * ceil((n - l_obs) / cs)).
+    eta = 1 keeps every chunk, i.e. the original cache."""
+    nc = -(-(n - l_obs) // cs)
+    return int(math.ceil(eta * nc - 1e-12))

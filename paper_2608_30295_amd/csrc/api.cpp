@@ -424,4 +424,25 @@ int catekv_decode_attn(int dtype, const catekv_decode_plan_t* plan, const void* 
   return ok();
 }
 
+int catekv_append_kv(int dtype, const catekv_kv_ptrs* kv, const int64_t* capacity, int64_t* lens,
+                     const void* k_new, const void* v_new, int batch, int hkv, int d, int32_t* overflow,
+                     void* stream) {
+  if (!valid_dtype(dtype)) return fail(CATEKV_ERR_UNSUPPORTED, "dtype %d unsupported", dtype);
+  if (!kv || !capacity || !lens || !k_new || !v_new) return fail(CATEKV_ERR_INVALID_ARG, "null tensor pointer");
+  if (batch < 1 || hkv < 1) return fail(CATEKV_ERR_INVALID_ARG, "batch=%d hkv=%d must be >= 1", batch, hkv);
+  if (d != catekv::kD) return fail(CATEKV_ERR_INVALID_ARG, "d=%d unsupported (d must be %d)", d, catekv::kD);
+  if ((int64_t)batch * hkv > (int64_t)INT32_MAX) return fail(CATEKV_ERR_INVALID_ARG, "batch * hkv too large");
+  catekv::AppendArgs a{};
+  a.kv = kv;
+  a.capacity = capacity;
+  a.lens = lens;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.overflow = overflow;
+  a.n_views = batch * hkv;
+  hipError_t e = catekv::launch_append(dtype, a, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "append_kv launch");
+  return ok();
+}
+
 }  // extern "C"

@@ -640,6 +640,42 @@ int decode_blocks_per_cu(int dtype, int G) {
   return 1;
 }
 
+// Appends the newest token of every view: one 64-thread workgroup per view,
+// one 16-byte piece of the K row or of the V row per thread.  The length is
+// bumped only after every thread has read it.
+template <typename T>
+__global__ __launch_bounds__(64) void append_kv_kernel(AppendArgs a) {
+  constexpr int kPieces = kD * (int)sizeof(T) / 16;   // 16-byte pieces per row
+  static_assert(2 * kPieces <= 64, "one thread per piece of the K and V rows");
+  const int bh = blockIdx.x;
+  const int64_t L = a.lens[bh];
+  if (L < 0 || L >= a.capacity[bh]) {
+    if (threadIdx.x == 0 && a.overflow) *a.overflow = 1;
+    return;
+  }
+  const int t = threadIdx.x;
+  const size_t row = (size_t)kD * sizeof(T);
+  const catekv_kv_ptrs p = a.kv[bh];
+  if (t < 2 * kPieces) {
+    const bool is_k = t < kPieces;
+    const int piece = is_k ? t : t - kPieces;
+    const char* src = reinterpret_cast<const char*>(is_k ? a.k_new : a.v_new) + (size_t)bh * row + piece * 16;
+    char* dst = reinterpret_cast<char*>(const_cast<void*>(is_k ? p.k : p.v)) + (size_t)L * row + piece * 16;
+    *reinterpret_cast<uint4*>(dst) = ldg16(src);
+  }
+  __syncthreads();
+  if (t == 0) a.lens[bh] = L + 1;
+}
+
+hipError_t launch_append(int dtype, const AppendArgs& a, hipStream_t stream) {
+  if (a.n_views <= 0) return hipSuccess;
+  if (dtype == CATEKV_BF16)
+    hipLaunchKernelGGL(append_kv_kernel<uint16_t>, dim3(a.n_views), dim3(64), 0, stream, a);
+  else
+    hipLaunchKernelGGL(append_kv_kernel<float>, dim3(a.n_views), dim3(64), 0, stream, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_decode(int dtype, int G, const DecodeArgs& a, hipStream_t stream) {
 #define CATEKV_DEC(T, GG) \
   if (G == GG) return launch_t<T, GG>(a, stream);

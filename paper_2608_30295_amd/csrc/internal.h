@@ -54,6 +54,18 @@ struct DecodeArgs {
 int decode_blocks_per_cu(int dtype, int G);
 hipError_t launch_decode(int dtype, int G, const DecodeArgs& a, hipStream_t stream);
 
+// ---- decode-time KV append ------------------------------------------------
+struct AppendArgs {
+  const catekv_kv_ptrs* kv;
+  const int64_t* capacity;
+  int64_t* lens;
+  const void* k_new;
+  const void* v_new;
+  int32_t* overflow;        // may be null
+  int n_views;
+};
+hipError_t launch_append(int dtype, const AppendArgs& a, hipStream_t stream);
+
 // ---- critical-token selection ------------------------------------------
 struct SelectGeom {
   int hq, hkv, G, l_obs, cs, n_sel, b;

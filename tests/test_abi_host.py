@@ -28,7 +28,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 11
+    assert len(names) == 12
     L = ck.lib()
     for n in names:
         assert hasattr(L, n), n
@@ -161,3 +161,24 @@ def test_classify_counts_for_eight_heads():
 def test_classify_rejects_bad_ratio():
     with pytest.raises(ck.CateKVError):
         ck.classify_heads(np.ones((1, 4), dtype=np.float32), 1.0)
+
+
+def test_append_kv_rejects_bad_arguments():
+    L = ck.lib()
+    args = dict(kv=FAKE, cap=FAKE, lens=FAKE, k=FAKE, v=FAKE)
+
+    def call(dtype=1, batch=1, hkv=2, d=128, **kw):
+        a = {**args, **kw}
+        return _status_and_msg(L.catekv_append_kv(dtype, a["kv"], a["cap"], a["lens"], a["k"], a["v"],
+                                                  batch, hkv, d, None, None))
+
+    rc, msg = call(lens=None)
+    assert rc == _lib.CATEKV_ERR_INVALID_ARG and "null" in msg
+    rc, _ = call(batch=0)
+    assert rc == _lib.CATEKV_ERR_INVALID_ARG
+    rc, _ = call(hkv=0)
+    assert rc == _lib.CATEKV_ERR_INVALID_ARG
+    rc, msg = call(d=64)
+    assert rc == _lib.CATEKV_ERR_INVALID_ARG and "d=64" in msg
+    rc, _ = call(dtype=7)
+    assert rc == _lib.CATEKV_ERR_UNSUPPORTED

@@ -1,0 +1,149 @@
+"""GPU parity of the extensions around the core path: the decode-time KV
+append of a generation loop, adaptive retention below 1 and query-aware
+retrieval in the adaptive heads, each against the oracle."""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2608_30295_amd as ck
+import synth
+from gpu_util import DEV, assert_rows_close, f64, to_dev, to_host_storage
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _storage(x, dtype):
+    return synth.f32_to_bf16_bits(x) if dtype == "bf16" else x.astype(np.float32)
+
+
+# ------------------------------------------------------------ KV append
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_append_then_decode_growing_cache(dtype):
+    """A generation loop: every step appends one token to every view (compact
+    or full alike) and decodes over the grown caches with one plan built at
+    capacity; a view that reaches capacity stops growing and raises the
+    overflow flag."""
+    rng = np.random.default_rng(21)
+    B, hq, hkv, d, steps = 2, 8, 2, 128, 20
+    lens0 = np.array([100, 2500, 0, 37], dtype=np.int64)
+    cap = lens0 + np.array([24, 24, 24, 5])
+    say(f"append/decode {dtype}: lens {lens0.tolist()} capacity {cap.tolist()}")
+    host_k, host_v, dev_k, dev_v = [], [], [], []
+    for L, C in zip(lens0, cap):
+        k = _storage(rng.standard_normal((C, d), dtype=np.float32), dtype)
+        v = _storage(rng.standard_normal((C, d), dtype=np.float32), dtype)
+        host_k.append(k[:L].copy())
+        host_v.append(v[:L].copy())
+        dev_k.append(to_dev(k))          # rows past L hold stale data the decode must never read
+        dev_v.append(to_dev(v))
+    table = ck.kv_table([(k.data_ptr(), v.data_ptr()) for k, v in zip(dev_k, dev_v)], DEV)
+    capacity = torch.from_numpy(cap).to(DEV)
+    lens = torch.from_numpy(lens0.copy()).to(DEV)
+    overflow = torch.zeros(1, dtype=torch.int32, device=DEV)
+    plan = ck.decode_plan(cap.reshape(B, hkv), hq, hkv, DEV, split_tokens=256)
+    for t in range(steps):
+        k_new = _storage(rng.standard_normal((B, hkv, d), dtype=np.float32), dtype)
+        v_new = _storage(rng.standard_normal((B, hkv, d), dtype=np.float32), dtype)
+        ck.append_kv(table, capacity, lens, to_dev(k_new), to_dev(v_new), overflow)
+        for i in range(B * hkv):
+            host_k[i], host_v[i], _ = O.append_token(host_k[i], host_v[i], k_new.reshape(-1, d)[i],
+                                                     v_new.reshape(-1, d)[i], int(cap[i]))
+        q = _storage(rng.standard_normal((B, hq, d), dtype=np.float32), dtype)
+        out, lse = ck.decode_attn(plan, to_dev(q), table, lens.view(B, hkv))
+        torch.cuda.synchronize()
+        assert lens.cpu().numpy().tolist() == [h.shape[0] for h in host_k]
+        out, lse = out.cpu().numpy(), lse.cpu().numpy()
+        for b in range(B):
+            views = [(f64(host_k[b * hkv + h]), f64(host_v[b * hkv + h])) for h in range(hkv)]
+            o_ref, l_ref = O.decode_gqa(f64(q)[b], views)
+            assert_rows_close(out[b], o_ref, dtype, f"step {t} b={b}")
+            np.testing.assert_allclose(lse[b], l_ref, atol=1e-4, rtol=0)
+    assert int(overflow.item()) == 1
+    assert lens.cpu().numpy().tolist() == (lens0 + np.minimum(steps, cap - lens0)).tolist()
+    for i in range(B * hkv):
+        L = host_k[i].shape[0]
+        assert np.array_equal(to_host_storage(dev_k[i])[:L], host_k[i])
+        assert np.array_equal(to_host_storage(dev_v[i])[:L], host_v[i])
+
+
+def test_append_without_overflow_leaves_flag_clear():
+    rng = np.random.default_rng(22)
+    k = torch.zeros(3, 128, dtype=torch.bfloat16, device=DEV)
+    v = torch.zeros(3, 128, dtype=torch.bfloat16, device=DEV)
+    table = ck.kv_table([(k.data_ptr(), v.data_ptr())], DEV)
+    cap = torch.tensor([3], dtype=torch.int64, device=DEV)
+    lens = torch.tensor([1], dtype=torch.int64, device=DEV)
+    flag = torch.zeros(1, dtype=torch.int32, device=DEV)
+    row = synth.f32_to_bf16_bits(rng.standard_normal((1, 1, 128), dtype=np.float32))
+    ck.append_kv(table, cap, lens, to_dev(row), to_dev(row), flag)
+    ck.append_kv(table, cap, lens, to_dev(row), to_dev(row), flag)
+    torch.cuda.synchronize()
+    assert int(lens.item()) == 3 and int(flag.item()) == 0
+    ck.append_kv(table, cap, lens, to_dev(row), to_dev(row), None)     # full: unchanged, no flag to set
+    torch.cuda.synchronize()
+    assert int(lens.item()) == 3
+    assert np.array_equal(to_host_storage(k)[1], row[0, 0]) and np.array_equal(to_host_storage(k)[2], row[0, 0])
+
+
+# --------------------------------------------- adaptive retention below 1
+
+@pytest.mark.parametrize("eta", [0.5, 0.3, 0.05])
+def test_retention_below_one(eta):
+    """Adaptive heads keep ceil(eta * chunks) chunks (argtopk(C_chunk, n eta)
+    of Algorithm 1) through the same selection and compaction kernels;
+    decoding then runs over compact views for every head."""
+    wl = synth.WORKLOADS["ctx32k_bf16"].scaled(n=20000 + 64 + 5)
+    seq = synth.make_sequence(wl)
+    n, G = seq.n, wl.group
+    adaptive, consistent = [0, 3, 6], [1, 2, 4, 5, 7]
+    ba = ck.adaptive_budget(n, wl.l_obs, wl.cs, eta)
+    assert ba == O.adaptive_budget(n, wl.l_obs, wl.cs, eta)
+    say(f"retention eta={eta}: {ba} of {-(-(n - wl.l_obs) // wl.cs)} chunks per adaptive head")
+    q_obs, k, v = to_dev(seq.q_obs), to_dev(seq.k), to_dev(seq.v)
+    lens = torch.full((wl.hkv,), n, dtype=torch.int64, device=DEV)
+    idx_c = ck.select_critical(q_obs, k, consistent, wl.cs, wl.chunk_budget)
+    kc, vc = ck.compact_kv(k, v, consistent, idx_c, wl.cs, wl.l_obs, lens)
+    idx_a = ck.select_critical(q_obs, k, adaptive, wl.cs, ba)
+    ka, va = ck.compact_kv(k, v, adaptive, idx_a, wl.cs, wl.l_obs, lens)
+    torch.cuda.synchronize()
+    idx_a_h, idx_c_h = idx_a.cpu().numpy(), idx_c.cpu().numpy()
+    qf, scale = f64(seq.q_obs), 1 / math.sqrt(128)
+    from gpu_util import check_topk
+    for s, h in enumerate(adaptive):
+        sc = O.chunk_scores(qf[h * G:(h + 1) * G], f64(seq.k[h:h + 1]), 0, G, wl.l_obs, wl.cs, scale)
+        check_topk(idx_a_h[s], sc, ba)
+    ka_h, va_h = to_host_storage(ka), to_host_storage(va)
+    lens_h = lens.cpu().numpy()
+    rows = {}
+    for heads_, idx_h, kk, vv in ((adaptive, idx_a_h, ka_h, va_h), (consistent, idx_c_h, None, None)):
+        for s, h in enumerate(heads_):
+            sel = idx_h[s][idx_h[s] >= 0]
+            rows[h] = O.compact_rows(n, wl.l_obs, wl.cs, sel)
+            assert lens_h[h] == rows[h].size
+            if kk is not None:
+                assert np.array_equal(kk[s][:rows[h].size], seq.k[h][rows[h]])
+                assert np.array_equal(vv[s][:rows[h].size], seq.v[h][rows[h]])
+    pairs, maxlen = [], []
+    for h in range(wl.hkv):
+        kt, vt = (ka[adaptive.index(h)], va[adaptive.index(h)]) if h in adaptive else \
+            (kc[consistent.index(h)], vc[consistent.index(h)])
+        pairs.append((kt.data_ptr(), vt.data_ptr()))
+        maxlen.append(kt.shape[0])
+    plan = ck.decode_plan(np.array([maxlen]), wl.hq, wl.hkv, DEV)
+    q_st = synth.decode_queries(wl, 3)
+    out, lse = ck.decode_attn(plan, to_dev(q_st), ck.kv_table(pairs, DEV), lens.view(1, -1))
+    torch.cuda.synchronize()
+    views = [(f64(seq.k[h][rows[h]]), f64(seq.v[h][rows[h]])) for h in range(wl.hkv)]
+    o_ref, l_ref = O.decode_gqa(f64(q_st)[0], views)
+    assert_rows_close(out.cpu().numpy()[0], o_ref, "bf16", f"eta={eta}")
+    np.testing.assert_allclose(lse.cpu().numpy()[0], l_ref, atol=1e-4, rtol=0)

@@ -360,3 +360,95 @@ class TestQuantileAndClassify:
         # r = 0.5 with H = 4: Eq. 5 keeps 2 heads per sample
         assert st.tolist() == [True, False, False, True]
         assert O.static_head_types(sc[:1], 0.5).tolist() == O.classify_sample(sc[0], 0.5).tolist()
+
+
+class TestAroundDecoding:
+    """Generation-loop append, retention below 1, query-aware retrieval and
+    attention recall."""
+
+    def test_append_reproduces_the_longer_sequence(self):
+        r = rng(40)
+        n, T, d = 50, 7, 16
+        K, V = r.normal(size=(n + T, d)), r.normal(size=(n + T, d))
+        k, v = K[:n], V[:n]
+        for t in range(T):
+            k, v, ok = O.append_token(k, v, K[n + t], V[n + t], capacity=n + T)
+            assert ok
+        assert np.array_equal(k, K) and np.array_equal(v, V)
+        # decoding the grown view is attention over the whole sequence (library SDPA)
+        q = r.normal(size=d)
+        ref = torch.nn.functional.scaled_dot_product_attention(
+            torch.from_numpy(q)[None, None, None], torch.from_numpy(K)[None, None],
+            torch.from_numpy(V)[None, None], scale=0.25)[0, 0, 0].numpy()
+        np.testing.assert_allclose(O.attention_decode(q, k, v, 0.25)[0], ref, atol=1e-12)
+
+    def test_append_stops_at_capacity(self):
+        k, v = np.zeros((3, 4)), np.zeros((3, 4))
+        k2, v2, ok = O.append_token(k, v, np.ones(4), np.ones(4), capacity=3)
+        assert not ok and k2.shape[0] == 3
+
+    def test_adaptive_budget_hand_values(self):
+        # n - l_obs = 90 keys -> 12 chunks of 8 (the last one partial)
+        assert [O.adaptive_budget(100, 10, 8, e) for e in (1.0, 0.5, 0.3, 0.25, 0.0)] == [12, 6, 4, 3, 0]
+
+    def test_retention_one_keeps_the_whole_cache(self):
+        r = rng(41)
+        n, l_obs, cs = 61, 5, 8
+        q, k = r.normal(size=(2, l_obs, 16)), r.normal(size=(1, n, 16))
+        b = O.adaptive_budget(n, l_obs, cs, 1.0)
+        idx = O.select_critical(q, k, [0], cs, b)[0]
+        assert np.array_equal(O.compact_rows(n, l_obs, cs, idx), np.arange(n))
+
+    def test_page_bounds_match_library_reduction(self):
+        r = rng(42)
+        k = r.normal(size=(37, 5))
+        kmin, kmax = O.page_bounds(k, 8)
+        starts = np.arange(0, 37, 8)
+        np.testing.assert_array_equal(kmin, np.minimum.reduceat(k, starts, axis=0))
+        np.testing.assert_array_equal(kmax, np.maximum.reduceat(k, starts, axis=0))
+
+    @pytest.mark.parametrize("seed", [0, 1, 2])
+    def test_page_score_bounds_every_token(self, seed):
+        r = rng(43 + seed)
+        k, qg = r.normal(size=(45, 12)), r.normal(size=(4, 12))
+        kmin, kmax = O.page_bounds(k, 8)
+        sc = O.page_scores(qg, kmin, kmax)
+        for c in range(sc.shape[0]):
+            rows = k[c * 8:(c + 1) * 8]
+            assert sc[c] >= (qg @ rows.T).max() - 1e-12
+
+    def test_page_score_is_tight_for_single_rows_and_repeated_rows(self):
+        r = rng(46)
+        k, qg = r.normal(size=(9, 6)), r.normal(size=(2, 6))
+        kmin, kmax = O.page_bounds(k, 1)
+        np.testing.assert_allclose(O.page_scores(qg, kmin, kmax), (qg @ k.T).max(axis=0), atol=1e-12)
+        rep = np.repeat(k[:2], 4, axis=0)            # two pages of four identical rows
+        kmin, kmax = O.page_bounds(rep, 4)
+        np.testing.assert_allclose(O.page_scores(qg, kmin, kmax), (qg @ k[:2].T).max(axis=0), atol=1e-12)
+
+    def test_page_score_one_dimension_is_the_exact_maximum(self):
+        r = rng(47)
+        k, q = r.normal(size=(20, 1)), r.normal(size=(1, 1))
+        kmin, kmax = O.page_bounds(k, 5)
+        np.testing.assert_allclose(O.page_scores(q, kmin, kmax), (q @ k.T).reshape(4, 5).max(axis=1), atol=1e-12)
+
+    def test_retrieval_with_single_row_pages_is_token_topk(self):
+        r = rng(48)
+        k, qg = r.normal(size=(30, 8)), r.normal(size=(3, 8))
+        got = O.retrieve_pages(qg, k, 1, 7)
+        best = (qg @ k.T).max(axis=0)
+        assert set(got.tolist()) == set(np.argsort(-best)[:7].tolist())
+        assert (np.diff(got) > 0).all()
+
+    def test_recall_extremes_and_topk_optimality(self):
+        r = rng(49)
+        k, q = r.normal(size=(8, 4)), r.normal(size=4)
+        assert abs(O.attention_recall(q, k, np.arange(8), 0.5) - 1.0) < 1e-12
+        assert O.attention_recall(q, k, np.zeros(0, dtype=np.int64), 0.5) == 0.0
+        best = max(O.attention_recall(q, k, np.array(c), 0.5) for c in itertools.combinations(range(8), 3))
+        assert abs(O.attention_recall(q, k, O.topk_keep(q, k, 3, 0.5), 0.5) - best) < 1e-12
+
+    def test_streaming_and_chunk_rows(self):
+        assert O.streaming_keep(10, 4, 1).tolist() == [0, 7, 8, 9]
+        assert O.streaming_keep(5, 9, 2).tolist() == [0, 1, 2, 3, 4]
+        assert O.chunk_rows(20, 8, np.array([2, 0])).tolist() == list(range(8)) + [16, 17, 18, 19]
