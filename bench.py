@@ -366,6 +366,88 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    def time_retrieval():
+        """One decode step with query-aware retrieval in the adaptive heads
+        (pages of cs rows, the consistent heads' budget): page scores + top
+        pages, the gather of their rows, then decode over the consistent
+        heads' compact caches and the gathered pages."""
+        n_keep = b
+        if n % wl.cs:
+            return None          # a partial last page would make the gathered length vary per step
+        bounds = [ck.page_bounds(L_[0], list(range(len(adaptive))), wl.cs) for L_ in layers]
+        n_pages = bounds[0][0].shape[1]
+        ws_r = ck.workspace(lib().catekv_retrieve_workspace(len(adaptive), n_pages), dev)
+        idx_r = torch.empty((len(adaptive), n_keep), dtype=torch.int32, device=dev)
+        kg = torch.empty((len(adaptive), n_keep * wl.cs, d), dtype=k_c.dtype, device=dev)
+        vg = torch.empty_like(kg)
+        lens_g = torch.zeros(len(adaptive), dtype=torch.int64, device=dev)   # gather lengths (adaptive numbering)
+        tabs = []
+        for li, L_ in enumerate(layers):
+            pairs = []
+            for h in range(hkv):
+                t_ = (L_[2][heads.index(h)], L_[3][heads.index(h)]) if h in heads else \
+                    (kg[adaptive.index(h)], vg[adaptive.index(h)])
+                pairs.append((t_[0].data_ptr(), t_[1].data_ptr()))
+            tabs.append(ck.kv_table(pairs, dev))
+        vl = [n_keep * wl.cs if h in adaptive else int(lens_h[h]) for h in range(hkv)]
+        plan_r = ck.decode_plan(np.array([vl], dtype=np.int64), hq, hkv, dev)
+        out_r = torch.empty_like(out)
+        harr_a = (_lib.ctypes.c_int32 * len(adaptive))(*range(len(adaptive)))
+
+        def retrieve(t, st):
+            li = t % n_layers
+            check(lib().catekv_retrieve_pages(dtc, qs[t % nq].data_ptr(), bounds[li][0].data_ptr(),
+                                              bounds[li][1].data_ptr(), hq, hkv, n_pages, d, harr_a, len(adaptive),
+                                              n_keep, idx_r.data_ptr(), ws_r.data_ptr(), ws_r.numel(),
+                                              st.cuda_stream))
+
+        def step_r(t, st):
+            li = t % n_layers
+            retrieve(t, st)
+            check(lib().catekv_compact_kv(dtc, layers[li][0].data_ptr(), layers[li][1].data_ptr(), len(adaptive), n,
+                                          d, wl.cs, 0, harr_a, len(adaptive), idx_r.data_ptr(), n_keep,
+                                          kg.data_ptr(), vg.data_ptr(), lens_g.data_ptr(), st.cuda_stream))
+            check(lib().catekv_decode_attn(dtc, _lib.ctypes.byref(plan_r.plan), qs[t % nq].data_ptr(),
+                                           tabs[li].data_ptr(), lens_r.data_ptr(), 1, hq, hkv, d, scale,
+                                           out_r.data_ptr(), None, plan_r.ws.data_ptr(), plan_r.ws.numel(),
+                                           st.cuda_stream))
+
+        # every gathered view holds n_keep whole pages (n is a multiple of the page size)
+        lens_r = torch.tensor(vl, dtype=torch.int64, device=dev)
+        res_r = {}
+        for name_, fn in (("retrieve_us", retrieve), ("step_us", step_r)):
+            for t in range(3):
+                fn(t, stream)
+            torch.cuda.synchronize()
+            cyc = min(64, n_layers * nq // math.gcd(n_layers, nq))
+            s4 = torch.cuda.Stream(device=dev)
+            s4.wait_stream(stream)
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.stream(s4):
+                gr.capture_begin()
+                for t in range(cyc):
+                    fn(t, s4)
+                gr.capture_end()
+            stream.wait_stream(s4)
+            torch.cuda.synchronize()
+            reps = max(1, round(args.steps / cyc))
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                gr.replay()
+            e1.record(stream)
+            e1.synchronize()
+            res_r[name_] = round(e0.elapsed_time(e1) * 1e3 / (reps * cyc), 2)
+            del gr
+        step_bytes = (len(adaptive) * n_pages * d * esz * 2 + 2 * len(adaptive) * n_keep * wl.cs * d * esz * 2
+                      + sum(vl) * d * esz * 2 + hq * d * esz + hq * d * 4)
+        res_r.update({"pages_kept": n_keep, "page_rows": wl.cs, "n_pages": n_pages,
+                      "bytes_per_step": int(step_bytes), "launch": "hip_graph",
+                      "note": "page bounds of every layer copy read each step; gather reads and writes the kept rows"})
+        log(f"[bench] query-aware retrieval: {res_r['step_us']:.2f} us/step "
+            f"(retrieval alone {res_r['retrieve_us']:.2f} us), {n_keep} pages of {n_pages} per adaptive head")
+        return res_r
+
     # ---------------- decode-time append and the retention sweep ----------------
     next_res = None
     if not args.no_next:
@@ -448,6 +530,8 @@ def main():
                 f"({bytes_step / 1e6:.1f} MB), adaptive selection {sel_us:.1f} us")
             del cps, ge
         next_res["retention_sweep"] = sweep
+        if adaptive:
+            next_res["query_aware_retrieval"] = time_retrieval()
 
     # ---------------- CPU oracle on a bounded sample ----------------
     cpu = None

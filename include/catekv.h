@@ -14,6 +14,13 @@
  *   catekv_decode_attn      GQA decode over mixed per-head cache lengths
  *                                                         (Algorithm 1, decoding stage)
  *
+ * and, around the decoding stage:
+ *
+ *   catekv_page_bounds      per-page key minima/maxima of adaptive heads
+ *   catekv_retrieve_pages   query-aware page retrieval per step
+ *                           (Algorithm 1, Retrieval(q, cache_k, cache_v); Section 4, with Quest)
+ *   catekv_append_kv        the generated token of each step into every view
+ *
  * Conventions shared by every call
  * --------------------------------
  * - Tensor arguments are caller-owned DEVICE pointers unless the name ends in
@@ -152,8 +159,11 @@ int catekv_select_critical(int dtype, const void* q_obs, const void* k,
  * k_c, v_c  [n_sel][b * cs + l_obs][d], device (capacity per head)
  * lens_out  int64 device array indexed by KV head id (e.g. one sequence's
  *           row of a [batch][hkv] length table); other entries untouched.
- * Errors: INVALID_ARG for null pointers or the selection errors above.  Index
- * values must come from catekv_select_critical with the same n, l_obs, cs. */
+ * l_obs may be 0 here (chunk rows only): with chunk indices over [0, n) from
+ * catekv_retrieve_pages this gathers the retrieved pages of a step.
+ * Errors: INVALID_ARG for null pointers or the selection errors above (with
+ * l_obs >= 0 allowed).  Index values must come from catekv_select_critical
+ * with the same n, l_obs, cs, or from catekv_retrieve_pages with l_obs = 0. */
 int catekv_compact_kv(int dtype, const void* k, const void* v, int hkv, int64_t n, int d,
                       int cs, int l_obs, const int32_t* sel_heads_host, int n_sel,
                       const int32_t* idx, int b, void* k_c, void* v_c, int64_t* lens_out,
@@ -201,6 +211,44 @@ int catekv_decode_attn(int dtype, const catekv_decode_plan_t* plan, const void* 
                        const catekv_kv_ptrs* kv, const int64_t* lens,
                        int batch, int hq, int hkv, int d, float scale,
                        float* out, float* lse, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Query-aware retrieval in adaptive heads -- Algorithm 1, decoding stage,    */
+/* Retrieval(q, cache_k, cache_v) "all or query-aware"; the page-based        */
+/* retrieval (Quest) that Section 4 integrates into the adaptive heads.       */
+/* ------------------------------------------------------------------------ */
+
+/* Page metadata of the selected heads' caches: pages are the chunks of cs
+ * rows [p cs, min((p + 1) cs, n)), p < n_pages = ceil(n / cs), and
+ *   kmin[s][p][j] = min over the page's rows t of K[heads[s]][t][j]
+ *   kmax[s][p][j] = max over the same rows,
+ * stored in the dtype of K (exact: minima and maxima of stored values).
+ * k           [hkv][n][d] (dtype)
+ * heads_host  [n_sel] KV head ids, host array, distinct, 1 <= n_sel <= 128
+ * kmin, kmax  [n_sel][n_pages][d] (dtype), caller-allocated
+ * Errors: INVALID_ARG for null pointers, n < 1, cs < 1 or a bad head list;
+ * UNSUPPORTED for d != 128 or n above 2^31 - 1. */
+int catekv_page_bounds(int dtype, const void* k, int hkv, int64_t n, int d, int cs,
+                       const int32_t* heads_host, int n_sel, void* kmin, void* kmax, void* stream);
+
+/* Workspace bytes of catekv_retrieve_pages. */
+size_t catekv_retrieve_workspace(int n_sel, int64_t n_pages);
+
+/* Pages to attend for one decode step of one sequence.  For each selected
+ * head h = heads_host[s] with query heads g in [h G, (h + 1) G), G = hq/hkv:
+ *   score[p] = max over g of sum_j max(q[g][j] kmin[s][p][j], q[g][j] kmax[s][p][j])
+ * (an upper bound of q_g . k over the page's rows), and idx_out[s] holds the
+ * n_keep pages with the largest scores (ties to the lower page), ascending,
+ * padded with -1 when n_keep > n_pages.  catekv_compact_kv with l_obs = 0,
+ * cs and b = n_keep then gathers those pages' rows for catekv_decode_attn.
+ * q        [hq][d] (dtype), the step's queries of this sequence
+ * kmin, kmax  from catekv_page_bounds for the same heads_host
+ * idx_out  [n_sel][n_keep] int32
+ * Errors: INVALID_ARG for null pointers, n_pages < 1, n_keep < 1 or a bad
+ * head list; UNSUPPORTED for unsupported shapes; WORKSPACE if ws is too small. */
+int catekv_retrieve_pages(int dtype, const void* q, const void* kmin, const void* kmax, int hq, int hkv,
+                          int64_t n_pages, int d, const int32_t* heads_host, int n_sel, int n_keep,
+                          int32_t* idx_out, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Decode-time KV append -- the generation loop around Algorithm 1's decoding */

@@ -14,6 +14,8 @@ from .binding import (  # noqa: F401
     decode_plan,
     decode_workspace,
     kv_table,
+    page_bounds,
+    retrieve_pages,
     score_heads,
     score_heads_workspace,
     select_critical,

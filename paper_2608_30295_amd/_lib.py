@@ -55,6 +55,11 @@ SIGNATURES = {
     "catekv_decode_attn": (c_int, [c_int, ctypes.POINTER(DecodePlanT), c_void_p, c_void_p, c_void_p, c_int,
                                    c_int, c_int, c_int, c_float, c_void_p, c_void_p, c_void_p, c_size,
                                    c_void_p]),
+    "catekv_page_bounds": (c_int, [c_int, c_void_p, c_int, c_i64, c_int, c_int, P_i32, c_int, c_void_p, c_void_p,
+                                   c_void_p]),
+    "catekv_retrieve_workspace": (c_size, [c_int, c_i64]),
+    "catekv_retrieve_pages": (c_int, [c_int, c_void_p, c_void_p, c_void_p, c_int, c_int, c_i64, c_int, P_i32, c_int,
+                                      c_int, c_void_p, c_void_p, c_size, c_void_p]),
     "catekv_append_kv": (c_int, [c_int, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_int, c_int, c_int,
                                  c_void_p, c_void_p]),
     "catekv_last_error": (ctypes.c_char_p, []),

@@ -211,3 +211,38 @@ def adaptive_budget(n: int, l_obs: int, cs: int, eta: float) -> int:
     eta = 1 keeps every chunk, i.e. the original cache."""
     nc = -(-(n - l_obs) // cs)
     return int(math.ceil(eta * nc - 1e-12))
+
+
+def page_bounds(k: torch.Tensor, heads: Sequence[int], cs: int) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Per-page key minima and maxima of the given KV heads (pages of cs rows):
+    k [Hkv][n][d] -> (kmin, kmax) [n_sel][ceil(n / cs)][d] in k's dtype."""
+    _need_cuda(k)
+    hkv, n, d = k.shape
+    heads = list(heads)
+    n_pages = -(-n // cs)
+    kmin = torch.empty((len(heads), n_pages, d), dtype=k.dtype, device=k.device)
+    kmax = torch.empty_like(kmin)
+    check(lib().catekv_page_bounds(_dtype_code(k), k.data_ptr(), hkv, n, d, cs, _heads_arg(heads), len(heads),
+                                   kmin.data_ptr(), kmax.data_ptr(), _stream(k.device)))
+    return kmin, kmax
+
+
+def retrieve_pages(q: torch.Tensor, kmin: torch.Tensor, kmax: torch.Tensor, heads: Sequence[int], hkv: int,
+                   n_keep: int, ws: Optional[torch.Tensor] = None,
+                   out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Query-aware page retrieval for one step of one sequence: q [Hq][d];
+    kmin/kmax from page_bounds for the same heads -> int32 [n_sel][n_keep]
+    page indices, ascending, -1 padded."""
+    _need_cuda(q, kmin, kmax)
+    hq, d = q.shape
+    heads = list(heads)
+    n_sel, n_pages, _ = kmin.shape
+    need = int(lib().catekv_retrieve_workspace(n_sel, n_pages))
+    if ws is None:
+        ws = workspace(need, q.device)
+    if out is None:
+        out = torch.empty((n_sel, n_keep), dtype=torch.int32, device=q.device)
+    check(lib().catekv_retrieve_pages(_dtype_code(q), q.data_ptr(), kmin.data_ptr(), kmax.data_ptr(), hq, hkv,
+                                      n_pages, d, _heads_arg(heads), n_sel, n_keep, out.data_ptr(), ws.data_ptr(),
+                                      ws.numel(), _stream(q.device)))
+    return out

@@ -164,8 +164,8 @@ int check_head_list(int hkv, const int32_t* heads, int n_sel) {
 }
 
 // Checks shared by selection and compaction (window, chunking, budget, heads).
-int check_window(int hkv, int l_obs, int64_t n, int cs, const int32_t* heads, int n_sel, int b) {
-  if (l_obs < 1) return fail(CATEKV_ERR_INVALID_ARG, "l_obs=%d must be >= 1", l_obs);
+int check_window(int hkv, int l_obs, int64_t n, int cs, const int32_t* heads, int n_sel, int b, int min_l_obs = 1) {
+  if (l_obs < min_l_obs) return fail(CATEKV_ERR_INVALID_ARG, "l_obs=%d must be >= %d", l_obs, min_l_obs);
   if ((int64_t)l_obs >= n) return fail(CATEKV_ERR_INVALID_ARG, "l_obs=%d must be below n=%lld", l_obs, (long long)n);
   if (n > INT32_MAX) return fail(CATEKV_ERR_UNSUPPORTED, "n=%lld above 2^31 - 1", (long long)n);
   if (cs < 1) return fail(CATEKV_ERR_INVALID_ARG, "chunk size %d must be >= 1", cs);
@@ -308,7 +308,7 @@ int catekv_compact_kv(int dtype, const void* k, const void* v, int hkv, int64_t 
   if (!k || !v || !idx || !k_c || !v_c || !lens_out) return fail(CATEKV_ERR_INVALID_ARG, "null tensor pointer");
   int rc = check_heads(hkv, hkv, d);
   if (rc) return rc;
-  rc = check_window(hkv, l_obs, n, cs, sel_heads_host, n_sel, b);
+  rc = check_window(hkv, l_obs, n, cs, sel_heads_host, n_sel, b, 0);
   if (rc) return rc;
   hipError_t e = catekv::launch_compact(dtype, k, v, hkv, n, cs, l_obs, sel_heads_host, n_sel, idx, b, k_c,
                                         v_c, lens_out, reinterpret_cast<hipStream_t>(stream));
@@ -421,6 +421,50 @@ int catekv_decode_attn(int dtype, const catekv_decode_plan_t* plan, const void* 
   a.lse = lse;
   hipError_t e = catekv::launch_decode(dtype, hq / hkv, a, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "decode_attn launch");
+  return ok();
+}
+
+int catekv_page_bounds(int dtype, const void* k, int hkv, int64_t n, int d, int cs, const int32_t* heads_host,
+                       int n_sel, void* kmin, void* kmax, void* stream) {
+  if (!valid_dtype(dtype)) return fail(CATEKV_ERR_UNSUPPORTED, "dtype %d unsupported", dtype);
+  if (!k || !kmin || !kmax) return fail(CATEKV_ERR_INVALID_ARG, "null tensor pointer");
+  int rc = check_heads(hkv, hkv, d);
+  if (rc) return rc;
+  if (n < 1) return fail(CATEKV_ERR_INVALID_ARG, "n=%lld must be >= 1", (long long)n);
+  if (n > INT32_MAX) return fail(CATEKV_ERR_UNSUPPORTED, "n=%lld above 2^31 - 1", (long long)n);
+  if (cs < 1) return fail(CATEKV_ERR_INVALID_ARG, "chunk size %d must be >= 1", cs);
+  rc = check_head_list(hkv, heads_host, n_sel);
+  if (rc) return rc;
+  hipError_t e = catekv::launch_page_bounds(dtype, k, n, cs, heads_host, n_sel, kmin, kmax,
+                                            reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "page_bounds launch");
+  return ok();
+}
+
+size_t catekv_retrieve_workspace(int n_sel, int64_t n_pages) {
+  if (n_sel < 1 || n_pages < 1) return 0;
+  return ((size_t)n_sel * (size_t)n_pages * sizeof(float) + 255) / 256 * 256;
+}
+
+int catekv_retrieve_pages(int dtype, const void* q, const void* kmin, const void* kmax, int hq, int hkv,
+                          int64_t n_pages, int d, const int32_t* heads_host, int n_sel, int n_keep,
+                          int32_t* idx_out, void* ws, size_t ws_bytes, void* stream) {
+  if (!valid_dtype(dtype)) return fail(CATEKV_ERR_UNSUPPORTED, "dtype %d unsupported", dtype);
+  if (!q || !kmin || !kmax || !idx_out) return fail(CATEKV_ERR_INVALID_ARG, "null tensor pointer");
+  int rc = check_heads(hq, hkv, d);
+  if (rc) return rc;
+  if (n_pages < 1) return fail(CATEKV_ERR_INVALID_ARG, "n_pages=%lld must be >= 1", (long long)n_pages);
+  if (n_pages > INT32_MAX) return fail(CATEKV_ERR_UNSUPPORTED, "n_pages above 2^31 - 1");
+  if (n_keep < 1) return fail(CATEKV_ERR_INVALID_ARG, "n_keep=%d must be >= 1", n_keep);
+  rc = check_head_list(hkv, heads_host, n_sel);
+  if (rc) return rc;
+  rc = check_ws(ws, ws_bytes, catekv_retrieve_workspace(n_sel, n_pages));
+  if (rc) return rc;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  float* scores = reinterpret_cast<float*>(ws);
+  hipError_t e = catekv::launch_page_scores(dtype, hq / hkv, q, kmin, kmax, n_pages, heads_host, n_sel, scores, s);
+  if (e == hipSuccess) e = catekv::launch_topk(scores, n_sel, n_pages, n_keep, idx_out, s);
+  if (e != hipSuccess) return hip_fail(e, "retrieve_pages launch");
   return ok();
 }
 

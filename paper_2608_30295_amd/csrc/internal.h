@@ -85,6 +85,17 @@ hipError_t launch_compact(int dtype, const void* k, const void* v, int hkv, int6
                           int l_obs, const int32_t* heads, int n_sel, const int32_t* idx, int b,
                           void* k_c, void* v_c, int64_t* lens_out, hipStream_t stream);
 
+// Indices of the b largest of each row of S [n_rows][n] (ties to the lower
+// index), ascending, -1 padded to b.
+hipError_t launch_topk(const float* S, int n_rows, int64_t n, int b, int32_t* idx_out, hipStream_t stream);
+
+// ---- query-aware retrieval in adaptive heads (page bounds and scores) -----
+hipError_t launch_page_bounds(int dtype, const void* k, int64_t n, int cs, const int32_t* heads, int n_sel,
+                              void* kmin, void* kmax, hipStream_t stream);
+hipError_t launch_page_scores(int dtype, int G, const void* q, const void* kmin, const void* kmax,
+                              int64_t n_pages, const int32_t* heads, int n_sel, float* scores,
+                              hipStream_t stream);
+
 // ---- CV head scoring -----------------------------------------------------
 struct ScoreGeom {
   int hq, hkv, G, lq;

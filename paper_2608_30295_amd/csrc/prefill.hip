@@ -916,16 +916,17 @@ hipError_t launch_select(int dtype, const SelectGeom& g, const void* q_obs, cons
   if (!a.cs_fused)
     hipLaunchKernelGGL(chunk_max_kernel, dim3((unsigned)((g.n_chunks + 255) / 256), g.n_sel), dim3(256), 0,
                        stream, a.colmass, g.n_keys, g.cs, g.n_chunks, S);
-  const int k_eff = (int)(g.b < g.n_chunks ? g.b : g.n_chunks);
-  if (g.n_chunks <= 16 * kTopkThreads)
-    hipLaunchKernelGGL(topk_reg_kernel<16>, dim3(g.n_sel), dim3(kTopkThreads), 0, stream, S, g.n_chunks, k_eff,
-                       g.b, idx_out);
-  else if (g.n_chunks <= 32 * kTopkThreads)
-    hipLaunchKernelGGL(topk_reg_kernel<32>, dim3(g.n_sel), dim3(kTopkThreads), 0, stream, S, g.n_chunks, k_eff,
-                       g.b, idx_out);
+  return launch_topk(S, g.n_sel, g.n_chunks, g.b, idx_out, stream);
+}
+
+hipError_t launch_topk(const float* S, int n_rows, int64_t n, int b, int32_t* idx_out, hipStream_t stream) {
+  const int k_eff = (int)(b < n ? b : n);
+  if (n <= 16 * kTopkThreads)
+    hipLaunchKernelGGL(topk_reg_kernel<16>, dim3(n_rows), dim3(kTopkThreads), 0, stream, S, n, k_eff, b, idx_out);
+  else if (n <= 32 * kTopkThreads)
+    hipLaunchKernelGGL(topk_reg_kernel<32>, dim3(n_rows), dim3(kTopkThreads), 0, stream, S, n, k_eff, b, idx_out);
   else
-    hipLaunchKernelGGL(topk_kernel, dim3(g.n_sel), dim3(kTopkThreads), 0, stream, S, g.n_chunks, k_eff,
-                       g.b, idx_out);
+    hipLaunchKernelGGL(topk_kernel, dim3(n_rows), dim3(kTopkThreads), 0, stream, S, n, k_eff, b, idx_out);
   return hipGetLastError();
 }
 

@@ -28,7 +28,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 12
+    assert len(names) == 15
     L = ck.lib()
     for n in names:
         assert hasattr(L, n), n
@@ -182,3 +182,23 @@ def test_append_kv_rejects_bad_arguments():
     assert rc == _lib.CATEKV_ERR_INVALID_ARG and "d=64" in msg
     rc, _ = call(dtype=7)
     assert rc == _lib.CATEKV_ERR_UNSUPPORTED
+
+
+def test_retrieval_rejects_bad_arguments():
+    L = ck.lib()
+    heads = (ctypes.c_int32 * 1)(0)
+    rc, _ = _status_and_msg(L.catekv_page_bounds(1, FAKE, 2, 100, 128, 0, heads, 1, FAKE, FAKE, None))
+    assert rc == _lib.CATEKV_ERR_INVALID_ARG                       # cs = 0
+    rc, _ = _status_and_msg(L.catekv_page_bounds(1, FAKE, 2, 0, 128, 8, heads, 1, FAKE, FAKE, None))
+    assert rc == _lib.CATEKV_ERR_INVALID_ARG                       # n = 0
+    bad = (ctypes.c_int32 * 1)(5)
+    rc, _ = _status_and_msg(L.catekv_page_bounds(1, FAKE, 2, 100, 128, 8, bad, 1, FAKE, FAKE, None))
+    assert rc == _lib.CATEKV_ERR_INVALID_ARG                       # head out of range
+    need = L.catekv_retrieve_workspace(1, 13)
+    assert need >= 13 * 4 and need % 256 == 0
+    rc, _ = _status_and_msg(L.catekv_retrieve_pages(1, FAKE, FAKE, FAKE, 8, 2, 13, 128, heads, 1, 0, FAKE, FAKE,
+                                                    need, None))
+    assert rc == _lib.CATEKV_ERR_INVALID_ARG                       # n_keep = 0
+    rc, _ = _status_and_msg(L.catekv_retrieve_pages(1, FAKE, FAKE, FAKE, 8, 2, 13, 128, heads, 1, 4, FAKE, FAKE,
+                                                    need - 256, None))
+    assert rc == _lib.CATEKV_ERR_WORKSPACE

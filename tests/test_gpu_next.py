@@ -147,3 +147,76 @@ def test_retention_below_one(eta):
     o_ref, l_ref = O.decode_gqa(f64(q_st)[0], views)
     assert_rows_close(out.cpu().numpy()[0], o_ref, "bf16", f"eta={eta}")
     np.testing.assert_allclose(lse.cpu().numpy()[0], l_ref, atol=1e-4, rtol=0)
+
+
+# ------------------------------------- query-aware retrieval (adaptive heads)
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_page_bounds(dtype):
+    rng = np.random.default_rng(31)
+    k = _storage(rng.standard_normal((3, 1003, 128), dtype=np.float32), dtype)   # ragged last page
+    say(f"page bounds {dtype}")
+    kmin, kmax = ck.page_bounds(to_dev(k), [2, 0], 8)
+    torch.cuda.synchronize()
+    got_min, got_max = f64(to_host_storage(kmin)), f64(to_host_storage(kmax))
+    for s, h in enumerate([2, 0]):
+        mn, mx = O.page_bounds(f64(k[h]), 8)
+        assert np.array_equal(got_min[s], mn) and np.array_equal(got_max[s], mx)
+
+
+@pytest.mark.parametrize("dtype,n_keep", [("bf16", 64), ("f32", 64), ("bf16", 3000)])
+def test_retrieve_gather_decode(dtype, n_keep):
+    """One decode step with query-aware retrieval in the adaptive heads: page
+    scores and top pages against the oracle, the gathered rows bitwise, and
+    attention over them."""
+    name = "ctx32k_bf16" if dtype == "bf16" else "ctx4k_f32"
+    wl = synth.WORKLOADS[name].scaled(n=20000 + 3 if dtype == "bf16" else 4096)
+    seq = synth.make_sequence(wl)
+    n, G, cs = seq.n, wl.group, wl.cs
+    adaptive = [0, 3, 6] if wl.hkv == 8 else [0, 2]
+    n_pages = -(-n // cs)
+    say(f"retrieve {dtype}: n={n} pages={n_pages} keep={n_keep} heads={adaptive}")
+    k, v = to_dev(seq.k), to_dev(seq.v)
+    kmin, kmax = ck.page_bounds(k, adaptive, cs)
+    q_st = synth.decode_queries(wl, 5)
+    idx = ck.retrieve_pages(to_dev(q_st)[0], kmin, kmax, adaptive, wl.hkv, n_keep)
+    lens = torch.full((wl.hkv,), n, dtype=torch.int64, device=DEV)
+    kg, vg = ck.compact_kv(k, v, adaptive, idx, cs, 0, lens)
+    torch.cuda.synchronize()
+    idx_h, lens_h = idx.cpu().numpy(), lens.cpu().numpy()
+    kg_h, vg_h = to_host_storage(kg), to_host_storage(vg)
+    qf = f64(q_st)[0]
+    from gpu_util import check_topk
+    rows = {}
+    for s, h in enumerate(adaptive):
+        mn, mx = O.page_bounds(f64(seq.k[h]), cs)
+        sc = O.page_scores(qf[h * G:(h + 1) * G], mn, mx)
+        swaps = check_topk(idx_h[s], sc, n_keep)
+        sel = idx_h[s][idx_h[s] >= 0]
+        rows[h] = O.chunk_rows(n, cs, sel)
+        assert lens_h[h] == rows[h].size
+        assert np.array_equal(kg_h[s][:rows[h].size], seq.k[h][rows[h]])
+        assert np.array_equal(vg_h[s][:rows[h].size], seq.v[h][rows[h]])
+        say(f"  head {h}: {sel.size} pages, {swaps} swaps inside the band")
+    pairs, maxlen = [], []
+    for h in range(wl.hkv):
+        kt, vt = (kg[adaptive.index(h)], vg[adaptive.index(h)]) if h in adaptive else (k[h], v[h])
+        pairs.append((kt.data_ptr(), vt.data_ptr()))
+        maxlen.append(kt.shape[0])
+    plan = ck.decode_plan(np.array([maxlen]), wl.hq, wl.hkv, DEV)
+    out, lse = ck.decode_attn(plan, to_dev(q_st), ck.kv_table(pairs, DEV), lens.view(1, -1))
+    torch.cuda.synchronize()
+    views = [(f64(seq.k[h][rows[h]]), f64(seq.v[h][rows[h]])) if h in adaptive else (f64(seq.k[h]), f64(seq.v[h]))
+             for h in range(wl.hkv)]
+    o_ref, l_ref = O.decode_gqa(qf, views)
+    assert_rows_close(out.cpu().numpy()[0], o_ref, dtype, "retrieval decode")
+    np.testing.assert_allclose(lse.cpu().numpy()[0], l_ref, atol=1e-4, rtol=0)
+
+
+def test_retrieve_more_pages_than_exist():
+    rng = np.random.default_rng(33)
+    k = to_dev(synth.f32_to_bf16_bits(rng.standard_normal((1, 50, 128), dtype=np.float32)))
+    q = to_dev(synth.f32_to_bf16_bits(rng.standard_normal((4, 128), dtype=np.float32)))
+    kmin, kmax = ck.page_bounds(k, [0], 8)
+    idx = ck.retrieve_pages(q, kmin, kmax, [0], 1, 10).cpu().numpy()
+    assert idx[0].tolist() == list(range(7)) + [-1, -1, -1]
