@@ -220,3 +220,37 @@ def test_retrieve_more_pages_than_exist():
     kmin, kmax = ck.page_bounds(k, [0], 8)
     idx = ck.retrieve_pages(q, kmin, kmax, [0], 1, 10).cpu().numpy()
     assert idx[0].tolist() == list(range(7)) + [-1, -1, -1]
+
+
+# ---------------------------------------------------- attention recall
+
+def test_recall_of_gpu_selection_and_retrieval_matches_oracle():
+    """The recall diagnostic on the GPU's own choices: the consistent
+    pattern from select_critical and the pages from retrieve_pages keep the
+    same attention mass as the oracle's choices."""
+    wl = synth.WORKLOADS["ctx4k_f32"]
+    seq = synth.make_sequence(wl)
+    n, G, cs, l_obs, b = seq.n, wl.group, wl.cs, wl.l_obs, wl.chunk_budget
+    scale = 1 / math.sqrt(128)
+    qf, kf = f64(seq.q_obs), f64(seq.k)
+    k = to_dev(seq.k)
+    idx_g = ck.select_critical(to_dev(seq.q_obs), k, list(range(wl.hkv)), cs, b).cpu().numpy()
+    idx_o = O.select_critical(qf, kf, range(wl.hkv), cs, b)
+    kmin, kmax = ck.page_bounds(k, list(range(wl.hkv)), cs)
+    q_st = synth.decode_queries(wl, 2)[0]
+    pages_g = ck.retrieve_pages(to_dev(q_st), kmin, kmax, list(range(wl.hkv)), wl.hkv, (b * cs + l_obs) // cs)
+    pages_g = pages_g.cpu().numpy()
+    qd = f64(q_st)
+    worst = 0.0
+    for h in range(wl.hkv):
+        rows_g = O.compact_rows(n, l_obs, cs, idx_g[h][idx_g[h] >= 0])
+        rows_o = O.compact_rows(n, l_obs, cs, idx_o[h])
+        mn, mx = O.page_bounds(kf[h], cs)
+        p_o = O.argtopk_ascending(O.page_scores(qd[h * G:(h + 1) * G], mn, mx), (b * cs + l_obs) // cs)
+        for g in range(h * G, (h + 1) * G):
+            a = O.attention_recall(qd[g], kf[h], rows_g, scale) - O.attention_recall(qd[g], kf[h], rows_o, scale)
+            c = O.attention_recall(qd[g], kf[h], O.chunk_rows(n, cs, pages_g[h]), scale) - \
+                O.attention_recall(qd[g], kf[h], O.chunk_rows(n, cs, p_o), scale)
+            worst = max(worst, abs(a), abs(c))
+    say(f"largest recall difference GPU vs oracle choices: {worst:.2e}")
+    assert worst < 1e-6
