@@ -436,20 +436,28 @@ __global__ void chunk_max_kernel(const float* __restrict__ C, int64_t n_keys, in
 constexpr int kTopkThreads = 1024;
 
 __device__ int block_exclusive_scan(int v, int* s_buf, int* total) {
-  // Hillis-Steele over kTopkThreads entries in LDS
-  const int t = threadIdx.x;
-  s_buf[t] = v;
-  __syncthreads();
-  for (int off = 1; off < kTopkThreads; off <<= 1) {
-    const int x = t >= off ? s_buf[t - off] : 0;
-    __syncthreads();
-    s_buf[t] += x;
-    __syncthreads();
+  // inclusive scan inside each wave (lane shuffles), then the 16 wave totals
+  // from LDS: two barriers for the whole workgroup
+  constexpr int NW = kTopkThreads / 64;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  int x = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(x, off);
+    if (lane >= off) x += y;
   }
-  const int incl = s_buf[t];
-  *total = s_buf[kTopkThreads - 1];
+  if (lane == 63) s_buf[wave] = x;
   __syncthreads();
-  return incl - v;
+  int before = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    const int sw = s_buf[w];
+    before += w < wave ? sw : 0;
+    tot += sw;
+  }
+  *total = tot;
+  __syncthreads();                 // s_buf is free for the next scan
+  return before + x - v;
 }
 
 // Indices of the k largest chunk scores of one head (ties to the lower
@@ -531,7 +539,8 @@ template <int PER>
 __global__ __launch_bounds__(kTopkThreads) void topk_reg_kernel(const float* __restrict__ S, int64_t n_chunks,
                                                                  int k, int b, int32_t* __restrict__ idx_out) {
   constexpr int NCOPY = 16;                // histogram copies (lane & 15): hot bins spread 16 ways
-  __shared__ int s_histc[NCOPY][256];
+  // copies padded to 257 words: one bin's copies fall into different LDS banks
+  __shared__ int s_histc[NCOPY][257];
   __shared__ int s_hist[256];
   __shared__ int s_scan[kTopkThreads];
   __shared__ uint32_t s_prefix;
@@ -545,11 +554,37 @@ __global__ __launch_bounds__(kTopkThreads) void topk_reg_kernel(const float* __r
   for (int i = 0; i < PER; ++i) key[i] = lo + i < n_chunks ? ord_key(Ss[lo + i]) : 0u;   // 0: below every score
   const int n_valid = (int)max<int64_t>(0, min<int64_t>(PER, n_chunks - lo));
 
+  // bits shared by every valid key: a radix digit made only of such bits puts
+  // all keys in one bin, so its pass is skipped (chunk scores share their sign
+  // and most exponent bits)
+  __shared__ uint32_t s_and[kTopkThreads / 64], s_or[kTopkThreads / 64];
+  uint32_t kand = 0xFFFFFFFFu, kor = 0u;
+#pragma unroll
+  for (int i = 0; i < PER; ++i)
+    if (i < n_valid) { kand &= key[i]; kor |= key[i]; }
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    kand &= (uint32_t)__shfl_xor((int)kand, off);
+    kor |= (uint32_t)__shfl_xor((int)kor, off);
+  }
+  if ((t & 63) == 0) { s_and[t >> 6] = kand; s_or[t >> 6] = kor; }
+  __syncthreads();
+  kand = 0xFFFFFFFFu;
+  kor = 0u;
+#pragma unroll
+  for (int w = 0; w < kTopkThreads / 64; ++w) { kand &= s_and[w]; kor |= s_or[w]; }
+  const uint32_t varying = kand ^ kor;
+
   uint32_t prefix = 0, mask = 0;
   int remaining = k;
   for (int pass = 0; pass < 4; ++pass) {
     const int shift = 24 - 8 * pass;
-    for (int i = t; i < NCOPY * 256; i += kTopkThreads) (&s_histc[0][0])[i] = 0;
+    if (((varying >> shift) & 255u) == 0u) {      // the same digit everywhere (uniform branch)
+      prefix |= kand & (255u << shift);
+      mask |= 255u << shift;
+      continue;
+    }
+    for (int i = t; i < NCOPY * 257; i += kTopkThreads) (&s_histc[0][0])[i] = 0;
     __syncthreads();
     const int cp = t & (NCOPY - 1);
 #pragma unroll
@@ -679,7 +714,7 @@ struct CvState {                 // per KV head, in the workspace
   uint32_t prefix;               // radix prefix of the order statistic x_(lo)
   int32_t remaining;             // 0-based rank still to resolve inside the prefix
   uint32_t min_above_key;        // smallest ordered key strictly above x_(lo)
-  uint32_t pad;
+  uint32_t need_scan;            // 1: min_above_key must come from a pass over A
   unsigned long long cnt_lt;     // entries strictly below x_(lo)
   double phi;
   unsigned long long sum_c, sum_c2;
@@ -703,6 +738,7 @@ __global__ void cv_init_kernel(CvState* st, uint32_t* hist, int64_t N, double k_
     s.prefix = 0;
     s.remaining = (int32_t)(int64_t)floor((double)(N - 1) * k_pct);
     s.min_above_key = 0xFFFFFFFFu;
+    s.need_scan = 0;
     s.cnt_lt = 0;
     s.phi = 0.0;
     s.sum_c = 0;
@@ -711,7 +747,21 @@ __global__ void cv_init_kernel(CvState* st, uint32_t* hist, int64_t N, double k_
 }
 
 // Histogram of one radix digit over the entries whose higher digits match
-// the prefix found so far.  hist: [hkv][kRadixBins] for this pass.
+// the prefix found so far.  hist: [hkv][kRadixBins] for this pass.  The
+// probabilities of A crowd into a few digits, so each wave first counts the
+// lanes that share its leading lane's digit with one ballot and one atomic;
+// only the other lanes add one by one.  16-byte loads, 4 entries per lane.
+__device__ __forceinline__ void hist_add(uint32_t* s_h, bool valid, uint32_t bin) {
+  const uint64_t act = __builtin_amdgcn_ballot_w64(valid);
+  if (act == 0) return;
+  const int lead = __builtin_ctzll(act);
+  const uint32_t lb = (uint32_t)__builtin_amdgcn_readlane((int)bin, lead);
+  const uint64_t same = __builtin_amdgcn_ballot_w64(valid && bin == lb);
+  const int lane = threadIdx.x & 63;
+  if (lane == lead) atomicAdd(&s_h[lb], (uint32_t)__builtin_popcountll(same));
+  else if (valid && bin != lb) atomicAdd(&s_h[bin], 1u);
+}
+
 __global__ void radix_hist_kernel(const float* __restrict__ A, int64_t N, int pass,
                                   const CvState* __restrict__ st, uint32_t* __restrict__ hist) {
   __shared__ uint32_t s_h[kRadixBins];
@@ -722,7 +772,18 @@ __global__ void radix_hist_kernel(const float* __restrict__ A, int64_t N, int pa
   const int shift = digit_shift(pass);
   const uint32_t dmask = pass == 2 ? 0x3FFu : 0x7FFu;
   const float* Ah = A + (size_t)h * N;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N;
+  const int64_t n4 = (N & 3) == 0 && ((reinterpret_cast<uintptr_t>(Ah) & 15) == 0) ? N / 4 : 0;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (int64_t)gridDim.x * blockDim.x) {
+    const float4 v = *reinterpret_cast<const float4*>(Ah + 4 * i);
+    const float f[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const uint32_t key = ord_key(f[e]);
+      hist_add(s_h, (key & pm) == pv, (key >> shift) & dmask);
+    }
+  }
+  // entries not covered by the 16-byte loads (N not a multiple of 4, or an unaligned head)
+  for (int64_t i = 4 * n4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N;
        i += (int64_t)gridDim.x * blockDim.x) {
     const uint32_t key = ord_key(Ah[i]);
     if ((key & pm) == pv) atomicAdd(&s_h[(key >> shift) & dmask], 1u);
@@ -732,35 +793,106 @@ __global__ void radix_hist_kernel(const float* __restrict__ A, int64_t N, int pa
     if (s_h[i]) atomicAdd(&hist[(size_t)h * kRadixBins + i], s_h[i]);
 }
 
-// Pick the digit that holds the target rank; one thread per head.  The
-// entries of lower digits are strictly below x_(lo) and are counted.
-__global__ void radix_pick_kernel(const uint32_t* __restrict__ hist, int pass, CvState* st, int hkv) {
-  const int h = blockIdx.x * blockDim.x + threadIdx.x;
-  if (h >= hkv) return;
+// Pick the digit that holds the target rank: one 256-thread workgroup per
+// head, 8 bins per thread, a block scan of the per-thread sums.  The entries
+// of lower digits are strictly below x_(lo) and are counted.  After the last
+// pass the smallest key above x_(lo) is read off the same histogram when it
+// lies in x_(lo)'s bucket; otherwise a pass over A is requested.
+constexpr int kPickThreads = 256;
+__global__ __launch_bounds__(kPickThreads) void radix_pick_kernel(const uint32_t* __restrict__ hist, int pass,
+                                                                  CvState* st, int hkv) {
+  constexpr int BPT = kRadixBins / kPickThreads;
+  __shared__ int64_t s_tot[kPickThreads / 64];
+  __shared__ int s_bin;
+  __shared__ int64_t s_cum;
+  __shared__ int s_next;
+  const int h = blockIdx.x;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const uint32_t* hh = hist + (size_t)h * kRadixBins;
   const int nb = pass == 2 ? 1024 : kRadixBins;
   const int64_t rem = st[h].remaining;
-  int64_t cum = 0;
-  int bin = 0;
-  for (bin = 0; bin < nb - 1; ++bin) {
-    if (cum + hh[bin] > rem) break;
-    cum += hh[bin];
+  uint32_t c[BPT];
+  int64_t mine = 0;
+#pragma unroll
+  for (int i = 0; i < BPT; ++i) {
+    const int bin = t * BPT + i;
+    c[i] = bin < nb ? hh[bin] : 0u;
+    mine += c[i];
   }
-  st[h].prefix |= (uint32_t)bin << digit_shift(pass);
-  st[h].remaining = (int32_t)(rem - cum);
-  st[h].cnt_lt += (unsigned long long)cum;
+  // exclusive prefix of `mine` over the workgroup
+  int64_t x = mine;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int64_t y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  if (lane == 63) s_tot[wave] = x;
+  if (t == 0) { s_bin = -1; s_next = 0x7FFFFFFF; }
+  __syncthreads();
+  int64_t before = x - mine;
+#pragma unroll
+  for (int w = 0; w < kPickThreads / 64; ++w) before += w < wave ? s_tot[w] : 0;
+  if (before <= rem && rem < before + mine) {
+    int64_t cum = before;
+    int i = 0;
+    for (i = 0; i < BPT - 1; ++i) {
+      if (cum + c[i] > rem) break;
+      cum += c[i];
+    }
+    s_bin = t * BPT + i;
+    s_cum = cum;
+  }
+  __syncthreads();
+  if (s_bin < 0) {            // rank beyond the counts (not reached with consistent counts): last bin
+    if (t == 0) {
+      int64_t cum = 0;
+      for (int b = 0; b < nb - 1; ++b) cum += hh[b];
+      s_bin = nb - 1;
+      s_cum = cum;
+    }
+    __syncthreads();
+  }
+  const int bin = s_bin;
+  if (pass == 2) {
+    // first non-empty bin above the chosen one, within x_(lo)'s 22-bit bucket
+#pragma unroll
+    for (int i = 0; i < BPT; ++i) {
+      const int b = t * BPT + i;
+      if (b > bin && b < nb && c[i] != 0u) atomicMin(&s_next, b);
+    }
+  }
+  __syncthreads();
+  if (t == 0) {
+    const uint32_t prefix = st[h].prefix | ((uint32_t)bin << digit_shift(pass));
+    st[h].prefix = prefix;
+    st[h].remaining = (int32_t)(rem - s_cum);
+    st[h].cnt_lt += (unsigned long long)s_cum;
+    if (pass == 2) {
+      if (s_next != 0x7FFFFFFF) st[h].min_above_key = (prefix & ~0x3FFu) | (uint32_t)s_next;
+      else st[h].need_scan = 1;
+    }
+  }
 }
 
 // Smallest ordered key strictly above x_(lo) (needed when x_(lo + 1) differs).
 __global__ void radix_min_above_kernel(const float* __restrict__ A, int64_t N, CvState* st) {
   __shared__ uint32_t s_min;
   const int h = blockIdx.y;
+  if (!st[h].need_scan) return;       // found in the last radix histogram
   if (threadIdx.x == 0) s_min = 0xFFFFFFFFu;
   __syncthreads();
   const uint32_t x = st[h].prefix;
   const float* Ah = A + (size_t)h * N;
   uint32_t mn = 0xFFFFFFFFu;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N;
+  const int64_t n4 = (N & 3) == 0 && ((reinterpret_cast<uintptr_t>(Ah) & 15) == 0) ? N / 4 : 0;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (int64_t)gridDim.x * blockDim.x) {
+    const float4 v = *reinterpret_cast<const float4*>(Ah + 4 * i);
+    const uint32_t k4[4] = {ord_key(v.x), ord_key(v.y), ord_key(v.z), ord_key(v.w)};
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+      if (k4[e] > x) mn = min(mn, k4[e]);
+  }
+  for (int64_t i = 4 * n4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N;
        i += (int64_t)gridDim.x * blockDim.x) {
     const uint32_t key = ord_key(Ah[i]);
     if (key > x) mn = min(mn, key);
@@ -788,6 +920,8 @@ __global__ void cv_threshold_kernel(CvState* st, const uint32_t* __restrict__ hi
 }
 
 // C_j = #{i : A[i][j] >= Phi} (Eq. 2-3); exact integer sums of C and C^2.
+// Four adjacent columns per thread through 16-byte loads when the row stride
+// allows it, eight rows in flight; the comparison stays in fp64 against Phi.
 __global__ void cv_count_kernel(const float* __restrict__ A, int lq, int64_t n_keys, CvState* st) {
   __shared__ unsigned long long s1, s2;
   const int h = blockIdx.y;
@@ -796,7 +930,39 @@ __global__ void cv_count_kernel(const float* __restrict__ A, int lq, int64_t n_k
   const double phi = st[h].phi;
   const float* Ah = A + (size_t)h * lq * n_keys;
   unsigned long long a1 = 0, a2 = 0;
-  for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n_keys;
+  const bool vec = (n_keys & 3) == 0 && (reinterpret_cast<uintptr_t>(Ah) & 15) == 0;
+  const int64_t nq = vec ? n_keys / 4 : 0;
+  for (int64_t jq = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; jq < nq;
+       jq += (int64_t)gridDim.x * blockDim.x) {
+    unsigned int c[4] = {0u, 0u, 0u, 0u};
+    const float* col = Ah + 4 * jq;
+    int i = 0;
+    for (; i + 8 <= lq; i += 8) {
+      float4 v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = *reinterpret_cast<const float4*>(col + (size_t)(i + u) * n_keys);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        c[0] += (double)v[u].x >= phi;
+        c[1] += (double)v[u].y >= phi;
+        c[2] += (double)v[u].z >= phi;
+        c[3] += (double)v[u].w >= phi;
+      }
+    }
+    for (; i < lq; ++i) {
+      const float4 v = *reinterpret_cast<const float4*>(col + (size_t)i * n_keys);
+      c[0] += (double)v.x >= phi;
+      c[1] += (double)v.y >= phi;
+      c[2] += (double)v.z >= phi;
+      c[3] += (double)v.w >= phi;
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      a1 += c[e];
+      a2 += (unsigned long long)c[e] * c[e];
+    }
+  }
+  for (int64_t j = 4 * nq + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n_keys;
        j += (int64_t)gridDim.x * blockDim.x) {
     unsigned long long cj = 0;
     for (int i = 0; i < lq; ++i) cj += (double)Ah[(size_t)i * n_keys + j] >= phi;
@@ -1005,7 +1171,7 @@ hipError_t launch_score(int dtype, const ScoreGeom& g, const void* q_rows, const
   for (int pass = 0; pass < 3; ++pass) {
     uint32_t* hp = hist + (size_t)pass * g.hkv * kRadixBins;
     hipLaunchKernelGGL(radix_hist_kernel, dim3(hb, g.hkv), dim3(256), 0, stream, a.obs, N, pass, st, hp);
-    hipLaunchKernelGGL(radix_pick_kernel, dim3(pb), dim3(64), 0, stream, hp, pass, st, g.hkv);
+    hipLaunchKernelGGL(radix_pick_kernel, dim3(g.hkv), dim3(kPickThreads), 0, stream, hp, pass, st, g.hkv);
   }
   hipLaunchKernelGGL(radix_min_above_kernel, dim3(hb, g.hkv), dim3(256), 0, stream, a.obs, N, st);
   hipLaunchKernelGGL(cv_threshold_kernel, dim3(pb), dim3(64), 0, stream, st,
