@@ -122,6 +122,80 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def time_decode_shape(torch, ck, wl, dev, stream, steps):
+    """Decode step time at a workload's shapes with K/V drawn on the GPU (the
+    values do not change the work): consistent heads hold b*cs + L_obs rows
+    (Eq. 5's count of the 8 heads for the workload's r), adaptive heads their
+    whole context; enough layer copies to exceed 1 GB rotate so the Infinity
+    Cache cannot serve a step; HIP-graph replays."""
+    import synth
+    from paper_2608_30295_amd import _lib
+    from paper_2608_30295_amd._lib import check, lib
+    hq, hkv, d = wl.hq, wl.hkv, wl.d
+    n_cons = hkv - 1 - int(math.floor((hkv - 1) * wl.r))
+    cons = list(range(1, 1 + n_cons))                  # which heads are consistent does not change the work
+    lens_b = synth.sequence_lengths(wl)
+    comp = wl.chunk_budget * wl.cs + wl.l_obs
+    vl = [[comp if h in cons else lens_b[b] for h in range(hkv)] for b in range(wl.batch)]
+    kv_bytes = sum(sum(r) for r in vl) * d * 2 * 2
+    n_cp = max(2, math.ceil(1.0e9 / kv_bytes))
+    copies = []
+    for _ in range(n_cp):
+        bufs, pairs = [], []
+        for b in range(wl.batch):
+            for h in range(hkv):
+                kk = torch.empty((vl[b][h], d), dtype=torch.bfloat16, device=dev).normal_()
+                vv = torch.empty_like(kk).normal_()
+                bufs += [kk, vv]
+                pairs.append((kk.data_ptr(), vv.data_ptr()))
+        copies.append((bufs, ck.kv_table(pairs, dev)))
+    lens = torch.tensor(vl, dtype=torch.int64, device=dev)
+    plan = ck.decode_plan(np.array(vl, dtype=np.int64), hq, hkv, dev)
+    nq = 8
+    qs = [torch.empty((wl.batch, hq, d), dtype=torch.bfloat16, device=dev).normal_() for _ in range(nq)]
+    out = torch.empty((wl.batch, hq, d), dtype=torch.float32, device=dev)
+    scale = 1.0 / math.sqrt(d)
+
+    def step(t, st):
+        check(lib().catekv_decode_attn(1, _lib.ctypes.byref(plan.plan), qs[t % nq].data_ptr(),
+                                       copies[t % n_cp][1].data_ptr(), lens.data_ptr(), wl.batch, hq, hkv, d,
+                                       scale, out.data_ptr(), None, plan.ws.data_ptr(), plan.ws.numel(),
+                                       st.cuda_stream))
+    for t in range(5):
+        step(t, stream)
+    torch.cuda.synchronize()
+    cyc = min(64, n_cp * nq // math.gcd(n_cp, nq))
+    s2 = torch.cuda.Stream(device=dev)
+    s2.wait_stream(stream)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s2):
+        g.capture_begin()
+        for t in range(cyc):
+            step(t, s2)
+        g.capture_end()
+    stream.wait_stream(s2)
+    torch.cuda.synchronize()
+    reps = max(1, round(min(steps, 100) / cyc))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        g.replay()
+    e1.record(stream)
+    e1.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / (reps * cyc)
+    algo = kv_bytes + wl.batch * hq * d * 2 + wl.batch * hq * d * 4
+    res = {"workload": wl.name, "batch": wl.batch, "consistent_heads_per_seq": n_cons,
+           "kv_tokens": int(sum(sum(r) for r in vl)), "bytes_per_step": int(algo), "us_per_step": round(us, 2),
+           "gbs": round(algo / (us * 1e-6) / 1e9, 1), "hbm_peak_frac": round(algo / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+           "layer_copies": n_cp, "workgroups": int(plan.plan.n_workers)}
+    if wl.batch > 1:
+        res["tokens_per_s"] = round(wl.batch / (us * 1e-6), 1)
+    log(f"[bench] {wl.name}: {us:.2f} us/step, {res['gbs']} GB/s on {algo / 1e6:.1f} MB per step")
+    del copies, g
+    torch.cuda.empty_cache()
+    return res
+
+
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
@@ -136,6 +210,8 @@ def parse():
     p.add_argument("--no-next", action="store_true",
                    help="skip the decode-time append timing and the retention sweep")
     p.add_argument("--etas", default="0.5,0.25,0.1", help="retention ratios of the adaptive heads to sweep")
+    p.add_argument("--no-workloads", action="store_true",
+                   help="skip the decode timing at the other workloads' shapes")
     p.add_argument("--copy-probe", action="store_true",
                    help=f"after timing, run a streaming kernel over {COPY_PROBE_BYTES} bytes (counter scale)")
     p.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -533,6 +609,12 @@ def main():
         if adaptive:
             next_res["query_aware_retrieval"] = time_retrieval()
 
+    # ---------------- decode at the other workloads' shapes ----------------
+    other = None
+    if not args.no_workloads:
+        other = [time_decode_shape(torch, ck, synth.WORKLOADS[name], dev, stream, args.steps)
+                 for name in ("ctx32k_bf16", "batch16_ragged_bf16", "ctx1m_bf16")]
+
     # ---------------- CPU oracle on a bounded sample ----------------
     cpu = None
     if not args.no_cpu_baseline:
@@ -607,6 +689,7 @@ def main():
         },
         "cpu_baseline": cpu,
         "next": next_res,
+        "other_workloads": other,
     }
     print(json.dumps(res), flush=True)
 
