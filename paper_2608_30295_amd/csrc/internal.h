@@ -23,7 +23,7 @@ struct DecodeItem {
 
 constexpr int kDecodeWaves = 4;    // waves per decode workgroup
 constexpr int kDecodeStages = 4;   // register prefetch depth (fp32 path)
-constexpr int kDecodeStagesMfma = 3;   // register prefetch depth (bf16 MFMA path, 16-token stages)
+constexpr int kDecodeStagesMfma = 2;   // register prefetch depth (bf16 MFMA path, 16-token stages)
 constexpr int kDecodeQuantum = 64; // tokens per workgroup load stage (16 per wave)
 
 // Per view: where its partial slots live and how many segments cover it.

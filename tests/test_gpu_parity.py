@@ -140,6 +140,62 @@ def test_decode_repeated_steps_reuse_plan():
     assert_rows_close(outs[0].cpu().numpy()[0], o_ref, "bf16")
 
 
+@pytest.mark.parametrize("G", [4, 8])
+def test_decode_steps_alternating_inputs_and_graph_replays(G):
+    # consecutive steps with other queries and caches on one plan and
+    # workspace must each match the oracle (no partial of an earlier step
+    # leaks into a later merge), and graph replays must reproduce the eager
+    # steps bit for bit
+    rng = np.random.default_rng(15 + G)
+    B, hkv = 2, 2
+    hq = G * hkv
+    lens = [9000, 500, 30000, 64]
+    sets = [_views(rng, lens, "bf16"), _views(rng, lens, "bf16")]
+    qs = [synth.f32_to_bf16_bits(rng.standard_normal((B, hq, 128), dtype=np.float32)) for _ in range(3)]
+    say(f"decode alternating steps G={G}")
+    kds = [[(to_dev(k), to_dev(v)) for k, v in vs] for vs in sets]
+    tables = [ck.kv_table([(k.data_ptr(), v.data_ptr()) for k, v in kd], DEV) for kd in kds]
+    plan = ck.decode_plan(np.array(lens), hq, hkv, DEV, split_tokens=256)
+    assert plan.plan.n_multi == 3
+    lens_dev = torch.tensor(lens, dtype=torch.int64, device=DEV)
+    qd = [to_dev(q) for q in qs]
+    steps = [(0, 0), (1, 1), (2, 0), (0, 1), (1, 0)]
+    outs = [torch.empty((B, hq, 128), dtype=torch.float32, device=DEV) for _ in steps]
+    lses = [torch.empty((B, hq), dtype=torch.float32, device=DEV) for _ in steps]
+    for i, (qi, si) in enumerate(steps):
+        ck.decode_attn(plan, qd[qi], tables[si], lens_dev, out=outs[i], lse=lses[i])
+    torch.cuda.synchronize()
+    eager = [(o.clone(), l.clone()) for o, l in zip(outs, lses)]
+    for i, (qi, si) in enumerate(steps):
+        qq = f64(qs[qi])
+        for b in range(B):
+            vv = [(f64(sets[si][b * hkv + h][0]), f64(sets[si][b * hkv + h][1])) for h in range(hkv)]
+            o_ref, l_ref = O.decode_gqa(qq[b], vv)
+            assert_rows_close(eager[i][0].cpu().numpy()[b], o_ref, "bf16", f"step {i} b={b}")
+            np.testing.assert_allclose(eager[i][1].cpu().numpy()[b], l_ref, atol=1e-4, rtol=0)
+    s2 = torch.cuda.Stream(device=DEV)
+    s2.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s2):
+        g.capture_begin()
+        for i, (qi, si) in enumerate(steps):
+            ck.decode_attn(plan, qd[qi], tables[si], lens_dev, out=outs[i], lse=lses[i])
+        g.capture_end()
+    torch.cuda.current_stream().wait_stream(s2)
+    for rep in range(3):
+        for o in outs:
+            o.fill_(7.0)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for i in range(len(steps)):
+            assert torch.equal(outs[i], eager[i][0]), f"replay {rep} step {i}"
+            assert torch.equal(lses[i], eager[i][1]), f"replay {rep} step {i}"
+        # eager work between replays on the same plan
+        ck.decode_attn(plan, qd[2], tables[1], lens_dev)
+        torch.cuda.synchronize()
+
+
 # ---------------------------------------------------------------- selection
 
 def _small(name, **kw):
