@@ -532,51 +532,59 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(const float* __restr
 }
 
 
-// Same selection with the scores held in registers: thread t owns the
-// contiguous chunks [t * PER, (t + 1) * PER), loaded once; the four radix
-// passes only touch LDS (histogram) and registers.
+// Same selection with the scores held in registers.  Wave w owns the
+// contiguous range [w * PER * 64, (w + 1) * PER * 64): its row i is the 64
+// consecutive chunks from w * PER * 64 + 64 i, one per lane, so every load
+// of the wave is one contiguous 256-byte read and ascending (row, lane) is
+// ascending index.  Radix passes over 8-bit digits count into 16 LDS copies
+// (lane & 15) of the histogram, double-buffered so the copy for the next
+// pass is cleared during this one; wave 0 sums the copies and finds the bin
+// of the target rank with a suffix scan, so a pass costs two barriers.  The
+// positions of the selected entries come from per-row ballots and one
+// exchange of the per-wave counts.
 template <int PER>
-__global__ __launch_bounds__(kTopkThreads) void topk_reg_kernel(const float* __restrict__ S, int64_t n_chunks,
+__global__ __launch_bounds__(kTopkThreads) void topk_wave_kernel(const float* __restrict__ S, int64_t n_chunks,
                                                                  int k, int b, int32_t* __restrict__ idx_out) {
-  constexpr int NCOPY = 16;                // histogram copies (lane & 15): hot bins spread 16 ways
-  // copies padded to 257 words: one bin's copies fall into different LDS banks
-  __shared__ int s_histc[NCOPY][257];
-  __shared__ int s_hist[256];
-  __shared__ int s_scan[kTopkThreads];
+  constexpr int NW = kTopkThreads / 64;
+  constexpr int NCOPY = 16;
+  constexpr int RS = 260;                  // words per copy: 256 bins, rows 16-byte aligned
+  __shared__ __attribute__((aligned(16))) int s_h[2][NCOPY][RS];
+  __shared__ uint32_t s_and[NW], s_or[NW];
+  __shared__ int s_gt[NW], s_eq[NW];
   __shared__ uint32_t s_prefix;
   __shared__ int s_remaining;
-  const int sel = blockIdx.x;
-  const float* Ss = S + (size_t)sel * n_chunks;
-  const int t = threadIdx.x;
-  const int64_t lo = (int64_t)t * PER;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const float* Ss = S + (size_t)blockIdx.x * n_chunks;
+  const int64_t base = (int64_t)wave * PER * 64 + lane;       // chunk of row 0; row i adds 64 i
+  const int64_t rem = n_chunks - base;
+  const int nv = rem <= 0 ? 0 : (int)min<int64_t>(PER, (rem + 63) / 64);   // rows holding a chunk
   uint32_t key[PER];
 #pragma unroll
-  for (int i = 0; i < PER; ++i) key[i] = lo + i < n_chunks ? ord_key(Ss[lo + i]) : 0u;   // 0: below every score
-  const int n_valid = (int)max<int64_t>(0, min<int64_t>(PER, n_chunks - lo));
+  for (int i = 0; i < PER; ++i) key[i] = i < nv ? ord_key(Ss[base + 64 * i]) : 0u;
 
-  // bits shared by every valid key: a radix digit made only of such bits puts
-  // all keys in one bin, so its pass is skipped (chunk scores share their sign
-  // and most exponent bits)
-  __shared__ uint32_t s_and[kTopkThreads / 64], s_or[kTopkThreads / 64];
+  // bits shared by every key: a digit made only of such bits puts all keys in
+  // one bin, so its pass is skipped (chunk scores share sign and most exponent bits)
   uint32_t kand = 0xFFFFFFFFu, kor = 0u;
 #pragma unroll
   for (int i = 0; i < PER; ++i)
-    if (i < n_valid) { kand &= key[i]; kor |= key[i]; }
+    if (i < nv) { kand &= key[i]; kor |= key[i]; }
 #pragma unroll
   for (int off = 1; off < 64; off <<= 1) {
     kand &= (uint32_t)__shfl_xor((int)kand, off);
     kor |= (uint32_t)__shfl_xor((int)kor, off);
   }
-  if ((t & 63) == 0) { s_and[t >> 6] = kand; s_or[t >> 6] = kor; }
+  if (lane == 0) { s_and[wave] = kand; s_or[wave] = kor; }
+  for (int i = t; i < NCOPY * RS; i += kTopkThreads) (&s_h[0][0][0])[i] = 0;
   __syncthreads();
   kand = 0xFFFFFFFFu;
   kor = 0u;
 #pragma unroll
-  for (int w = 0; w < kTopkThreads / 64; ++w) { kand &= s_and[w]; kor |= s_or[w]; }
+  for (int w = 0; w < NW; ++w) { kand &= s_and[w]; kor |= s_or[w]; }
   const uint32_t varying = kand ^ kor;
 
   uint32_t prefix = 0, mask = 0;
-  int remaining = k;
+  int remaining = k;       // rank (from the top) still to locate among keys matching the prefix
+  int cur = 0;
   for (int pass = 0; pass < 4; ++pass) {
     const int shift = 24 - 8 * pass;
     if (((varying >> shift) & 255u) == 0u) {      // the same digit everywhere (uniform branch)
@@ -584,39 +592,36 @@ __global__ __launch_bounds__(kTopkThreads) void topk_reg_kernel(const float* __r
       mask |= 255u << shift;
       continue;
     }
-    for (int i = t; i < NCOPY * 257; i += kTopkThreads) (&s_histc[0][0])[i] = 0;
-    __syncthreads();
-    const int cp = t & (NCOPY - 1);
+    for (int i = t; i < NCOPY * RS; i += kTopkThreads) (&s_h[cur ^ 1][0][0])[i] = 0;
+    const int cp = lane & (NCOPY - 1);
 #pragma unroll
     for (int i = 0; i < PER; ++i)
-      if (i < n_valid && (key[i] & mask) == prefix) atomicAdd(&s_histc[cp][(key[i] >> shift) & 255], 1);
+      if (i < nv && (key[i] & mask) == prefix) atomicAdd(&s_h[cur][cp][(key[i] >> shift) & 255u], 1);
     __syncthreads();
-    if (t < 256) {
-      int v = 0;
+    if (wave == 0) {
+      // lane l holds bins 4 l .. 4 l + 3; suffix sums over the lanes count the bins above
+      int h0 = 0, h1 = 0, h2 = 0, h3 = 0;
 #pragma unroll
-      for (int c2 = 0; c2 < NCOPY; ++c2) v += s_histc[c2][t];
-      s_hist[t] = v;
-    }
-    __syncthreads();
-    if (t < 64) {
-      // wave 0 finds, from the top bin down, the bin where the count reaches `remaining`
-      int h[4], c4 = 0;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) { h[i] = s_hist[255 - (4 * t + i)]; c4 += h[i]; }
-      // inclusive scan of c4 over the 64 lanes (bins 255 .. 0)
+      for (int c = 0; c < NCOPY; ++c) {
+        const int4 v = *reinterpret_cast<const int4*>(&s_h[cur][c][4 * lane]);
+        h0 += v.x; h1 += v.y; h2 += v.z; h3 += v.w;
+      }
+      const int c4 = h0 + h1 + h2 + h3;
       int incl = c4;
+#pragma unroll
       for (int off = 1; off < 64; off <<= 1) {
-        const int y = __shfl_up(incl, off);
-        if (t >= off) incl += y;
+        const int y = __shfl_down(incl, off);
+        if (lane + off < 64) incl += y;
       }
       const int excl = incl - c4;
       if (excl < remaining && incl >= remaining) {
-        int cum = excl, i = 0;
-        for (i = 0; i < 3; ++i) {
-          if (cum + h[i] >= remaining) break;
-          cum += h[i];
+        const int h[4] = {h0, h1, h2, h3};
+        int cum = excl, j = 3;
+        for (; j > 0; --j) {
+          if (cum + h[j] >= remaining) break;
+          cum += h[j];
         }
-        s_prefix = prefix | ((uint32_t)(255 - (4 * t + i)) << shift);
+        s_prefix = prefix | ((uint32_t)(4 * lane + j) << shift);
         s_remaining = remaining - cum;
       }
     }
@@ -624,36 +629,41 @@ __global__ __launch_bounds__(kTopkThreads) void topk_reg_kernel(const float* __r
     prefix = s_prefix;
     remaining = s_remaining;
     mask |= 255u << shift;
-    __syncthreads();
+    cur ^= 1;
   }
-  const uint32_t tau = prefix;
-  int n_eq = 0;
+  const uint32_t tau = prefix;   // key of the k-th largest score
+  // `remaining` entries equal to tau are taken, lowest indices first
+
+  int n_gt = 0, n_eq = 0;
 #pragma unroll
-  for (int i = 0; i < PER; ++i) n_eq += (i < n_valid && key[i] == tau);
-  int tot;
-  const int eq_before = block_exclusive_scan(n_eq, s_scan, &tot);
-  int n_take = 0;
-  {
-    int eb = eq_before;
+  for (int i = 0; i < PER; ++i)
+    if (i < nv) { n_gt += key[i] > tau; n_eq += key[i] == tau; }
 #pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      if (i >= n_valid) continue;
-      if (key[i] > tau) ++n_take;
-      else if (key[i] == tau) { if (eb < remaining) ++n_take; ++eb; }
-    }
+  for (int off = 1; off < 64; off <<= 1) {
+    n_gt += __shfl_xor(n_gt, off);
+    n_eq += __shfl_xor(n_eq, off);
   }
-  int pos = block_exclusive_scan(n_take, s_scan, &tot);
-  int32_t* out = idx_out + (size_t)sel * b;
-  {
-    int eb = eq_before;
+  if (lane == 0) { s_gt[wave] = n_gt; s_eq[wave] = n_eq; }
+  __syncthreads();
+  int pos = 0, eqr = 0;          // entries taken and ties seen in the waves before this one
+  for (int w = 0; w < wave; ++w) {
+    const int e = s_eq[w];
+    pos += s_gt[w] + min(max(remaining - eqr, 0), e);
+    eqr += e;
+  }
+  int32_t* out = idx_out + (size_t)blockIdx.x * b;
+  const uint64_t below = __lanemask_lt();
 #pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      if (i >= n_valid) continue;
-      bool take = false;
-      if (key[i] > tau) take = true;
-      else if (key[i] == tau) { take = eb < remaining; ++eb; }
-      if (take && pos < k) out[pos++] = (int32_t)(lo + i);
-    }
+  for (int i = 0; i < PER; ++i) {
+    const bool v = i < nv;
+    const bool gt = v && key[i] > tau, eq = v && key[i] == tau;
+    const uint64_t meq = __ballot(eq);
+    const bool take = gt || (eq && eqr + __popcll(meq & below) < remaining);
+    const uint64_t mt = __ballot(take);
+    const int p = pos + __popcll(mt & below);
+    if (take && p < k) out[p] = (int32_t)(base + 64 * i);
+    pos += __popcll(mt);
+    eqr += __popcll(meq);
   }
   for (int i = k + t; i < b; i += kTopkThreads) out[i] = -1;
 }
@@ -1088,9 +1098,9 @@ hipError_t launch_select(int dtype, const SelectGeom& g, const void* q_obs, cons
 hipError_t launch_topk(const float* S, int n_rows, int64_t n, int b, int32_t* idx_out, hipStream_t stream) {
   const int k_eff = (int)(b < n ? b : n);
   if (n <= 16 * kTopkThreads)
-    hipLaunchKernelGGL(topk_reg_kernel<16>, dim3(n_rows), dim3(kTopkThreads), 0, stream, S, n, k_eff, b, idx_out);
+    hipLaunchKernelGGL(topk_wave_kernel<16>, dim3(n_rows), dim3(kTopkThreads), 0, stream, S, n, k_eff, b, idx_out);
   else if (n <= 32 * kTopkThreads)
-    hipLaunchKernelGGL(topk_reg_kernel<32>, dim3(n_rows), dim3(kTopkThreads), 0, stream, S, n, k_eff, b, idx_out);
+    hipLaunchKernelGGL(topk_wave_kernel<32>, dim3(n_rows), dim3(kTopkThreads), 0, stream, S, n, k_eff, b, idx_out);
   else
     hipLaunchKernelGGL(topk_kernel, dim3(n_rows), dim3(kTopkThreads), 0, stream, S, n, k_eff, b, idx_out);
   return hipGetLastError();

@@ -222,6 +222,28 @@ def test_retrieve_more_pages_than_exist():
     assert idx[0].tolist() == list(range(7)) + [-1, -1, -1]
 
 
+@pytest.mark.parametrize("n_pages", [9000, 20000])
+def test_retrieve_exact_ties_lowest_pages_first(n_pages):
+    """Pages repeat 37 random patterns, so page scores tie exactly in groups
+    and the k-th score falls inside a group: the chosen pages must be the
+    oracle's (ties to the lower page), on both register layouts of the top-k
+    (up to 16384 and up to 32768 scores)."""
+    rng = np.random.default_rng(40 + n_pages)
+    cs, n_keep, G = 8, 700, 4
+    pat = synth.f32_to_bf16_bits(rng.standard_normal((37, cs, 128), dtype=np.float32))
+    kk = pat[np.arange(n_pages) % 37].reshape(1, n_pages * cs, 128)
+    q_st = synth.f32_to_bf16_bits(rng.standard_normal((G, 128), dtype=np.float32))
+    say(f"retrieve ties: pages={n_pages} keep={n_keep}")
+    kmin, kmax = ck.page_bounds(to_dev(kk), [0], cs)
+    idx = ck.retrieve_pages(to_dev(q_st), kmin, kmax, [0], 1, n_keep).cpu().numpy()[0]
+    mn, mx = O.page_bounds(f64(kk[0]), cs)
+    sc = O.page_scores(f64(q_st), mn, mx)
+    want = O.argtopk_ascending(sc, n_keep)
+    kth = np.sort(sc)[::-1][n_keep - 1]
+    assert (sc == kth).sum() > 1 and (sc > kth).sum() < n_keep   # the k-th lies inside a tie group
+    assert idx.tolist() == want.tolist()
+
+
 # ---------------------------------------------------- attention recall
 
 def test_recall_of_gpu_selection_and_retrieval_matches_oracle():
