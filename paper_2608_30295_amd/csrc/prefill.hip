@@ -930,57 +930,52 @@ __global__ void cv_threshold_kernel(CvState* st, const uint32_t* __restrict__ hi
 }
 
 // C_j = #{i : A[i][j] >= Phi} (Eq. 2-3); exact integer sums of C and C^2.
-// Four adjacent columns per thread through 16-byte loads when the row stride
-// allows it, eight rows in flight; the comparison stays in fp64 against Phi.
-__global__ void cv_count_kernel(const float* __restrict__ A, int lq, int64_t n_keys, CvState* st) {
+// A workgroup takes 64 adjacent columns at a time (one per lane, so every
+// row read is 256 contiguous bytes, whatever the row stride) and its four
+// waves split the rows, each with up to kCountRows loads in flight per lane;
+// the four partial counts of a column meet in LDS before C_j is squared.
+// The comparison stays in fp64 against Phi.
+constexpr int kCountRows = 16;
+__global__ __launch_bounds__(256) void cv_count_kernel(const float* __restrict__ A, int lq, int64_t n_keys,
+                                                        CvState* st) {
+  __shared__ unsigned int s_c[4][64];
   __shared__ unsigned long long s1, s2;
   const int h = blockIdx.y;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;   // wave = row group
   if (threadIdx.x == 0) { s1 = 0; s2 = 0; }
   __syncthreads();
   const double phi = st[h].phi;
   const float* Ah = A + (size_t)h * lq * n_keys;
+  const int rpg = (lq + 3) / 4;
+  const int r0 = wave * rpg, r1 = min(lq, r0 + rpg);
   unsigned long long a1 = 0, a2 = 0;
-  const bool vec = (n_keys & 3) == 0 && (reinterpret_cast<uintptr_t>(Ah) & 15) == 0;
-  const int64_t nq = vec ? n_keys / 4 : 0;
-  for (int64_t jq = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; jq < nq;
-       jq += (int64_t)gridDim.x * blockDim.x) {
-    unsigned int c[4] = {0u, 0u, 0u, 0u};
-    const float* col = Ah + 4 * jq;
-    int i = 0;
-    for (; i + 8 <= lq; i += 8) {
-      float4 v[8];
+  for (int64_t j0 = (int64_t)blockIdx.x * 64; j0 < n_keys; j0 += (int64_t)gridDim.x * 64) {
+    const int64_t j = j0 + lane;
+    unsigned int c = 0;
+    if (j < n_keys) {
+      for (int i0 = r0; i0 < r1; i0 += kCountRows) {
+        float v[kCountRows];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = *reinterpret_cast<const float4*>(col + (size_t)(i + u) * n_keys);
+        for (int u = 0; u < kCountRows; ++u)
+          if (i0 + u < r1) v[u] = Ah[(size_t)(i0 + u) * n_keys + j];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        c[0] += (double)v[u].x >= phi;
-        c[1] += (double)v[u].y >= phi;
-        c[2] += (double)v[u].z >= phi;
-        c[3] += (double)v[u].w >= phi;
+        for (int u = 0; u < kCountRows; ++u)
+          if (i0 + u < r1) c += (double)v[u] >= phi;
       }
     }
-    for (; i < lq; ++i) {
-      const float4 v = *reinterpret_cast<const float4*>(col + (size_t)i * n_keys);
-      c[0] += (double)v.x >= phi;
-      c[1] += (double)v.y >= phi;
-      c[2] += (double)v.z >= phi;
-      c[3] += (double)v.w >= phi;
+    s_c[wave][lane] = c;
+    __syncthreads();
+    if (wave == 0 && j < n_keys) {
+      const unsigned int cj = s_c[0][lane] + s_c[1][lane] + s_c[2][lane] + s_c[3][lane];
+      a1 += cj;
+      a2 += (unsigned long long)cj * cj;
     }
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      a1 += c[e];
-      a2 += (unsigned long long)c[e] * c[e];
-    }
+    __syncthreads();
   }
-  for (int64_t j = 4 * nq + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n_keys;
-       j += (int64_t)gridDim.x * blockDim.x) {
-    unsigned long long cj = 0;
-    for (int i = 0; i < lq; ++i) cj += (double)Ah[(size_t)i * n_keys + j] >= phi;
-    a1 += cj;
-    a2 += cj * cj;
+  if (wave == 0) {              // only wave 0 holds sums
+    atomicAdd(&s1, a1);
+    atomicAdd(&s2, a2);
   }
-  atomicAdd(&s1, a1);
-  atomicAdd(&s2, a2);
   __syncthreads();
   if (threadIdx.x == 0) {
     atomicAdd(&st[h].sum_c, s1);
@@ -1186,7 +1181,9 @@ hipError_t launch_score(int dtype, const ScoreGeom& g, const void* q_rows, const
   hipLaunchKernelGGL(radix_min_above_kernel, dim3(hb, g.hkv), dim3(256), 0, stream, a.obs, N, st);
   hipLaunchKernelGGL(cv_threshold_kernel, dim3(pb), dim3(64), 0, stream, st,
                      hist + (size_t)2 * g.hkv * kRadixBins, N, g.k_pct, g.alpha, g.hkv);
-  const unsigned cb = (unsigned)std::min<int64_t>(1024, (g.n_keys + 255) / 256);
+  // 64 columns per workgroup and step; few enough workgroups that the two
+  // per-head totals are not a hot spot of global atomics
+  const unsigned cb = (unsigned)std::min<int64_t>(256, (g.n_keys + 63) / 64);
   hipLaunchKernelGGL(cv_count_kernel, dim3(cb, g.hkv), dim3(256), 0, stream, a.obs, g.lq, g.n_keys, st);
   hipLaunchKernelGGL(cv_final_kernel, dim3(pb), dim3(64), 0, stream, st, g.n_keys, cv_out, g.hkv);
   return hipGetLastError();
