@@ -101,6 +101,27 @@ def test_decode_device_length_below_plan():
     assert_rows_close(out[0], o_ref, "bf16")
 
 
+def test_decode_device_length_above_plan_and_negative():
+    # L = min(lens, planned max_len): a device length above the plan is
+    # clamped to it, a negative one reads as an empty view
+    rng = np.random.default_rng(16)
+    B, hq, hkv = 1, 12, 3
+    held = [5000, 700, 300]               # rows each view holds
+    plan_len = [1000, 700, 300]
+    actual = [5000, 650, -3]
+    views = _views(rng, held, "bf16")
+    q_st = synth.f32_to_bf16_bits(rng.standard_normal((B, hq, 128), dtype=np.float32))
+    say("decode device lengths above the plan and negative")
+    lens_dev = torch.tensor(actual, dtype=torch.int64, device=DEV)
+    out, lse, _, _ = run_decode(views, B, hq, hkv, "bf16", q_st, split=256, lens_dev=lens_dev, max_len=plan_len)
+    used = [1000, 650]
+    vv = [(f64(views[h][0])[:used[h]], f64(views[h][1])[:used[h]]) for h in range(2)]
+    o_ref, l_ref = O.decode_gqa(f64(q_st)[0][:8], vv)
+    assert_rows_close(out[0][:8], o_ref, "bf16")
+    np.testing.assert_allclose(lse[0][:8], l_ref, atol=1e-4, rtol=0)
+    assert (out[0][8:] == 0).all() and (lse[0][8:] == -np.inf).all()
+
+
 @pytest.mark.parametrize("G", [1, 2, 4, 8])
 def test_decode_group_sizes(G):
     rng = np.random.default_rng(20 + G)
