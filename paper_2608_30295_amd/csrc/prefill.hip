@@ -728,6 +728,8 @@ struct CvState {                 // per KV head, in the workspace
   unsigned long long cnt_lt;     // entries strictly below x_(lo)
   double phi;
   unsigned long long sum_c, sum_c2;
+  unsigned long long c0;         // entries in x_(lo)'s top-digit bin (known after the first pass)
+  uint32_t n_cand;               // those entries, gathered by the second pass when they fit
 };
 
 constexpr int kRadixBins = 2048;   // digits: bits [31:21], [20:10] (11 bits), [9:0] (10 bits)
@@ -753,6 +755,8 @@ __global__ void cv_init_kernel(CvState* st, uint32_t* hist, int64_t N, double k_
     s.phi = 0.0;
     s.sum_c = 0;
     s.sum_c2 = 0;
+    s.c0 = 0;
+    s.n_cand = 0;
   }
 }
 
@@ -761,9 +765,7 @@ __global__ void cv_init_kernel(CvState* st, uint32_t* hist, int64_t N, double k_
 // probabilities of A crowd into a few digits, so each wave first counts the
 // lanes that share its leading lane's digit with one ballot and one atomic;
 // only the other lanes add one by one.  16-byte loads, 4 entries per lane.
-__device__ __forceinline__ void hist_add(uint32_t* s_h, bool valid, uint32_t bin) {
-  const uint64_t act = __builtin_amdgcn_ballot_w64(valid);
-  if (act == 0) return;
+__device__ __forceinline__ void hist_add_act(uint32_t* s_h, uint64_t act, bool valid, uint32_t bin) {
   const int lead = __builtin_ctzll(act);
   const uint32_t lb = (uint32_t)__builtin_amdgcn_readlane((int)bin, lead);
   const uint64_t same = __builtin_amdgcn_ballot_w64(valid && bin == lb);
@@ -771,36 +773,94 @@ __device__ __forceinline__ void hist_add(uint32_t* s_h, bool valid, uint32_t bin
   if (lane == lead) atomicAdd(&s_h[lb], (uint32_t)__builtin_popcountll(same));
   else if (valid && bin != lb) atomicAdd(&s_h[bin], 1u);
 }
+__device__ __forceinline__ void hist_add(uint32_t* s_h, bool valid, uint32_t bin) {
+  const uint64_t act = __builtin_amdgcn_ballot_w64(valid);
+  if (act) hist_add_act(s_h, act, valid, bin);
+}
 
-__global__ void radix_hist_kernel(const float* __restrict__ A, int64_t N, int pass,
-                                  const CvState* __restrict__ st, uint32_t* __restrict__ hist) {
+// The entries of x_(lo)'s top-digit bin (c0 of them, counted by the first
+// pass) are all that the last two digits are resolved over.  When c0 fits the
+// candidate buffer (cap keys per head), the second pass also gathers them, so
+// the third pass and the search for the next key above x_(lo) read the
+// candidates instead of A.  Gathering rides on the histogram's own ballot:
+// a wave with no matching lane skips both.
+constexpr int kGatherWave = 512;     // candidates a wave stages in LDS before writing them out
+
+__global__ __launch_bounds__(256) void radix_hist_kernel(const float* __restrict__ A, int64_t N, int pass,
+                                                         CvState* st, uint32_t* __restrict__ hist,
+                                                         uint32_t* __restrict__ cand, uint32_t cap) {
   __shared__ uint32_t s_h[kRadixBins];
+  __shared__ uint32_t s_buf[4][kGatherWave];
+  __shared__ uint32_t s_wc[4];
+  __shared__ uint32_t s_base;
   const int h = blockIdx.y;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const bool use_cand = st[h].c0 <= (unsigned long long)cap;   // uniform over the launch for head h
+  const bool gather = pass == 1 && use_cand;
   for (int i = threadIdx.x; i < kRadixBins; i += blockDim.x) s_h[i] = 0;
   __syncthreads();
   const uint32_t pm = digit_mask_above(pass), pv = st[h].prefix & pm;
   const int shift = digit_shift(pass);
   const uint32_t dmask = pass == 2 ? 0x3FFu : 0x7FFu;
-  const float* Ah = A + (size_t)h * N;
-  const int64_t n4 = (N & 3) == 0 && ((reinterpret_cast<uintptr_t>(Ah) & 15) == 0) ? N / 4 : 0;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (int64_t)gridDim.x * blockDim.x) {
-    const float4 v = *reinterpret_cast<const float4*>(Ah + 4 * i);
-    const float f[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const uint32_t key = ord_key(f[e]);
+  uint32_t* ch = cand + (size_t)h * cap;
+  // a wave-uniform count of the wave's candidates (from the ballots, no
+  // atomics in the loop); a wave's stage holds kGatherWave, any beyond go
+  // straight to the buffer
+  uint32_t wcnt = 0;
+  auto visit = [&](bool match, uint32_t key) {
+    const uint64_t act = __builtin_amdgcn_ballot_w64(match);
+    if (act == 0) return;
+    hist_add_act(s_h, act, match, (key >> shift) & dmask);
+    if (gather) {
+      if (match) {
+        const uint32_t off = wcnt + (uint32_t)__builtin_popcountll(act & __lanemask_lt());
+        if (off < (uint32_t)kGatherWave) s_buf[wave][off] = key;
+        else ch[atomicAdd(&st[h].n_cand, 1u)] = key;
+      }
+      wcnt += (uint32_t)__builtin_popcountll(act);
+    }
+  };
+  if (pass == 2 && use_cand) {
+    const int64_t nc = st[h].n_cand;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nc;
+         i += (int64_t)gridDim.x * blockDim.x) {
+      const uint32_t key = ch[i];
       hist_add(s_h, (key & pm) == pv, (key >> shift) & dmask);
     }
+  } else {
+    const float* Ah = A + (size_t)h * N;
+    const int64_t n4 = (N & 3) == 0 && ((reinterpret_cast<uintptr_t>(Ah) & 15) == 0) ? N / 4 : 0;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4;
+         i += (int64_t)gridDim.x * blockDim.x) {
+      const float4 v = *reinterpret_cast<const float4*>(Ah + 4 * i);
+      const float f[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t key = ord_key(f[e]);
+        visit((key & pm) == pv, key);
+      }
+    }
+    // entries not covered by the 16-byte loads (N not a multiple of 4, or an unaligned head)
+    for (int64_t i = 4 * n4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N;
+         i += (int64_t)gridDim.x * blockDim.x) {
+      const uint32_t key = ord_key(Ah[i]);
+      visit((key & pm) == pv, key);
+    }
   }
-  // entries not covered by the 16-byte loads (N not a multiple of 4, or an unaligned head)
-  for (int64_t i = 4 * n4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const uint32_t key = ord_key(Ah[i]);
-    if ((key & pm) == pv) atomicAdd(&s_h[(key >> shift) & dmask], 1u);
-  }
+  if (gather && lane == 0) s_wc[wave] = min(wcnt, (uint32_t)kGatherWave);
   __syncthreads();
   for (int i = threadIdx.x; i < kRadixBins; i += blockDim.x)
     if (s_h[i]) atomicAdd(&hist[(size_t)h * kRadixBins + i], s_h[i]);
+  if (gather) {
+    if (threadIdx.x == 0) {
+      const uint32_t tot = s_wc[0] + s_wc[1] + s_wc[2] + s_wc[3];
+      s_base = tot ? atomicAdd(&st[h].n_cand, tot) : 0u;
+    }
+    __syncthreads();
+    uint32_t dst = s_base;
+    for (int w = 0; w < wave; ++w) dst += s_wc[w];
+    for (uint32_t i = lane; i < s_wc[wave]; i += 64) ch[dst + i] = s_buf[wave][i];
+  }
 }
 
 // Pick the digit that holds the target rank: one 256-thread workgroup per
@@ -815,6 +875,7 @@ __global__ __launch_bounds__(kPickThreads) void radix_pick_kernel(const uint32_t
   __shared__ int64_t s_tot[kPickThreads / 64];
   __shared__ int s_bin;
   __shared__ int64_t s_cum;
+  __shared__ uint32_t s_bcnt;
   __shared__ int s_next;
   const int h = blockIdx.x;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
@@ -851,6 +912,7 @@ __global__ __launch_bounds__(kPickThreads) void radix_pick_kernel(const uint32_t
     }
     s_bin = t * BPT + i;
     s_cum = cum;
+    s_bcnt = c[i];
   }
   __syncthreads();
   if (s_bin < 0) {            // rank beyond the counts (not reached with consistent counts): last bin
@@ -859,6 +921,7 @@ __global__ __launch_bounds__(kPickThreads) void radix_pick_kernel(const uint32_t
       for (int b = 0; b < nb - 1; ++b) cum += hh[b];
       s_bin = nb - 1;
       s_cum = cum;
+      s_bcnt = hh[nb - 1];
     }
     __syncthreads();
   }
@@ -877,6 +940,7 @@ __global__ __launch_bounds__(kPickThreads) void radix_pick_kernel(const uint32_t
     st[h].prefix = prefix;
     st[h].remaining = (int32_t)(rem - s_cum);
     st[h].cnt_lt += (unsigned long long)s_cum;
+    if (pass == 0) st[h].c0 = s_bcnt;
     if (pass == 2) {
       if (s_next != 0x7FFFFFFF) st[h].min_above_key = (prefix & ~0x3FFu) | (uint32_t)s_next;
       else st[h].need_scan = 1;
@@ -885,31 +949,47 @@ __global__ __launch_bounds__(kPickThreads) void radix_pick_kernel(const uint32_t
 }
 
 // Smallest ordered key strictly above x_(lo) (needed when x_(lo + 1) differs).
-__global__ void radix_min_above_kernel(const float* __restrict__ A, int64_t N, CvState* st) {
+// from_cand: over the gathered candidates (x_(lo)'s top-digit bin), when they
+// were gathered; otherwise, and when no candidate lies above x_(lo) (then the
+// key sits in a higher top-digit bin), over A.
+__global__ __launch_bounds__(256) void radix_min_above_kernel(const float* __restrict__ A, int64_t N, CvState* st,
+                                                              const uint32_t* __restrict__ cand, uint32_t cap,
+                                                              int from_cand) {
   __shared__ uint32_t s_min;
   const int h = blockIdx.y;
   if (!st[h].need_scan) return;       // found in the last radix histogram
+  const bool use_cand = st[h].c0 <= (unsigned long long)cap;
+  if (from_cand ? !use_cand : (use_cand && st[h].min_above_key != 0xFFFFFFFFu)) return;
   if (threadIdx.x == 0) s_min = 0xFFFFFFFFu;
   __syncthreads();
   const uint32_t x = st[h].prefix;
-  const float* Ah = A + (size_t)h * N;
   uint32_t mn = 0xFFFFFFFFu;
-  const int64_t n4 = (N & 3) == 0 && ((reinterpret_cast<uintptr_t>(Ah) & 15) == 0) ? N / 4 : 0;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (int64_t)gridDim.x * blockDim.x) {
-    const float4 v = *reinterpret_cast<const float4*>(Ah + 4 * i);
-    const uint32_t k4[4] = {ord_key(v.x), ord_key(v.y), ord_key(v.z), ord_key(v.w)};
+  if (from_cand) {
+    const uint32_t* ch = cand + (size_t)h * cap;
+    const int64_t nc = st[h].n_cand;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nc; i += (int64_t)gridDim.x * blockDim.x) {
+      const uint32_t key = ch[i];
+      if (key > x) mn = min(mn, key);
+    }
+  } else {
+    const float* Ah = A + (size_t)h * N;
+    const int64_t n4 = (N & 3) == 0 && ((reinterpret_cast<uintptr_t>(Ah) & 15) == 0) ? N / 4 : 0;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (int64_t)gridDim.x * blockDim.x) {
+      const float4 v = *reinterpret_cast<const float4*>(Ah + 4 * i);
+      const uint32_t k4[4] = {ord_key(v.x), ord_key(v.y), ord_key(v.z), ord_key(v.w)};
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
-      if (k4[e] > x) mn = min(mn, k4[e]);
-  }
-  for (int64_t i = 4 * n4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const uint32_t key = ord_key(Ah[i]);
-    if (key > x) mn = min(mn, key);
+      for (int e = 0; e < 4; ++e)
+        if (k4[e] > x) mn = min(mn, k4[e]);
+    }
+    for (int64_t i = 4 * n4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N;
+         i += (int64_t)gridDim.x * blockDim.x) {
+      const uint32_t key = ord_key(Ah[i]);
+      if (key > x) mn = min(mn, key);
+    }
   }
   atomicMin(&s_min, mn);
   __syncthreads();
-  if (threadIdx.x == 0) atomicMin(&st[h].min_above_key, s_min);
+  if (threadIdx.x == 0 && s_min != 0xFFFFFFFFu) atomicMin(&st[h].min_above_key, s_min);
 }
 
 // Phi = alpha * (x_(lo) + frac * (x_(lo+1) - x_(lo))) in fp64 (Eq. 2).
@@ -1125,8 +1205,14 @@ hipError_t launch_compact(int dtype, const void* k, const void* v, int hkv, int6
 }
 
 struct ScoreLayout {
-  size_t rowpart, rowoff, obs, hist, state, total;
+  size_t rowpart, rowoff, obs, hist, cand, state, total;
 };
+// Candidate keys per head: an eighth of the observation matrix (the top-digit
+// bin of a high quantile holds far fewer; larger bins take the path over A).
+static uint32_t cand_cap(const ScoreGeom& g) {
+  const int64_t N = (int64_t)g.lq * g.n_keys;
+  return (uint32_t)std::max<int64_t>(4096, (N + 7) / 8);
+}
 static ScoreLayout score_layout(const ScoreGeom& g) {
   ScoreLayout L{};
   const int rp = rows_pad(g.G * g.lq);
@@ -1135,6 +1221,7 @@ static ScoreLayout score_layout(const ScoreGeom& g) {
   L.rowoff = o; o += align256((size_t)g.hkv * rp * sizeof(float));
   L.obs = o; o += align256((size_t)g.hkv * g.lq * g.n_keys * sizeof(float));
   L.hist = o; o += align256((size_t)3 * g.hkv * kRadixBins * sizeof(uint32_t));
+  L.cand = o; o += align256((size_t)g.hkv * cand_cap(g) * sizeof(uint32_t));
   L.state = o; o += align256((size_t)g.hkv * sizeof(CvState));
   L.total = o;
   return L;
@@ -1173,12 +1260,15 @@ hipError_t launch_score(int dtype, const ScoreGeom& g, const void* q_rows, const
   hipLaunchKernelGGL(cv_init_kernel, dim3(24), dim3(256), 0, stream, st, hist, N, g.k_pct, g.hkv);
   const unsigned hb = (unsigned)std::min<int64_t>(512, (N + 1023) / 1024);
   const unsigned pb = (unsigned)((g.hkv + 63) / 64);
+  uint32_t* cand = reinterpret_cast<uint32_t*>(w + L.cand);
+  const uint32_t cap = cand_cap(g);
   for (int pass = 0; pass < 3; ++pass) {
     uint32_t* hp = hist + (size_t)pass * g.hkv * kRadixBins;
-    hipLaunchKernelGGL(radix_hist_kernel, dim3(hb, g.hkv), dim3(256), 0, stream, a.obs, N, pass, st, hp);
+    hipLaunchKernelGGL(radix_hist_kernel, dim3(hb, g.hkv), dim3(256), 0, stream, a.obs, N, pass, st, hp, cand, cap);
     hipLaunchKernelGGL(radix_pick_kernel, dim3(g.hkv), dim3(kPickThreads), 0, stream, hp, pass, st, g.hkv);
   }
-  hipLaunchKernelGGL(radix_min_above_kernel, dim3(hb, g.hkv), dim3(256), 0, stream, a.obs, N, st);
+  hipLaunchKernelGGL(radix_min_above_kernel, dim3(hb, g.hkv), dim3(256), 0, stream, a.obs, N, st, cand, cap, 1);
+  hipLaunchKernelGGL(radix_min_above_kernel, dim3(hb, g.hkv), dim3(256), 0, stream, a.obs, N, st, cand, cap, 0);
   hipLaunchKernelGGL(cv_threshold_kernel, dim3(pb), dim3(64), 0, stream, st,
                      hist + (size_t)2 * g.hkv * kRadixBins, N, g.k_pct, g.alpha, g.hkv);
   // 64 columns per workgroup and step; few enough workgroups that the two

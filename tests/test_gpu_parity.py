@@ -327,6 +327,26 @@ def test_score_heads(name, kw, causal):
     np.testing.assert_allclose(cv, ref, rtol=1e-4, atol=1e-6)
 
 
+def test_score_heads_crowded_and_spread_quantile_bins():
+    # head 0 has zero keys: every entry of its observation matrix is equal, so
+    # the quantile's top-digit bin holds all of them (more than the candidate
+    # buffer: the passes run over A); head 1 is spread (candidates gathered)
+    wl = _small("ctx32k_bf16", n=3000, hq=8, hkv=2)
+    seq = synth.make_sequence(wl)
+    k = seq.k.copy()
+    k[0] = 0
+    say("score_heads with a crowded and a spread head")
+    cv = ck.score_heads(to_dev(seq.q_cv), to_dev(k), q_pos0=seq.q_cv_pos0, l_init=wl.l_init,
+                        l_rec=wl.l_rec, k_pct=wl.k_pct, alpha=wl.alpha, causal=False)
+    torch.cuda.synchronize()
+    cv = cv.cpu().numpy().astype(np.float64)
+    ref = O.score_heads(f64(seq.q_cv), seq.q_cv_pos0, f64(k), wl.l_init, wl.l_rec, wl.k_pct, wl.alpha,
+                        causal=False)
+    say("  gpu", np.round(cv, 6), "\n  ref", np.round(ref, 6))
+    assert ref[0] == 0.0
+    np.testing.assert_allclose(cv, ref, rtol=1e-4, atol=1e-6)
+
+
 def test_score_heads_toy_through_abi():
     # the hand-worked 2 x 4 toy (cv = sqrt(3)) driven through the GPU path
     A = np.array([[0.7, 0.1, 0.1, 0.1], [0.6, 0.2, 0.1, 0.1]])
