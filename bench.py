@@ -196,6 +196,62 @@ def time_decode_shape(torch, ck, wl, dev, stream, steps):
     return res
 
 
+def time_prefill_shape(torch, ck, wl, dev, stream):
+    """CV scoring, selection and compaction once per request at a workload's
+    shapes with K, V and the query rows drawn on the GPU (normal values; the
+    work does not depend on them): CV over all KV heads with the workload's
+    observation rows, selection and compaction over the consistent heads
+    (Eq. 5's count for the workload's r)."""
+    import synth
+    hq, hkv, d, n = wl.hq, wl.hkv, wl.d, wl.n
+    G = hq // hkv
+    n_cons = hkv - 1 - int(math.floor((hkv - 1) * wl.r))
+    heads = list(range(1, 1 + n_cons))
+    k = torch.empty((hkv, n, d), dtype=torch.bfloat16, device=dev).normal_()
+    v = torch.empty_like(k).normal_()
+    q_obs = torch.empty((hq, wl.l_obs, d), dtype=torch.bfloat16, device=dev).normal_()
+    lq = wl.cv_calib_rows or wl.l_obs
+    q_cv = torch.empty((hq, lq, d), dtype=torch.bfloat16, device=dev).normal_()
+    q_pos0 = n if wl.cv_calib_rows else n - wl.l_obs      # decode-time calibration rows sit after the prompt
+    b = wl.chunk_budget
+    cv_ws = ck.workspace(ck.score_heads_workspace(hq, hkv, lq, n, wl.l_init, wl.l_rec), dev)
+    sel_ws = ck.workspace(ck.select_workspace(hq, hkv, wl.l_obs, n, wl.cs, len(heads)), dev)
+    lens = torch.zeros(hkv, dtype=torch.int64, device=dev)
+    cap = b * wl.cs + wl.l_obs
+    k_c = torch.empty((len(heads), cap, d), dtype=k.dtype, device=dev)
+    v_c = torch.empty_like(k_c)
+
+    def time_it(fn, reps):
+        fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        e1.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / reps
+    t_cv = time_it(lambda: ck.score_heads(q_cv, k, q_pos0=q_pos0, l_init=wl.l_init, l_rec=wl.l_rec,
+                                          k_pct=wl.k_pct, alpha=wl.alpha, ws=cv_ws), 2)
+    idx = ck.select_critical(q_obs, k, heads, wl.cs, b, ws=sel_ws)
+    t_sel = time_it(lambda: ck.select_critical(q_obs, k, heads, wl.cs, b, ws=sel_ws), 3)
+    t_cmp = time_it(lambda: ck.compact_kv(k, v, heads, idx, wl.cs, wl.l_obs, lens, out=(k_c, v_c)), 3)
+    n_keys = n - wl.l_obs
+    esz = 2
+    sel_flops = 2.0 * len(heads) * G * wl.l_obs * n_keys * d
+    sel_bytes = len(heads) * n_keys * d * esz + 2 * len(heads) * cap * d * esz * 2
+    roof = max(sel_flops / (BF16_MFMA_PEAK_TFLOPS * 1e12), sel_bytes / (HBM_PEAK_GBS * 1e9)) * 1e6
+    res = {"workload": wl.name, "consistent_heads": n_cons, "cv_rows": lq, "score_heads_us": round(t_cv, 1),
+           "select_critical_us": round(t_sel, 1), "compact_kv_us": round(t_cmp, 1),
+           "select_roofline_us": round(roof, 1),
+           "select_plus_compact_vs_roofline": round((t_sel + t_cmp) / roof, 3),
+           "data": "K, V and query rows drawn on the GPU"}
+    log(f"[bench] {wl.name} prefill: CV {t_cv:.1f} us, selection {t_sel:.1f} us + compaction {t_cmp:.1f} us "
+        f"(roofline {roof:.1f} us)")
+    del k, v, q_obs, q_cv, cv_ws, sel_ws, k_c, v_c
+    torch.cuda.empty_cache()
+    return res
+
+
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
@@ -610,10 +666,11 @@ def main():
             next_res["query_aware_retrieval"] = time_retrieval()
 
     # ---------------- decode at the other workloads' shapes ----------------
-    other = None
+    other = other_prefill = None
     if not args.no_workloads:
         other = [time_decode_shape(torch, ck, synth.WORKLOADS[name], dev, stream, args.steps)
                  for name in ("ctx32k_bf16", "batch16_ragged_bf16", "ctx1m_bf16")]
+        other_prefill = [time_prefill_shape(torch, ck, synth.WORKLOADS["ctx1m_bf16"], dev, stream)]
 
     # ---------------- CPU oracle on a bounded sample ----------------
     cpu = None
@@ -690,6 +747,7 @@ def main():
         "cpu_baseline": cpu,
         "next": next_res,
         "other_workloads": other,
+        "other_prefill": other_prefill,
     }
     print(json.dumps(res), flush=True)
 
