@@ -175,7 +175,8 @@ int catekv_compact_kv(int dtype, const void* k, const void* v, int hkv, int64_t 
 
 /* Workspace bytes for a decode plan over max_len_host [batch][hkv].
  * split_tokens is the number of tokens each decode workgroup streams; <= 0
- * spreads all tokens over the workgroups the device holds at once. */
+ * spreads all tokens over the workgroups the device holds at once (one per
+ * compute unit when all views together hold fewer than 2^18 rows). */
 size_t catekv_decode_workspace(const int64_t* max_len_host, int batch, int hq, int hkv,
                                int split_tokens);
 
@@ -183,7 +184,8 @@ size_t catekv_decode_workspace(const int64_t* max_len_host, int batch, int hq, i
  * max_len_host [batch][hkv] (full length for adaptive heads, b cs + l_obs for
  * consistent heads), writes it into ws and fills *plan.  All views are laid
  * end to end and cut into equal shares, one per decode workgroup (by default
- * the number of workgroups the current device runs at once), so long and
+ * the number of workgroups the current device runs at once, or one per
+ * compute unit below 2^18 rows in all), so long and
  * short views balance across compute units.  Blocks until the upload has
  * completed, so max_len_host may be reused on return.  The plan and ws serve
  * every later catekv_decode_attn call with the same shapes; calls sharing a

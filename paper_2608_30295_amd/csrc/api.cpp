@@ -86,12 +86,20 @@ struct PlanLayout {
 
 size_t a256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-int device_workers(int G) {
+// Decode workgroups of a default plan: as many as the device holds at once,
+// or one per compute unit when the step is small (fewer than kFewTokens rows
+// in all views; 128 MB of bf16 K and V): a step that short is dominated by its
+// fixed costs (start-up chain, partials, merge), which one workgroup per CU
+// halves, while a longer step streams slightly faster with two.
+constexpr int64_t kFewTokens = 1 << 18;
+int device_workers(int G, const int64_t* max_len, int n_views) {
   int dev = 0, n_cu = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n_cu < 1)
     n_cu = 256;
-  return n_cu * catekv::decode_blocks_per_cu(CATEKV_BF16, G);
+  int64_t total = 0;
+  for (int v = 0; v < n_views; ++v) total += max_len[v];
+  return total < kFewTokens ? n_cu : n_cu * catekv::decode_blocks_per_cu(CATEKV_BF16, G);
 }
 
 // Cuts the views (in index order, laid end to end in units of
@@ -321,7 +329,7 @@ size_t catekv_decode_workspace(const int64_t* max_len_host, int batch, int hq, i
   const int nv = batch * hkv;
   for (int i = 0; i < nv; ++i)
     if (max_len_host[i] < 0 || max_len_host[i] > INT32_MAX) return 0;
-  return plan_layout(max_len_host, nv, hq / hkv, split_tokens, device_workers(hq / hkv)).total;
+  return plan_layout(max_len_host, nv, hq / hkv, split_tokens, device_workers(hq / hkv, max_len_host, nv)).total;
 }
 
 int catekv_decode_plan(const int64_t* max_len_host, int batch, int hq, int hkv, int split_tokens,
@@ -335,7 +343,7 @@ int catekv_decode_plan(const int64_t* max_len_host, int batch, int hq, int hkv, 
   if (rc) return rc;
   if (!ws) return fail(CATEKV_ERR_WORKSPACE, "workspace pointer is null");
   const int G = hq / hkv;
-  const PlanLayout P = plan_layout(max_len_host, nv, G, split_tokens, device_workers(G));
+  const PlanLayout P = plan_layout(max_len_host, nv, G, split_tokens, device_workers(G, max_len_host, nv));
   rc = check_ws(ws, ws_bytes, P.total);
   if (rc) return rc;
 
