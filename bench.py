@@ -743,6 +743,8 @@ def main():
             "select_roofline_us": round(sel_roof_us, 1),
             "select_plus_compact_vs_roofline": round((t_sel + t_cmp) / sel_roof_us, 3),
             "select_tflops": round(sel_flops / (t_sel * 1e-6) / 1e12, 1),
+            # the two Q K^T passes the exact method runs, against the dense bf16 MFMA peak
+            "select_two_pass_mfma_frac": round(2 * sel_flops / (t_sel * 1e-6) / (BF16_MFMA_PEAK_TFLOPS * 1e12), 4),
         },
         "cpu_baseline": cpu,
         "next": next_res,
