@@ -451,7 +451,7 @@ int catekv_page_bounds(int dtype, const void* k, int hkv, int64_t n, int d, int 
 
 size_t catekv_retrieve_workspace(int n_sel, int64_t n_pages) {
   if (n_sel < 1 || n_pages < 1) return 0;
-  return ((size_t)n_sel * (size_t)n_pages * sizeof(float) + 255) / 256 * 256;
+  return a256((size_t)n_sel * (size_t)n_pages * sizeof(float)) + a256(catekv::topk_workspace_bytes(n_sel, n_pages));
 }
 
 int catekv_retrieve_pages(int dtype, const void* q, const void* kmin, const void* kmax, int hq, int hkv,
@@ -471,7 +471,8 @@ int catekv_retrieve_pages(int dtype, const void* q, const void* kmin, const void
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   float* scores = reinterpret_cast<float*>(ws);
   hipError_t e = catekv::launch_page_scores(dtype, hq / hkv, q, kmin, kmax, n_pages, heads_host, n_sel, scores, s);
-  if (e == hipSuccess) e = catekv::launch_topk(scores, n_sel, n_pages, n_keep, idx_out, s);
+  char* topk_ws = reinterpret_cast<char*>(ws) + a256((size_t)n_sel * (size_t)n_pages * sizeof(float));
+  if (e == hipSuccess) e = catekv::launch_topk(scores, n_sel, n_pages, n_keep, idx_out, topk_ws, s);
   if (e != hipSuccess) return hip_fail(e, "retrieve_pages launch");
   return ok();
 }

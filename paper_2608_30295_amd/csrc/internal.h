@@ -87,7 +87,12 @@ hipError_t launch_compact(int dtype, const void* k, const void* v, int hkv, int6
 
 // Indices of the b largest of each row of S [n_rows][n] (ties to the lower
 // index), ascending, -1 padded to b.
-hipError_t launch_topk(const float* S, int n_rows, int64_t n, int b, int32_t* idx_out, hipStream_t stream);
+// Indices of the min(b, n) largest of each row of S [n_rows][n] (ties to the
+// lower index), ascending, -1 padded to b.  ws: topk_workspace_bytes() bytes
+// (rows longer than 32768 scores are reduced slice by slice through it).
+size_t topk_workspace_bytes(int n_rows, int64_t n);
+hipError_t launch_topk(const float* S, int n_rows, int64_t n, int b, int32_t* idx_out, void* ws,
+                       hipStream_t stream);
 
 // ---- query-aware retrieval in adaptive heads (page bounds and scores) -----
 hipError_t launch_page_bounds(int dtype, const void* k, int64_t n, int cs, const int32_t* heads, int n_sel,

@@ -542,32 +542,79 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(const float* __restr
 // of the target rank with a suffix scan, so a pass costs two barriers.  The
 // positions of the selected entries come from per-row ballots and one
 // exchange of the per-wave counts.
-template <int PER>
-__global__ __launch_bounds__(kTopkThreads) void topk_wave_kernel(const float* __restrict__ S, int64_t n_chunks,
-                                                                 int k, int b, int32_t* __restrict__ idx_out) {
+//
+// Three uses (MODE): a whole row of scores; one slice of a row (longer rows
+// are cut into kTopkSlice-score slices whose own k best, in ascending order,
+// go to a candidate list); a row's candidate list (scores looked up through
+// the list, -1 entries never chosen, output mapped back through it).  The k
+// best of a row are always among its slices' k best (an entry outranked by k
+// entries of its own slice is outranked by k entries of the row; ties go to
+// the lower index in both), and the candidate list is ascending, so the two
+// stages reproduce the one-stage result.
+enum TopkMode { kTopkRow = 0, kTopkSliceMode = 1, kTopkList = 2 };
+constexpr int64_t kTopkSlice = 16 * kTopkThreads;   // scores per slice
+
+struct TopkArgs {
+  const float* S;          // scores [rows][n]
+  int64_t n;
+  const int32_t* list;     // kTopkList: candidate indices [rows][list_len], -1 = none
+  int64_t list_len;
+  int k, b;                // select k; kTopkRow / kTopkList write b entries per row (-1 padded)
+  int32_t* out;            // kTopkSliceMode: [rows][n_slices][k]; otherwise [rows][b]
+};
+
+template <int PER, int MODE>
+__global__ __launch_bounds__(kTopkThreads) void topk_wave_kernel(TopkArgs a) {
   constexpr int NW = kTopkThreads / 64;
   constexpr int NCOPY = 16;
   constexpr int RS = 260;                  // words per copy: 256 bins, rows 16-byte aligned
+  static_assert(PER <= 32, "validity is a 32-bit mask per lane");
   __shared__ __attribute__((aligned(16))) int s_h[2][NCOPY][RS];
   __shared__ uint32_t s_and[NW], s_or[NW];
   __shared__ int s_gt[NW], s_eq[NW];
   __shared__ uint32_t s_prefix;
   __shared__ int s_remaining;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const float* Ss = S + (size_t)blockIdx.x * n_chunks;
-  const int64_t base = (int64_t)wave * PER * 64 + lane;       // chunk of row 0; row i adds 64 i
-  const int64_t rem = n_chunks - base;
-  const int nv = rem <= 0 ? 0 : (int)min<int64_t>(PER, (rem + 63) / 64);   // rows holding a chunk
+  const int row = MODE == kTopkSliceMode ? blockIdx.y : blockIdx.x;
+  const float* Ss = a.S + (size_t)row * a.n;
+  int64_t start = 0, len = a.n;
+  int k = a.k, b = a.b;
+  int32_t* out = a.out + (size_t)row * a.b;
+  const int32_t* lst = nullptr;
+  if (MODE == kTopkSliceMode) {
+    start = (int64_t)blockIdx.x * kTopkSlice;
+    len = min(kTopkSlice, a.n - start);
+    k = (int)min((int64_t)a.k, len);
+    b = a.k;
+    out = a.out + ((size_t)row * gridDim.x + blockIdx.x) * a.k;
+  } else if (MODE == kTopkList) {
+    len = a.list_len;
+    lst = a.list + (size_t)row * a.list_len;
+  }
+  const int64_t base = (int64_t)wave * PER * 64 + lane;       // entry of row 0; row i adds 64 i
   uint32_t key[PER];
+  uint32_t vmask = 0;                                          // bit i: row i holds an entry
+  const int64_t rem = len - base;
+  const int nv = rem <= 0 ? 0 : (int)min<int64_t>(PER, (rem + 63) / 64);
 #pragma unroll
-  for (int i = 0; i < PER; ++i) key[i] = i < nv ? ord_key(Ss[base + 64 * i]) : 0u;
+  for (int i = 0; i < PER; ++i) {
+    if (MODE == kTopkList) {
+      const int32_t j = i < nv ? lst[base + 64 * i] : -1;
+      key[i] = j >= 0 ? ord_key(Ss[j]) : 0u;
+      vmask |= (j >= 0 ? 1u : 0u) << i;
+    } else {
+      key[i] = i < nv ? ord_key(Ss[start + base + 64 * i]) : 0u;
+      vmask |= (i < nv ? 1u : 0u) << i;
+    }
+  }
+  auto valid = [&](int i) { return (vmask >> i) & 1u; };
 
   // bits shared by every key: a digit made only of such bits puts all keys in
   // one bin, so its pass is skipped (chunk scores share sign and most exponent bits)
   uint32_t kand = 0xFFFFFFFFu, kor = 0u;
 #pragma unroll
   for (int i = 0; i < PER; ++i)
-    if (i < nv) { kand &= key[i]; kor |= key[i]; }
+    if (valid(i)) { kand &= key[i]; kor |= key[i]; }
 #pragma unroll
   for (int off = 1; off < 64; off <<= 1) {
     kand &= (uint32_t)__shfl_xor((int)kand, off);
@@ -596,7 +643,7 @@ __global__ __launch_bounds__(kTopkThreads) void topk_wave_kernel(const float* __
     const int cp = lane & (NCOPY - 1);
 #pragma unroll
     for (int i = 0; i < PER; ++i)
-      if (i < nv && (key[i] & mask) == prefix) atomicAdd(&s_h[cur][cp][(key[i] >> shift) & 255u], 1);
+      if (valid(i) && (key[i] & mask) == prefix) atomicAdd(&s_h[cur][cp][(key[i] >> shift) & 255u], 1);
     __syncthreads();
     if (wave == 0) {
       // lane l holds bins 4 l .. 4 l + 3; suffix sums over the lanes count the bins above
@@ -637,7 +684,7 @@ __global__ __launch_bounds__(kTopkThreads) void topk_wave_kernel(const float* __
   int n_gt = 0, n_eq = 0;
 #pragma unroll
   for (int i = 0; i < PER; ++i)
-    if (i < nv) { n_gt += key[i] > tau; n_eq += key[i] == tau; }
+    if (valid(i)) { n_gt += key[i] > tau; n_eq += key[i] == tau; }
 #pragma unroll
   for (int off = 1; off < 64; off <<= 1) {
     n_gt += __shfl_xor(n_gt, off);
@@ -651,17 +698,19 @@ __global__ __launch_bounds__(kTopkThreads) void topk_wave_kernel(const float* __
     pos += s_gt[w] + min(max(remaining - eqr, 0), e);
     eqr += e;
   }
-  int32_t* out = idx_out + (size_t)blockIdx.x * b;
   const uint64_t below = __lanemask_lt();
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
-    const bool v = i < nv;
+    const bool v = valid(i);
     const bool gt = v && key[i] > tau, eq = v && key[i] == tau;
     const uint64_t meq = __ballot(eq);
     const bool take = gt || (eq && eqr + __popcll(meq & below) < remaining);
     const uint64_t mt = __ballot(take);
     const int p = pos + __popcll(mt & below);
-    if (take && p < k) out[p] = (int32_t)(base + 64 * i);
+    if (take && p < k) {
+      const int64_t e = base + 64 * i;
+      out[p] = MODE == kTopkList ? lst[e] : (int32_t)(start + e);
+    }
     pos += __popcll(mt);
     eqr += __popcll(meq);
   }
@@ -1097,7 +1146,7 @@ int64_t score_block_tokens(int64_t n_keys, int n_heads) {
 }
 
 struct SelectLayout {
-  size_t rowpart, rowoff, colmass, chunks, total;
+  size_t rowpart, rowoff, colmass, chunks, topk, total;
 };
 static SelectLayout select_layout(const SelectGeom& g) {
   SelectLayout L{};
@@ -1107,6 +1156,7 @@ static SelectLayout select_layout(const SelectGeom& g) {
   L.rowoff = o; o += align256((size_t)g.n_sel * rp * sizeof(float));
   L.colmass = o; o += align256((size_t)g.n_sel * g.n_keys * sizeof(float));
   L.chunks = o; o += align256((size_t)g.n_sel * g.n_chunks * sizeof(float));
+  L.topk = o; o += align256(topk_workspace_bytes(g.n_sel, g.n_chunks));
   L.total = o;
   return L;
 }
@@ -1167,17 +1217,40 @@ hipError_t launch_select(int dtype, const SelectGeom& g, const void* q_obs, cons
   if (!a.cs_fused)
     hipLaunchKernelGGL(chunk_max_kernel, dim3((unsigned)((g.n_chunks + 255) / 256), g.n_sel), dim3(256), 0,
                        stream, a.colmass, g.n_keys, g.cs, g.n_chunks, S);
-  return launch_topk(S, g.n_sel, g.n_chunks, g.b, idx_out, stream);
+  return launch_topk(S, g.n_sel, g.n_chunks, g.b, idx_out, w + L.topk, stream);
 }
 
-hipError_t launch_topk(const float* S, int n_rows, int64_t n, int b, int32_t* idx_out, hipStream_t stream) {
+size_t topk_workspace_bytes(int n_rows, int64_t n) {
+  return n > 2 * kTopkSlice ? (size_t)n_rows * 2 * kTopkSlice * sizeof(int32_t) : 0;
+}
+
+hipError_t launch_topk(const float* S, int n_rows, int64_t n, int b, int32_t* idx_out, void* ws,
+                       hipStream_t stream) {
   const int k_eff = (int)(b < n ? b : n);
-  if (n <= 16 * kTopkThreads)
-    hipLaunchKernelGGL(topk_wave_kernel<16>, dim3(n_rows), dim3(kTopkThreads), 0, stream, S, n, k_eff, b, idx_out);
-  else if (n <= 32 * kTopkThreads)
-    hipLaunchKernelGGL(topk_wave_kernel<32>, dim3(n_rows), dim3(kTopkThreads), 0, stream, S, n, k_eff, b, idx_out);
-  else
+  TopkArgs a{};
+  a.S = S; a.n = n; a.k = k_eff; a.b = b; a.out = idx_out;
+  const int64_t n_slices = (n + kTopkSlice - 1) / kTopkSlice;
+  if (n <= kTopkSlice) {
+    hipLaunchKernelGGL((topk_wave_kernel<16, kTopkRow>), dim3(n_rows), dim3(kTopkThreads), 0, stream, a);
+  } else if (n <= 2 * kTopkSlice) {
+    hipLaunchKernelGGL((topk_wave_kernel<32, kTopkRow>), dim3(n_rows), dim3(kTopkThreads), 0, stream, a);
+  } else if (ws && n_slices * k_eff <= 2 * kTopkSlice) {
+    // the k best of every slice, then the k best of those candidates
+    int32_t* cand = reinterpret_cast<int32_t*>(ws);
+    TopkArgs s1 = a;
+    s1.out = cand;
+    hipLaunchKernelGGL((topk_wave_kernel<16, kTopkSliceMode>), dim3((unsigned)n_slices, n_rows),
+                       dim3(kTopkThreads), 0, stream, s1);
+    TopkArgs s2 = a;
+    s2.list = cand;
+    s2.list_len = n_slices * k_eff;
+    if (s2.list_len <= kTopkSlice)
+      hipLaunchKernelGGL((topk_wave_kernel<16, kTopkList>), dim3(n_rows), dim3(kTopkThreads), 0, stream, s2);
+    else
+      hipLaunchKernelGGL((topk_wave_kernel<32, kTopkList>), dim3(n_rows), dim3(kTopkThreads), 0, stream, s2);
+  } else {
     hipLaunchKernelGGL(topk_kernel, dim3(n_rows), dim3(kTopkThreads), 0, stream, S, n, k_eff, b, idx_out);
+  }
   return hipGetLastError();
 }
 

@@ -229,6 +229,7 @@ SEL_CASES = [
     ("ctx32k_bf16", dict(n=64 + 40)),                         # shorter than one tile
     ("ctx128k_bf16", dict(n=9000, hq=16, hkv=2)),            # G = 8 rows of 512
     ("ctx32k_bf16", dict(n=64 + 8 * 17000 + 3, hq=8, hkv=2)), # over 16384 chunk scores per head
+    ("ctx32k_bf16", dict(n=16 + 8 * 40000 + 5, hq=4, hkv=2, l_obs=16)),   # over 32768: slices, then candidates
 ]
 
 
