@@ -240,6 +240,10 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
           acc[j][mt] = x;
         }
       }
+      // from a tile's first softmax block to its end the wave runs at raised
+      // priority (reset before the next tile): measured ~1.5% per pass with
+      // two waves sharing a SIMD
+      __builtin_amdgcn_s_setprio(1);
       if (MASK) {
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
@@ -326,6 +330,7 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
       }
     };
 
+    __builtin_amdgcn_s_setprio(0);
     const bool need_mask = tcol0 + kTileTok > col_end || (CAUSAL && a.key_off + tcol0 + kTileTok - 1 > qpos_min);
     if (need_mask) tile_body(std::true_type{});
     else tile_body(std::false_type{});
