@@ -548,8 +548,8 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(const float* __restr
 // positions of the selected entries come from per-row ballots and one
 // exchange of the per-wave counts.
 //
-// Three uses (MODE): a whole row of scores; one slice of a row (longer rows
-// are cut into kTopkSlice-score slices whose own k best, in ascending order,
+// Three uses (MODE): a whole row of scores; one slice of a row (rows are cut
+// into PER * kTopkThreads-score slices whose own k best, in ascending order,
 // go to a candidate list); a row's candidate list (scores looked up through
 // the list, -1 entries never chosen, output mapped back through it).  The k
 // best of a row are always among its slices' k best (an entry outranked by k
@@ -557,7 +557,8 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(const float* __restr
 // the lower index in both), and the candidate list is ascending, so the two
 // stages reproduce the one-stage result.
 enum TopkMode { kTopkRow = 0, kTopkSliceMode = 1, kTopkList = 2 };
-constexpr int64_t kTopkSlice = 16 * kTopkThreads;   // scores per slice
+constexpr int64_t kTopkSlice = 16 * kTopkThreads;   // scores per slice of long rows
+constexpr int64_t kTopkSmallSlice = 4 * kTopkThreads;   // scores per slice of short rows
 
 struct TopkArgs {
   const float* S;          // scores [rows][n]
@@ -587,8 +588,9 @@ __global__ __launch_bounds__(kTopkThreads) void topk_wave_kernel(TopkArgs a) {
   int32_t* out = a.out + (size_t)row * a.b;
   const int32_t* lst = nullptr;
   if (MODE == kTopkSliceMode) {
-    start = (int64_t)blockIdx.x * kTopkSlice;
-    len = min(kTopkSlice, a.n - start);
+    constexpr int64_t SL = (int64_t)PER * kTopkThreads;
+    start = (int64_t)blockIdx.x * SL;
+    len = min(SL, a.n - start);
     k = (int)min((int64_t)a.k, len);
     b = a.k;
     out = a.out + ((size_t)row * gridDim.x + blockIdx.x) * a.k;
@@ -1226,7 +1228,24 @@ hipError_t launch_select(int dtype, const SelectGeom& g, const void* q_obs, cons
 }
 
 size_t topk_workspace_bytes(int n_rows, int64_t n) {
-  return n > 2 * kTopkSlice ? (size_t)n_rows * 2 * kTopkSlice * sizeof(int32_t) : 0;
+  return n > kTopkSmallSlice ? (size_t)n_rows * 2 * kTopkSlice * sizeof(int32_t) : 0;
+}
+
+// k best of each row's candidate list (ascending indices into the row)
+static void launch_topk_list(const TopkArgs& a, int n_rows, hipStream_t stream) {
+  const int64_t m = a.list_len;
+  if (m <= 1 * kTopkThreads)
+    hipLaunchKernelGGL((topk_wave_kernel<1, kTopkList>), dim3(n_rows), dim3(kTopkThreads), 0, stream, a);
+  else if (m <= 2 * kTopkThreads)
+    hipLaunchKernelGGL((topk_wave_kernel<2, kTopkList>), dim3(n_rows), dim3(kTopkThreads), 0, stream, a);
+  else if (m <= 4 * kTopkThreads)
+    hipLaunchKernelGGL((topk_wave_kernel<4, kTopkList>), dim3(n_rows), dim3(kTopkThreads), 0, stream, a);
+  else if (m <= 8 * kTopkThreads)
+    hipLaunchKernelGGL((topk_wave_kernel<8, kTopkList>), dim3(n_rows), dim3(kTopkThreads), 0, stream, a);
+  else if (m <= 16 * kTopkThreads)
+    hipLaunchKernelGGL((topk_wave_kernel<16, kTopkList>), dim3(n_rows), dim3(kTopkThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL((topk_wave_kernel<32, kTopkList>), dim3(n_rows), dim3(kTopkThreads), 0, stream, a);
 }
 
 hipError_t launch_topk(const float* S, int n_rows, int64_t n, int b, int32_t* idx_out, void* ws,
@@ -1235,7 +1254,24 @@ hipError_t launch_topk(const float* S, int n_rows, int64_t n, int b, int32_t* id
   TopkArgs a{};
   a.S = S; a.n = n; a.k = k_eff; a.b = b; a.out = idx_out;
   const int64_t n_slices = (n + kTopkSlice - 1) / kTopkSlice;
-  if (n <= kTopkSlice) {
+  const int64_t n_small = (n + kTopkSmallSlice - 1) / kTopkSmallSlice;
+  // A row of up to 2 kTopkSlice scores fits one workgroup, but a few such rows
+  // leave most compute units idle: there 4096-score slices run side by side
+  // and a second launch picks among their k best.  Measured: k = 256 of 16384
+  // gains ~1.7 us on three rows, k = 1024 loses ~2.7 us, so k is held to at
+  // most an eighth of a slice.
+  const bool few_short_rows = ws && n > kTopkSmallSlice && n <= 2 * kTopkSlice &&
+                              8 * k_eff <= kTopkSmallSlice && (int64_t)n_rows * n_small <= 2048;
+  if (few_short_rows) {
+    TopkArgs s1 = a;
+    s1.out = reinterpret_cast<int32_t*>(ws);
+    hipLaunchKernelGGL((topk_wave_kernel<4, kTopkSliceMode>), dim3((unsigned)n_small, n_rows),
+                       dim3(kTopkThreads), 0, stream, s1);
+    TopkArgs s2 = a;
+    s2.list = s1.out;
+    s2.list_len = n_small * k_eff;
+    launch_topk_list(s2, n_rows, stream);
+  } else if (n <= kTopkSlice) {
     hipLaunchKernelGGL((topk_wave_kernel<16, kTopkRow>), dim3(n_rows), dim3(kTopkThreads), 0, stream, a);
   } else if (n <= 2 * kTopkSlice) {
     hipLaunchKernelGGL((topk_wave_kernel<32, kTopkRow>), dim3(n_rows), dim3(kTopkThreads), 0, stream, a);
@@ -1249,10 +1285,7 @@ hipError_t launch_topk(const float* S, int n_rows, int64_t n, int b, int32_t* id
     TopkArgs s2 = a;
     s2.list = cand;
     s2.list_len = n_slices * k_eff;
-    if (s2.list_len <= kTopkSlice)
-      hipLaunchKernelGGL((topk_wave_kernel<16, kTopkList>), dim3(n_rows), dim3(kTopkThreads), 0, stream, s2);
-    else
-      hipLaunchKernelGGL((topk_wave_kernel<32, kTopkList>), dim3(n_rows), dim3(kTopkThreads), 0, stream, s2);
+    launch_topk_list(s2, n_rows, stream);
   } else {
     hipLaunchKernelGGL(topk_kernel, dim3(n_rows), dim3(kTopkThreads), 0, stream, S, n, k_eff, b, idx_out);
   }
