@@ -222,14 +222,16 @@ def test_retrieve_more_pages_than_exist():
     assert idx[0].tolist() == list(range(7)) + [-1, -1, -1]
 
 
-@pytest.mark.parametrize("n_pages,n_keep", [(9000, 700), (20000, 700), (40000, 700), (40000, 15000)])
+@pytest.mark.parametrize("n_pages,n_keep", [(9000, 700), (20000, 700), (40000, 700), (40000, 15000),
+                                            (4097, 300), (12289, 1), (16384, 256), (32768, 512)])
 def test_retrieve_exact_ties_lowest_pages_first(n_pages, n_keep):
     """Pages repeat 37 random patterns, so page scores tie exactly in groups
     and the k-th score falls inside a group: the chosen pages must be the
     oracle's (ties to the lower page) on every path of the top-k: one
     workgroup per row up to 16384 and up to 32768 scores, slices then
     candidates beyond that, and the global-memory kernel when the slices'
-    candidates would not fit."""
+    candidates would not fit; for short rows with k <= 512, 4096-score
+    slices then candidates (a one-score last slice at 4097, k = 1, k = 512)."""
     rng = np.random.default_rng(40 + n_pages + n_keep)
     cs, G = 8, 4
     pat = synth.f32_to_bf16_bits(rng.standard_normal((37, cs, 128), dtype=np.float32))
