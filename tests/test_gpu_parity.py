@@ -230,6 +230,8 @@ SEL_CASES = [
     ("ctx128k_bf16", dict(n=9000, hq=16, hkv=2)),            # G = 8 rows of 512
     ("ctx32k_bf16", dict(n=64 + 8 * 17000 + 3, hq=8, hkv=2)), # over 16384 chunk scores per head
     ("ctx32k_bf16", dict(n=16 + 8 * 40000 + 5, hq=4, hkv=2, l_obs=16)),   # over 32768: slices, then candidates
+    ("ctx32k_bf16", dict(n=64 + 8 * 4097, hq=8, hkv=2, budget=4096)),    # 4096-score slices, one-score last slice, k = 512
+    ("ctx32k_bf16", dict(n=64 + 8 * 9000 + 5, hq=8, hkv=2, budget=8)),   # 4096-score slices, k = 1
 ]
 
 
