@@ -261,34 +261,38 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
       }
 
       if (MODE == kRowStats) {
-        // lazy running maximum: move it only when the half-tile maximum exceeds
-        // it by more than 8 in log2 units (terms stay below 2^8)
-        float tmc[MT][4];
+        // lazy running maximum: the pair's terms are taken against the current
+        // maximum, which moves (to the pair's maximum) only when a term would
+        // exceed 2^64 -- on a row's first scores (the maximum starts at
+        // kMInit) or a score 64 log2 units above it; sums stay below 2^82,
+        // and one compare per pair replaces a maximum search
+        float part[MT][4];
         bool upd = false;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            tmc[mt][r] = fmaxf(acc[0][mt][r], acc[1][mt][r]) * a.c;
-            upd |= tmc[mt][r] - st_mc[mt][r] > 8.0f;
+            part[mt][r] = fast_exp2(__builtin_fmaf(acc[0][mt][r], a.c, -st_mc[mt][r])) +
+                          fast_exp2(__builtin_fmaf(acc[1][mt][r], a.c, -st_mc[mt][r]));
+            upd |= !(part[mt][r] <= 0x1p64f);
           }
         if (__builtin_amdgcn_ballot_w64(upd)) {
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
             for (int r = 0; r < 4; ++r)
-              if (tmc[mt][r] - st_mc[mt][r] > 8.0f) {
-                st_l[mt][r] *= fast_exp2(st_mc[mt][r] - tmc[mt][r]);
-                st_mc[mt][r] = tmc[mt][r];
+              if (!(part[mt][r] <= 0x1p64f)) {
+                const float tmc = fmaxf(acc[0][mt][r], acc[1][mt][r]) * a.c;
+                st_l[mt][r] *= fast_exp2(st_mc[mt][r] - tmc);
+                st_mc[mt][r] = tmc;
+                part[mt][r] = fast_exp2(__builtin_fmaf(acc[0][mt][r], a.c, -tmc)) +
+                              fast_exp2(__builtin_fmaf(acc[1][mt][r], a.c, -tmc));
               }
         }
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-              st_l[mt][r] += fast_exp2(__builtin_fmaf(acc[j][mt][r], a.c, -st_mc[mt][r]));
+          for (int r = 0; r < 4; ++r) st_l[mt][r] += part[mt][r];
       } else if (MODE == kColMass) {
 #pragma unroll
         for (int j = 0; j < 2; ++j)

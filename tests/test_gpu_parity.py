@@ -235,6 +235,35 @@ SEL_CASES = [
 ]
 
 
+def test_select_score_spikes_move_the_row_maximum():
+    """Five keys along each group's mean query direction, scaled so that
+    most rows score them 60-900 nats above the other keys, sit after the
+    rows' first tiles: the running row maximum has to move in mid-row (the
+    terms would otherwise leave fp32's range), and the selection still
+    matches the oracle's."""
+    wl = _small("ctx32k_bf16", n=9000 + 37, hq=8, hkv=2)
+    seq = synth.make_sequence(wl)
+    G, d = wl.group, 128
+    k32 = synth.bf16_bits_to_f32(seq.k)
+    q32 = synth.bf16_bits_to_f32(seq.q_obs)
+    spikes = [2503, 6001, 6002, 7500, 8801]
+    for h in range(wl.hkv):
+        u = q32[h * G:(h + 1) * G].reshape(-1, d).astype(np.float64).mean(axis=0)
+        u /= np.linalg.norm(u)
+        for j, p in enumerate(spikes):
+            k32[h, p] = (60.0 * (1 + j) * math.sqrt(d) * u).astype(np.float32)
+    kb = synth.f32_to_bf16_bits(k32)
+    heads = [1, 0]
+    b = wl.chunk_budget
+    say(f"select with score spikes n={seq.n} b={b} spikes={spikes}")
+    idx = ck.select_critical(to_dev(seq.q_obs), to_dev(kb), heads, wl.cs, b).cpu().numpy()
+    qf, kf = f64(seq.q_obs), f64(kb)
+    for s_, h in enumerate(heads):
+        sc = O.chunk_scores(qf, kf, h, G, wl.l_obs, wl.cs, 1 / math.sqrt(d))
+        assert int(np.argmax(sc)) == spikes[-1] // wl.cs   # the largest spike's chunk leads
+        check_topk(idx[s_], sc, b)
+
+
 @pytest.mark.parametrize("name,kw", SEL_CASES)
 def test_select_and_compact(name, kw):
     wl = _small(name, **kw)
