@@ -143,6 +143,36 @@ class TestSelection:
         Ab = O.selection_observation_matrix(q[1:], k, 0.25)
         np.testing.assert_allclose(A, (Aa + Ab) / 2, atol=1e-15)
 
+    def test_chunk_scores_with_unit_chunks_sum_to_window_length(self):
+        # Algorithm 1 normalises each window row over exactly K[:-L_obs]: with
+        # cs = 1, BlockMax is the identity and the column masses of the L_obs
+        # row-stochastic rows add up to L_obs.  A softmax over any wider key
+        # range (the whole row, or one window key more) leaves less.
+        r = rng(19)
+        Hq, Hkv, L, n, d = 8, 2, 12, 150, 32
+        q, k = r.normal(size=(Hq, L, d)), r.normal(size=(Hkv, n, d))
+        for h in range(Hkv):
+            C = O.chunk_scores(q, k, h, Hq // Hkv, L, 1, 1 / math.sqrt(d))
+            assert C.shape == (n - L,)
+            assert abs(C.sum() - L) < 1e-11
+
+    @pytest.mark.parametrize("L", [1, 3])
+    def test_chunk_scores_exclude_the_window_keys(self, L):
+        # Two prefix keys whose scores differ by ln 3 and L window keys with a
+        # far larger score.  Restricted to K[:-L_obs], every window row puts
+        # 3/4 and 1/4 on the two prefix keys, so C = (3/4 L, 1/4 L); were the
+        # window keys inside the softmax they would take almost all the mass.
+        d = 16
+        q = np.zeros((1, L, d)); q[0, :, 0] = 1.0
+        k = np.zeros((1, 2 + L, d))
+        k[0, 0, 0] = math.log(3.0) * math.sqrt(d)
+        k[0, 2:, 0] = 40.0 * math.sqrt(d)
+        C = O.chunk_scores(q, k, 0, 1, L, 1, 1 / math.sqrt(d))
+        np.testing.assert_allclose(C, [0.75 * L, 0.25 * L], rtol=0, atol=1e-14)
+        # one chunk over both keys: BlockMax keeps the larger mass
+        C2 = O.chunk_scores(q, k, 0, 1, L, 2, 1 / math.sqrt(d))
+        np.testing.assert_allclose(C2, [0.75 * L], rtol=0, atol=1e-14)
+
     def test_block_max_worked_example(self):
         np.testing.assert_array_equal(O.block_max(np.array([1., 5., 2., 3., 4.]), 2), [5, 3, 4])
         np.testing.assert_array_equal(O.block_max(np.array([1., 5., 2.]), 8), [5])
@@ -360,6 +390,14 @@ class TestQuantileAndClassify:
         # r = 0.5 with H = 4: Eq. 5 keeps 2 heads per sample
         assert st.tolist() == [True, False, False, True]
         assert O.static_head_types(sc[:1], 0.5).tolist() == O.classify_sample(sc[0], 0.5).tolist()
+
+    @pytest.mark.parametrize("r,n_cons", [(0.25, 6), (0.3, 5), (0.4, 5), (0.5, 4)])
+    def test_static_set_size_equals_one_sample_of_distinct_scores(self, r, n_cons):
+        # eight heads, distinct scores: Eq. 5 keeps the heads strictly above the
+        # linear r-quantile; the static set over several samples keeps as many
+        sc = np.stack([rng(32 + s).permutation(np.arange(8) * 0.1 + 0.05) for s in range(5)])
+        assert O.classify_sample(sc[0], r).sum() == n_cons
+        assert O.static_head_types(sc, r).sum() == n_cons
 
 
 class TestAroundDecoding:
