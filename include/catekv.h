@@ -76,6 +76,7 @@ typedef struct catekv_decode_plan_t {
   uint64_t magic;
   int32_t batch, hq, hkv, split_tokens;
   int32_t n_workers, n_segments, n_slots, n_multi;
+  int32_t variant, reserved;
   uint64_t segs_off, workers_off, views_off, slots_off, ws_bytes;
   int64_t max_len_total;
 } catekv_decode_plan_t;

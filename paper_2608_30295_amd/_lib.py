@@ -30,6 +30,7 @@ class DecodePlanT(ctypes.Structure):
         ("split_tokens", ctypes.c_int32),
         ("n_workers", ctypes.c_int32), ("n_segments", ctypes.c_int32), ("n_slots", ctypes.c_int32),
         ("n_multi", ctypes.c_int32),
+        ("variant", ctypes.c_int32), ("reserved", ctypes.c_int32),
         ("segs_off", ctypes.c_uint64), ("workers_off", ctypes.c_uint64), ("views_off", ctypes.c_uint64),
         ("slots_off", ctypes.c_uint64),
         ("ws_bytes", ctypes.c_uint64),

@@ -86,17 +86,22 @@ struct PlanLayout {
 
 size_t a256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Decode workgroups of a default plan: as many as the device holds at once,
-// or one per compute unit when the step is small (fewer than kFewTokens rows
-// in all views; 128 MB of bf16 K and V): a step that short is dominated by its
-// fixed costs (start-up chain, partials, merge), which one workgroup per CU
-// halves, while a longer step streams slightly faster with two.
-constexpr int64_t kFewTokens = 1 << 18;
-int device_workers(int G, const int64_t* max_len, int n_views) {
+int device_cus() {
   int dev = 0, n_cu = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n_cu < 1)
     n_cu = 256;
+  return n_cu;
+}
+
+// Workgroups of a 4-wave plan: as many as the device holds at once, or one
+// per compute unit when the step is small (fewer than kFewTokens rows in all
+// views; 128 MB of bf16 K and V): a step that short is dominated by its fixed
+// costs (start-up chain, partials, merge), which one workgroup per CU halves,
+// while a longer step streams slightly faster with two.
+constexpr int64_t kFewTokens = 1 << 18;
+int device_workers(int G, const int64_t* max_len, int n_views) {
+  const int n_cu = device_cus();
   int64_t total = 0;
   for (int v = 0; v < n_views; ++v) total += max_len[v];
   return total < kFewTokens ? n_cu : n_cu * catekv::decode_blocks_per_cu(CATEKV_BF16, G);
@@ -148,6 +153,23 @@ PlanLayout plan_layout(const int64_t* max_len, int n_views, int G, int split, in
   P.slots_off = o; o += a256((size_t)std::max(P.n_slots, 1) * sf);
   P.total = o;
   return P;
+}
+
+// The decode layout of a plan: one 8-wave workgroup per compute unit, whose
+// LDS table holds up to kDecodeV2MaxSeg segments per workgroup; when some
+// workgroup's share would cross more views than that (many tiny or empty
+// views), the 4-wave layout, which reads segment descriptors as it goes.
+PlanLayout choose_plan(const int64_t* max_len, int n_views, int G, int split, int* variant) {
+  PlanLayout P = plan_layout(max_len, n_views, G, split, device_cus());
+  std::vector<int> per_worker(P.n_workers, 0);
+  int most = 0;
+  for (const Segment& sg : P.segs) most = std::max(most, ++per_worker[sg.worker]);
+  if (most <= catekv::kDecodeV2MaxSeg) {
+    *variant = catekv::kDecodeStreamV2;
+    return P;
+  }
+  *variant = catekv::kDecodeStreamK4;
+  return plan_layout(max_len, n_views, G, split, device_workers(G, max_len, n_views));
 }
 
 int check_lengths(const int64_t* max_len, int n) {
@@ -329,7 +351,8 @@ size_t catekv_decode_workspace(const int64_t* max_len_host, int batch, int hq, i
   const int nv = batch * hkv;
   for (int i = 0; i < nv; ++i)
     if (max_len_host[i] < 0 || max_len_host[i] > INT32_MAX) return 0;
-  return plan_layout(max_len_host, nv, hq / hkv, split_tokens, device_workers(hq / hkv, max_len_host, nv)).total;
+  int variant = 0;
+  return choose_plan(max_len_host, nv, hq / hkv, split_tokens, &variant).total;
 }
 
 int catekv_decode_plan(const int64_t* max_len_host, int batch, int hq, int hkv, int split_tokens,
@@ -343,7 +366,8 @@ int catekv_decode_plan(const int64_t* max_len_host, int batch, int hq, int hkv, 
   if (rc) return rc;
   if (!ws) return fail(CATEKV_ERR_WORKSPACE, "workspace pointer is null");
   const int G = hq / hkv;
-  const PlanLayout P = plan_layout(max_len_host, nv, G, split_tokens, device_workers(G, max_len_host, nv));
+  int variant = 0;
+  const PlanLayout P = choose_plan(max_len_host, nv, G, split_tokens, &variant);
   rc = check_ws(ws, ws_bytes, P.total);
   if (rc) return rc;
 
@@ -388,6 +412,7 @@ int catekv_decode_plan(const int64_t* max_len_host, int batch, int hq, int hkv, 
   plan->n_segments = P.n_segments;
   plan->n_slots = P.n_slots;
   plan->n_multi = P.n_multi;
+  plan->variant = variant;
   plan->segs_off = P.segs_off;
   plan->workers_off = P.workers_off;
   plan->views_off = P.views_off;
@@ -424,6 +449,7 @@ int catekv_decode_attn(int dtype, const catekv_decode_plan_t* plan, const void* 
   a.n_multi = plan->n_multi;
   a.n_views = batch * hkv;
   a.hkv = hkv;
+  a.variant = plan->variant;
   a.scale = scale;
   a.out = out;
   a.lse = lse;

@@ -518,6 +518,279 @@ void decode_stream_mfma_kernel(DecodeArgs a) {
   }
 }
 
+// ---- bf16 storage, one 8-wave workgroup per compute unit ---------------------
+// The same contraction layout as above, with three changes:
+//  * All segments of the worker are described once, at the start, in an LDS
+//    table (view pointers, token range, output row or partial slot, and the
+//    group's query rows), so no descriptor load sits between two tiles.
+//  * Each wave's tiles (tile u of a segment goes to wave u % 8) form one
+//    continuous stream across the worker's segments: the load of the next tile
+//    is issued before the current one is used even when the next tile belongs
+//    to the next segment.
+//  * At the end of a segment the eight waves merge their (m, l, O) through LDS
+//    after a barrier that waits only for LDS operations, so the loads already
+//    in flight keep streaming; a wave with no tile in a segment contributes an
+//    empty state.  The LDS merge area is double-buffered by segment parity.
+// P V runs on v_mfma_f32_16x16x16_bf16 with P split into a bf16 high part and
+// a bf16 remainder (P = hi + lo up to 2^-18 relative; the bf16 products are
+// exact in the fp32 accumulator).  The score tile's lanes and registers are
+// already that instruction's A operand (head = lane % 16, token 4 (lane / 16)
+// + i); the B operand of product e takes dim 8 (lane % 16) + e of the four
+// token rows a lane loaded, so O keeps the layout of the fp32 path.
+constexpr int kV2Waves = 8;
+constexpr int kV2MaxSeg = kDecodeV2MaxSeg;   // segments per worker held in the LDS table
+
+struct V2Seg {
+  const char* k;
+  const char* v;
+  int32_t t0, t_end, n_units, row0, slot, n_parts;
+};
+
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+// bf16 pair (RNE) of two fp32 values, as one 32-bit word (x in the low half)
+__device__ __forceinline__ uint32_t pack_bf16(float x, float y) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{x, y}), bf16x2_t));
+}
+
+template <int G>
+__global__ __launch_bounds__(kV2Waves * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void decode_stream_v2_kernel(DecodeArgs a) {
+  static_assert(G <= 16, "heads of a group must fit the 16 MFMA columns");
+  constexpr int WAVES = kV2Waves;
+  constexpr int NT = WAVES * 64;
+  constexpr int SF = G * kD + 2 * G;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int n16 = lane & 15, k4 = lane >> 4;
+  const int hkv = a.hkv, hq = hkv * G;
+  const float scale = a.scale;
+  const float c = scale * kLog2e;
+  const float thr = 8.0f / c;
+  const bool head_lane = n16 < G;
+
+  __shared__ V2Seg s_seg[kV2MaxSeg];
+  __shared__ uint4 s_q[kV2MaxSeg][G][16];       // per segment: G query rows of 16 x 16 bytes
+  __shared__ float s_o[2][WAVES][G][kD];
+  __shared__ float s_ml[2][WAVES][2][G];
+
+  const int seg_lo = a.worker_seg[blockIdx.x];
+  const int nseg = a.worker_seg[blockIdx.x + 1] - seg_lo;   // the plan keeps it <= kV2MaxSeg
+
+  if ((int)threadIdx.x < nseg) {
+    const DecodeItem it = a.items[seg_lo + threadIdx.x];
+    const catekv_kv_ptrs view = a.kv[it.bh];
+    int64_t len = a.lens[it.bh];
+    const ViewInfo vi = a.views[it.bh];
+    len = len < 0 ? 0 : len;
+    const int t_end = (int)((int64_t)it.t1 < len ? (int64_t)it.t1 : len);
+    const int b = it.bh / hkv, h = it.bh - b * hkv;
+    V2Seg sg;
+    sg.k = reinterpret_cast<const char*>(view.k);
+    sg.v = reinterpret_cast<const char*>(view.v);
+    sg.t0 = it.t0;
+    sg.t_end = t_end;
+    sg.n_units = t_end > it.t0 ? (t_end - it.t0 + 15) / 16 : 0;
+    sg.row0 = b * hq + h * G;
+    sg.slot = vi.first_slot + it.part;
+    sg.n_parts = vi.n_parts;
+    s_seg[threadIdx.x] = sg;
+  }
+  for (int t = threadIdx.x; t < nseg * G * 16; t += NT) {
+    const int sgi = t / (G * 16), r = t - sgi * (G * 16);
+    const int g = r >> 4, piece = r & 15;
+    const int bh = a.items[seg_lo + sgi].bh;
+    const int b = bh / hkv, h = bh - b * hkv;
+    s_q[sgi][g][piece] = ldg16(reinterpret_cast<const char*>(a.q) +
+                               ((size_t)b * hq + (size_t)h * G + g) * (kD * 2) + piece * 16);
+  }
+  __syncthreads();
+
+  // ---- this wave's tile stream ----------------------------------------------
+  int is = 0, iu = wave;                          // issue cursor: segment, tile of the segment
+  auto skip = [&]() {
+    while (is < nseg && iu >= s_seg[is].n_units) {
+      ++is;
+      iu = wave;
+    }
+  };
+  skip();
+
+  uint4 kb[2][4], vb[2][4];
+  int meta_seg[2], meta_tile[2];                 // segment and first token of the tile in each buffer
+  int lseg = 0, ltile = 0;                       // the last tile issued for real
+  // Loads of one tile; past the end of the stream the last real tile is read
+  // again (cached) and the buffer is marked empty.  Rows past a segment's end
+  // re-read its first row, so every address lies inside a segment's rows.
+  auto issue = [&](int buf) {
+    if (is < nseg) {
+      lseg = is;
+      ltile = s_seg[is].t0 + iu * 16;
+      meta_seg[buf] = is;
+      meta_tile[buf] = ltile;
+      iu += WAVES;
+      skip();
+    } else {
+      meta_seg[buf] = -1;
+    }
+    const V2Seg& sg = s_seg[lseg];
+    int tk = ltile + n16;
+    tk = tk < sg.t_end ? tk : sg.t0;
+    const char* kr = sg.k + (size_t)tk * (kD * 2) + k4 * 16;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) kb[buf][ks] = ldg16(kr + ks * 64);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      int tv = ltile + 4 * k4 + r;
+      tv = tv < sg.t_end ? tv : sg.t0;
+      vb[buf][r] = ldg16(sg.v + (size_t)tv * (kD * 2) + n16 * 16);
+    }
+  };
+
+  // running state of the segment whose tiles this wave is consuming
+  f32x4_t O[8];
+  float m, l;
+  int st_seg = -1;
+  auto reset_state = [&]() {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) O[e] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    m = head_lane ? kDecodeMFloor : INFINITY;
+    l = 0.f;
+  };
+  reset_state();
+  uint4 qb[4];
+  int q_seg = -1;
+
+  // merge of segment s: every wave writes its state (or an empty one), then the
+  // workgroup reduces the eight states and writes the output or the partial
+  int merged = 0;
+  auto merge = [&](int s) {
+    const int buf = s & 1;
+    const bool mine = st_seg == s;
+    float lt = mine ? l : 0.f;
+    lt += shfl_xor(lt, 16);
+    lt += shfl_xor(lt, 32);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int head = 4 * k4 + r;
+      if (head < G) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) s_o[buf][wave][head][8 * n16 + e] = mine ? O[e][r] : 0.f;
+      }
+    }
+    if (lane < G) {
+      s_ml[buf][wave][0][lane] = mine ? m : kDecodeMFloor;
+      s_ml[buf][wave][1][lane] = lt;
+    }
+    if (mine) {
+      reset_state();
+      st_seg = -1;
+    }
+    barrier_lds_only();
+    const V2Seg& sg = s_seg[s];
+    for (int t = threadIdx.x; t < G * kD; t += NT) {
+      const int g = t / kD, e = t - g * kD;
+      float M = kDecodeMFloor;
+#pragma unroll
+      for (int w = 0; w < WAVES; ++w) M = fmaxf(M, s_ml[buf][w][0][g]);
+      float L = 0.f, Ov = 0.f;
+#pragma unroll
+      for (int w = 0; w < WAVES; ++w) {
+        const float cw = fast_exp2((s_ml[buf][w][0][g] - M) * c);
+        L += s_ml[buf][w][1][g] * cw;
+        Ov += s_o[buf][w][g][e] * cw;
+      }
+      const float Mn = M * scale;                 // natural-log units of the scaled score
+      if (sg.n_parts == 1) emit(a.out, a.lse, (size_t)sg.row0 + g, e, Mn, L, Ov);
+      else put_slot<G>(a.slots + (size_t)sg.slot * SF, g, e, Mn, L, Ov);
+    }
+  };
+
+  auto consume = [&](int buf) {
+    const int s = meta_seg[buf];
+    while (merged < s) merge(merged++);
+    if (q_seg != s) {
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) qb[ks] = head_lane ? s_q[s][head_lane ? n16 : 0][4 * ks + k4] : make_uint4(0, 0, 0, 0);
+      q_seg = s;
+    }
+    st_seg = s;
+    const int tile = meta_tile[buf];
+    const int t_end = s_seg[s].t_end;
+    f32x4_t S = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+      S = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kb[buf][ks]),
+                                                  __builtin_bit_cast(bf16x8_t, qb[ks]), S, 0, 0, 0);
+    float sv[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sv[r] = tile + 4 * k4 + r < t_end ? S[r] : -INFINITY;
+    float mx = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+    mx = fmaxf(mx, shfl_xor(mx, 16));
+    mx = fmaxf(mx, shfl_xor(mx, 32));
+    const bool need = head_lane && mx > m + thr;
+    if (__builtin_amdgcn_ballot_w64(need)) {
+      float corr = 1.f;
+      if (head_lane && mx > m) {
+        corr = fast_exp2((m - mx) * c);           // 0 while m is still the floor
+        m = mx;
+      }
+      l *= corr;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int src = (4 * k4 + r) & 15;
+        const float cr = __int_as_float(__builtin_amdgcn_ds_bpermute(src << 2, __float_as_int(corr)));
+#pragma unroll
+        for (int e = 0; e < 8; ++e) O[e][r] *= cr;
+      }
+    }
+    const float mc = m * c;
+    float P[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      P[r] = fast_exp2(__builtin_fmaf(sv[r], c, -mc));
+      l += P[r];
+    }
+    // P = hi + lo, both bf16
+    const uint32_t h01 = pack_bf16(P[0], P[1]), h23 = pack_bf16(P[2], P[3]);
+    const uint32_t l01 = pack_bf16(P[0] - __uint_as_float(h01 << 16), P[1] - __uint_as_float(h01 & 0xffff0000u));
+    const uint32_t l23 = pack_bf16(P[2] - __uint_as_float(h23 << 16), P[3] - __uint_as_float(h23 & 0xffff0000u));
+    const s16x4_t A_hi = __builtin_bit_cast(s16x4_t, make_uint2(h01, h23));
+    const s16x4_t A_lo = __builtin_bit_cast(s16x4_t, make_uint2(l01, l23));
+    const uint32_t w0[4] = {vb[buf][0].x, vb[buf][0].y, vb[buf][0].z, vb[buf][0].w};
+    const uint32_t w1[4] = {vb[buf][1].x, vb[buf][1].y, vb[buf][1].z, vb[buf][1].w};
+    const uint32_t w2[4] = {vb[buf][2].x, vb[buf][2].y, vb[buf][2].z, vb[buf][2].w};
+    const uint32_t w3[4] = {vb[buf][3].x, vb[buf][3].y, vb[buf][3].z, vb[buf][3].w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      // dims 8 n16 + 2 i (low halves) and 8 n16 + 2 i + 1 (high halves) of the four token rows
+      const uint2 be = make_uint2((w0[i] & 0xffffu) | (w1[i] << 16), (w2[i] & 0xffffu) | (w3[i] << 16));
+      const uint2 bo = make_uint2((w0[i] >> 16) | (w1[i] & 0xffff0000u), (w2[i] >> 16) | (w3[i] & 0xffff0000u));
+      const s16x4_t Be = __builtin_bit_cast(s16x4_t, be), Bo = __builtin_bit_cast(s16x4_t, bo);
+      O[2 * i] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(A_hi, Be, O[2 * i], 0, 0, 0);
+      O[2 * i] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(A_lo, Be, O[2 * i], 0, 0, 0);
+      O[2 * i + 1] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(A_hi, Bo, O[2 * i + 1], 0, 0, 0);
+      O[2 * i + 1] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(A_lo, Bo, O[2 * i + 1], 0, 0, 0);
+    }
+  };
+
+  if (is < nseg) {
+    issue(0);
+    bool more = true;
+    while (more) {
+#pragma unroll
+      for (int B = 0; B < 2; ++B) {
+        issue(B ^ 1);
+        if (meta_seg[B] >= 0) consume(B);
+        else more = false;
+      }
+    }
+  }
+  while (merged < nseg) merge(merged++);
+}
+
 // Merges the partials of every view covered by more than one segment: one
 // workgroup per (view, query head).  Thread (part lane pl, dim quad dq) loads
 // the float4 o of parts pl, pl + 8, ... together with their (m, l) in one
@@ -603,10 +876,13 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(DecodeA
 
 template <typename T, int G>
 static hipError_t launch_t(const DecodeArgs& a, hipStream_t stream) {
-  if constexpr (std::is_same<T, uint16_t>::value)
-    hipLaunchKernelGGL((decode_stream_mfma_kernel<G, kDecodeWaves, kDecodeStagesMfma>), dim3(a.n_workers),
-                       dim3(kDecodeWaves * 64), 0, stream, a);
-  else
+  if constexpr (std::is_same<T, uint16_t>::value) {
+    if (a.variant == kDecodeStreamV2)
+      hipLaunchKernelGGL((decode_stream_v2_kernel<G>), dim3(a.n_workers), dim3(kV2Waves * 64), 0, stream, a);
+    else
+      hipLaunchKernelGGL((decode_stream_mfma_kernel<G, kDecodeWaves, kDecodeStagesMfma>), dim3(a.n_workers),
+                         dim3(kDecodeWaves * 64), 0, stream, a);
+  } else
     hipLaunchKernelGGL((decode_stream_kernel<T, G, kDecodeWaves, kDecodeStages>), dim3(a.n_workers),
                        dim3(kDecodeWaves * 64), 0, stream, a);
   if (a.n_multi > 0)

@@ -26,6 +26,12 @@ constexpr int kDecodeStages = 4;   // register prefetch depth (fp32 path)
 constexpr int kDecodeStagesMfma = 2;   // register prefetch depth (bf16 MFMA path, 16-token stages)
 constexpr int kDecodeQuantum = 64; // tokens per workgroup load stage (16 per wave)
 
+// Decode kernels a plan is cut for.
+constexpr int kDecodeStreamK4 = 1;   // 4-wave workgroups, as many as the device holds (any segment count)
+constexpr int kDecodeStreamV2 = 2;   // one 8-wave workgroup per compute unit (bf16), <= kDecodeV2MaxSeg
+                                     // segments per workgroup
+constexpr int kDecodeV2MaxSeg = 16;
+
 // Per view: where its partial slots live and how many segments cover it.
 struct ViewInfo {
   int32_t first_slot;     // slot of part 0
@@ -45,6 +51,7 @@ struct DecodeArgs {
   const ViewInfo* views;
   float* slots;                 // partial slots
   int n_workers, n_views, n_multi, hkv;
+  int variant;                  // kDecodeStreamK4 or kDecodeStreamV2
   float scale;
   float* out;
   float* lse;
