@@ -9,6 +9,7 @@
  *   catekv_score_heads      CV head score per KV head      (Section 3.2, Eq. 1-4)
  *   catekv_classify_heads   consistent/adaptive head types (Eq. 5; static identification)
  *   catekv_select_critical  critical chunks per head       (Algorithm 1, pre-filling stage)
+ *   catekv_adaptive_budget  chunk budget for retention eta (Algorithm 1, argtopk(C_chunk, n eta))
  *   catekv_compact_kv       dense compact K/V per head     (Algorithm 1, Cache(K, V, i_k, L_obs))
  *   catekv_decode_plan      split-KV work list for a batch (host side, once per request)
  *   catekv_decode_attn      GQA decode over mixed per-head cache lengths
@@ -150,6 +151,20 @@ int catekv_select_critical(int dtype, const void* q_obs, const void* k,
                            const int32_t* sel_heads_host, int n_sel, int b,
                            int32_t* idx_out, void* ws, size_t ws_bytes, void* stream);
 
+/* Chunk budget of an adaptive head for retention ratio eta (Algorithm 1,
+ * adaptive branch, argtopk(C_chunk, n eta)), counted in chunks of the
+ * selection range: *b_out = ceil(eta * ceil((n - l_obs) / cs)), eta read as
+ * the decimal ratio it stands for (a product within 1e-9 relative of an
+ * integer is that integer); eta = 1 keeps every chunk, i.e. the whole cache,
+ * and the last l_obs tokens are kept on top, as for consistent heads.  Host
+ * only.
+ * Pass the result as b to catekv_select_critical and catekv_compact_kv for
+ * the adaptive heads (b >= 1 there; eta small enough to give 0 keeps only
+ * the window).
+ * Errors: INVALID_ARG for a null b_out, l_obs outside [0, n), cs < 1 or eta
+ * outside [0, 1]. */
+int catekv_adaptive_budget(int64_t n, int l_obs, int cs, double eta, int64_t* b_out);
+
 /* Cache(K, V, i_k, L_obs) of Algorithm 1: for each selected head s, writes the
  * rows of the chunks idx[s][*] (ascending; entries < 0 ignored; the last chunk
  * may be partial) followed by the last l_obs rows k[h][n - l_obs .. n) into
@@ -207,9 +222,10 @@ int catekv_decode_plan(const int64_t* max_len_host, int batch, int hq, int hkv,
  *       full cache or into compact caches; rows beyond L are never used)
  * lens  [batch][hkv] int64, device (read on the device at run time)
  * out   [batch][hq][d] fp32; lse [batch][hq] fp32 or NULL.
+ * scale > 0 and finite (1/sqrt(d) for the paper's attention).
  * ws must be the workspace given to catekv_decode_plan for `plan`.
- * Errors: INVALID_ARG if shapes disagree with the plan or pointers are null;
- * WORKSPACE if ws is too small. */
+ * Errors: INVALID_ARG if shapes disagree with the plan, pointers are null or
+ * scale is not positive and finite; WORKSPACE if ws is too small. */
 int catekv_decode_attn(int dtype, const catekv_decode_plan_t* plan, const void* q,
                        const catekv_kv_ptrs* kv, const int64_t* lens,
                        int batch, int hq, int hkv, int d, float scale,

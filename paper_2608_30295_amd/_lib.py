@@ -45,6 +45,7 @@ SIGNATURES = {
                                    c_i64, c_i64, c_double, c_double, c_int, c_void_p, c_void_p, c_size,
                                    c_void_p]),
     "catekv_classify_heads": (c_int, [P_f32, c_int, c_int, c_double, P_u8]),
+    "catekv_adaptive_budget": (c_int, [c_i64, c_int, c_int, c_double, P_i64]),
     "catekv_select_workspace": (c_size, [c_int, c_int, c_int, c_i64, c_int, c_int]),
     "catekv_select_critical": (c_int, [c_int, c_void_p, c_void_p, c_int, c_int, c_int, c_i64, c_int, c_int,
                                        P_i32, c_int, c_int, c_void_p, c_void_p, c_size, c_void_p]),

@@ -206,11 +206,11 @@ def append_kv(kv: torch.Tensor, capacity: torch.Tensor, lens: torch.Tensor, k_ne
 
 
 def adaptive_budget(n: int, l_obs: int, cs: int, eta: float) -> int:
-    """Chunk budget of an adaptive head for retention ratio eta (Algorithm 1,
-    argtopk(C_chunk, n eta) counted in chunks): ceil(eta * ceil((n - l_obs) / cs)).
-    eta = 1 keeps every chunk, i.e. the original cache."""
-    nc = -(-(n - l_obs) // cs)
-    return int(math.ceil(eta * nc - 1e-12))
+    """Chunk budget of an adaptive head for retention ratio eta
+    (catekv_adaptive_budget: Algorithm 1, argtopk(C_chunk, n eta) in chunks)."""
+    b = ctypes.c_int64(0)
+    check(lib().catekv_adaptive_budget(int(n), int(l_obs), int(cs), float(eta), ctypes.byref(b)))
+    return int(b.value)
 
 
 def page_bounds(k: torch.Tensor, heads: Sequence[int], cs: int) -> Tuple[torch.Tensor, torch.Tensor]:

@@ -285,6 +285,22 @@ int catekv_score_heads(int dtype, const void* q_rows, int64_t q_pos0, const void
   return ok();
 }
 
+int catekv_adaptive_budget(int64_t n, int l_obs, int cs, double eta, int64_t* b_out) {
+  if (!b_out) return fail(CATEKV_ERR_INVALID_ARG, "b_out is null");
+  if (l_obs < 0 || (int64_t)l_obs >= n) return fail(CATEKV_ERR_INVALID_ARG, "l_obs=%d outside [0, n=%lld)", l_obs, (long long)n);
+  if (cs < 1) return fail(CATEKV_ERR_INVALID_ARG, "chunk size %d must be >= 1", cs);
+  if (!(eta >= 0.0 && eta <= 1.0)) return fail(CATEKV_ERR_INVALID_ARG, "eta=%g outside [0, 1]", eta);
+  const int64_t nc = (n - l_obs + cs - 1) / cs;
+  // eta is the decimal ratio the caller means: a product within 1e-9
+  // (relative) of an integer is that integer, so the binary representation
+  // of, e.g., 0.1 or 0.3 neither adds nor drops a chunk
+  const double p = eta * (double)nc;
+  const double r = std::nearbyint(p);
+  const int64_t b = std::fabs(p - r) <= 1e-9 * std::max(1.0, p) ? (int64_t)r : (int64_t)std::ceil(p);
+  *b_out = std::min<int64_t>(std::max<int64_t>(b, 0), nc);
+  return ok();
+}
+
 int catekv_classify_heads(const float* cv_host, int S, int H, double r, uint8_t* is_consistent_host) {
   if (!cv_host || !is_consistent_host) return fail(CATEKV_ERR_INVALID_ARG, "null pointer");
   if (S < 1 || H < 1) return fail(CATEKV_ERR_INVALID_ARG, "S=%d H=%d must be >= 1", S, H);
@@ -433,7 +449,8 @@ int catekv_decode_attn(int dtype, const catekv_decode_plan_t* plan, const void* 
   if (plan->batch != batch || plan->hq != hq || plan->hkv != hkv)
     return fail(CATEKV_ERR_INVALID_ARG, "shapes (batch=%d hq=%d hkv=%d) differ from the plan (%d, %d, %d)", batch, hq,
                 hkv, plan->batch, plan->hq, plan->hkv);
-  if (!std::isfinite(scale)) return fail(CATEKV_ERR_INVALID_ARG, "scale is not finite");
+  if (!(scale > 0.f) || !std::isfinite(scale))
+    return fail(CATEKV_ERR_INVALID_ARG, "scale=%g must be positive and finite", (double)scale);
   rc = check_ws(ws, ws_bytes, plan->ws_bytes);
   if (rc) return rc;
   char* w = reinterpret_cast<char*>(ws);

@@ -782,7 +782,7 @@ __global__ void compact_kernel(CompactArgs a) {
 
 struct CvState {                 // per KV head, in the workspace
   uint32_t prefix;               // radix prefix of the order statistic x_(lo)
-  int32_t remaining;             // 0-based rank still to resolve inside the prefix
+  int64_t remaining;             // 0-based rank still to resolve inside the prefix (up to N - 1 >= 2^31)
   uint32_t min_above_key;        // smallest ordered key strictly above x_(lo)
   uint32_t need_scan;            // 1: min_above_key must come from a pass over A
   unsigned long long cnt_lt;     // entries strictly below x_(lo)
@@ -808,7 +808,7 @@ __global__ void cv_init_kernel(CvState* st, uint32_t* hist, int64_t N, double k_
   if (blockIdx.x == 0 && threadIdx.x < hkv) {
     CvState& s = st[threadIdx.x];
     s.prefix = 0;
-    s.remaining = (int32_t)(int64_t)floor((double)(N - 1) * k_pct);
+    s.remaining = (int64_t)floor((double)(N - 1) * k_pct);
     s.min_above_key = 0xFFFFFFFFu;
     s.need_scan = 0;
     s.cnt_lt = 0;
@@ -998,7 +998,7 @@ __global__ __launch_bounds__(kPickThreads) void radix_pick_kernel(const uint32_t
   if (t == 0) {
     const uint32_t prefix = st[h].prefix | ((uint32_t)bin << digit_shift(pass));
     st[h].prefix = prefix;
-    st[h].remaining = (int32_t)(rem - s_cum);
+    st[h].remaining = rem - s_cum;
     st[h].cnt_lt += (unsigned long long)s_cum;
     if (pass == 0) st[h].c0 = s_bcnt;
     if (pass == 2) {

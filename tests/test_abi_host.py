@@ -28,7 +28,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 15
+    assert len(names) == 16
     L = ck.lib()
     for n in names:
         assert hasattr(L, n), n
@@ -83,6 +83,51 @@ def test_decode_attn_rejects_unplanned_use():
     rc, _ = _status_and_msg(L.catekv_decode_attn(7, ctypes.byref(plan), FAKE, FAKE, FAKE, 1, 32, 8, 128,
                                                  0.08, FAKE, None, FAKE, 1 << 20, None))
     assert rc == _lib.CATEKV_ERR_UNSUPPORTED
+
+
+def test_decode_attn_rejects_non_positive_scale():
+    # the softmax needs scale > 0: a zero or negative scale is refused before any launch
+    L = ck.lib()
+    plan = _lib.DecodePlanT()
+    ml = np.array([64, 64], dtype=np.int64)
+    ws = np.zeros(1, dtype=np.uint8)
+    assert L.catekv_decode_workspace(ml.ctypes.data_as(_lib.P_i64), 1, 8, 2, 0) > 0
+    plan.magic = 0x43617465504c414e                    # a plan header as catekv_decode_plan fills it
+    plan.batch, plan.hq, plan.hkv, plan.ws_bytes = 1, 8, 2, 1 << 20
+    for scale in (0.0, -0.088, float("inf"), float("nan")):
+        rc, msg = _status_and_msg(L.catekv_decode_attn(1, ctypes.byref(plan), FAKE, FAKE, FAKE, 1, 8, 2, 128,
+                                                       scale, FAKE, None, FAKE, 1 << 20, None))
+        assert rc == _lib.CATEKV_ERR_INVALID_ARG and "scale" in msg, scale
+    del ws
+
+
+# --------------------------------------------- retention budget (Algorithm 1, argtopk(C_chunk, n eta))
+
+def _budget(n, l_obs, cs, eta):
+    b = ctypes.c_int64(-7)
+    rc = ck.lib().catekv_adaptive_budget(n, l_obs, cs, eta, ctypes.byref(b))
+    return rc, b.value
+
+
+def test_adaptive_budget_hand_values():
+    # n - l_obs = 90 keys -> 12 chunks of 8 (the last one partial)
+    assert [_budget(100, 10, 8, e) for e in (1.0, 0.5, 0.3, 0.25, 0.0)] == [(0, 12), (0, 6), (0, 4), (0, 3), (0, 0)]
+    # 131072 - 64 keys -> 16376 chunks: the workloads' sweep
+    assert [_budget(131072, 64, 8, e)[1] for e in (0.5, 0.25, 0.1)] == [8188, 4094, 1638]
+    # eta is the decimal ratio: 10 chunks at 0.1, 0.3, 0.7 keep 1, 3, 7 (the
+    # stored 0.1 lies above 1/10, the stored 0.3 and 0.7 below), and 0.55 keeps 6
+    assert [_budget(88, 8, 8, e)[1] for e in (0.1, 0.3, 0.7, 0.5, 0.55)] == [1, 3, 7, 5, 6]
+    # one chunk over an integer product stays exact for large counts
+    assert _budget(8 * 1000003 + 8, 8, 8, 0.5)[1] == 500002
+    assert ck.adaptive_budget(100, 10, 8, 0.3) == 4
+
+
+def test_adaptive_budget_rejects_bad_arguments():
+    for args in ((100, 10, 8, 1.5), (100, 10, 8, -0.1), (100, 10, 0, 0.5), (100, 100, 8, 0.5), (100, -1, 8, 0.5),
+                 (100, 10, 8, float("nan"))):
+        rc, b = _budget(*args)
+        assert rc == _lib.CATEKV_ERR_INVALID_ARG and b == -7, args
+    assert ck.lib().catekv_adaptive_budget(100, 10, 8, 0.5, None) == _lib.CATEKV_ERR_INVALID_ARG
 
 
 def test_select_rejects_bad_arguments():

@@ -197,3 +197,30 @@ def test_ctx1m_sampled():
     q_st, out, lse, plan = decode_batch([p], wl, 0)
     adap = [h for h in range(wl.hkv) if h not in p.heads][0]
     check_decode(p, q_st[0], out[0], lse[0], [p.heads[0] * wl.group, adap * wl.group + 2])
+
+
+def test_cv_quantile_rank_beyond_two_to_the_31():
+    """Eq. 2 over an observation matrix of more than 2^31 entries: the rank of
+    the k-th percentile element, floor((N - 1) k), no longer fits 32 bits.
+    Closed form: one query row pattern (q = e_0) against zero keys except m
+    planted keys with one equal, larger score; every row puts the same mass
+    on the planted columns, the quantile lands among those entries, so C is
+    L_q on the m planted columns and 0 elsewhere and cv = sqrt((n'' - m) / m)."""
+    lq, n, m = 64, 33_600_000, 16_800
+    N = lq * n
+    assert N > 2 ** 31
+    k_pct = 0.9999                     # (N - 1) k lies among the lq * m planted entries
+    assert (N - 1) * k_pct >= N - lq * m
+    say(f"CV over {N} observation entries (rank {int((N - 1) * k_pct)})")
+    k = torch.zeros((1, n, 128), dtype=torch.bfloat16, device=DEV)
+    cols = torch.from_numpy(np.random.default_rng(5).choice(n, size=m, replace=False)).to(DEV)
+    k[0, cols, 0] = 45.25              # exact in bf16: score 45.25 / sqrt(128) against q = e_0
+    q = torch.zeros((1, lq, 128), dtype=torch.bfloat16, device=DEV)
+    q[0, :, 0] = 1.0
+    cv = ck.score_heads(q, k, q_pos0=n, l_init=0, l_rec=0, k_pct=k_pct, alpha=1.0, causal=False)
+    torch.cuda.synchronize()
+    want = math.sqrt((n - m) / m)
+    got = float(cv.cpu()[0])
+    del k
+    torch.cuda.empty_cache()
+    assert abs(got - want) <= 1e-4 * want, (got, want)

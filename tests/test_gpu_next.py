@@ -107,7 +107,6 @@ def test_retention_below_one(eta):
     n, G = seq.n, wl.group
     adaptive, consistent = [0, 3, 6], [1, 2, 4, 5, 7]
     ba = ck.adaptive_budget(n, wl.l_obs, wl.cs, eta)
-    assert ba == O.adaptive_budget(n, wl.l_obs, wl.cs, eta)
     say(f"retention eta={eta}: {ba} of {-(-(n - wl.l_obs) // wl.cs)} chunks per adaptive head")
     q_obs, k, v = to_dev(seq.q_obs), to_dev(seq.k), to_dev(seq.v)
     lens = torch.full((wl.hkv,), n, dtype=torch.int64, device=DEV)
