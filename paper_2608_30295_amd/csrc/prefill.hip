@@ -1165,7 +1165,9 @@ static SelectLayout select_layout(const SelectGeom& g) {
   size_t o = 0;
   L.rowpart = o; o += align256((size_t)g.n_sel * g.n_colblk * rp * sizeof(float2));
   L.rowoff = o; o += align256((size_t)g.n_sel * rp * sizeof(float));
-  L.colmass = o; o += align256((size_t)g.n_sel * g.n_keys * sizeof(float));
+  // per-key column mass only when BlockMax cannot be fused into the score pass
+  // (cs not dividing the 64-column tile)
+  L.colmass = o; o += kTileTok % g.cs == 0 ? 0 : align256((size_t)g.n_sel * g.n_keys * sizeof(float));
   L.chunks = o; o += align256((size_t)g.n_sel * g.n_chunks * sizeof(float));
   L.topk = o; o += align256(topk_workspace_bytes(g.n_sel, g.n_chunks));
   L.total = o;
@@ -1173,6 +1175,7 @@ static SelectLayout select_layout(const SelectGeom& g) {
 }
 
 size_t select_workspace_bytes(const SelectGeom& g) { return select_layout(g).total; }
+
 
 template <typename T, int MODE, int G, bool CAUSAL>
 static hipError_t launch_score_mt(int mt, dim3 grid, hipStream_t s, const ScoreArgs& a) {
