@@ -151,6 +151,23 @@ int catekv_select_critical(int dtype, const void* q_obs, const void* k,
                            const int32_t* sel_heads_host, int n_sel, int b,
                            int32_t* idx_out, void* ws, size_t ws_bytes, void* stream);
 
+/* catekv_select_critical for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same computation and outputs, with the scratch taken from a
+ * 16 MiB device array inside the library (one per GPU, held until the process
+ * ends) instead of a caller workspace.  It allocates nothing.  Every call on a
+ * GPU shares that GPU's array, so calls that overlap in time on one GPU race
+ * (even on different streams); the array keeps the last call's contents and
+ * nothing in it needs clearing.  16 MiB covers the selection of up to 8 heads
+ * at 1M tokens when cs divides 64 (catekv_select_workspace() gives the need).
+ * Errors: those of catekv_select_critical; UNSUPPORTED when the selection
+ * needs more scratch than the array holds; HIP if the array's device address
+ * cannot be obtained. */
+int catekv_select_critical_noalloc(int dtype, const void* q_obs, const void* k,
+                                   int hq, int hkv, int l_obs, int64_t n, int d, int cs,
+                                   const int32_t* sel_heads_host, int n_sel, int b,
+                                   int32_t* idx_out, void* stream);
+
 /* Chunk budget of an adaptive head for retention ratio eta (Algorithm 1,
  * adaptive branch, argtopk(C_chunk, n eta)), counted in chunks of the
  * selection range: *b_out = ceil(eta * ceil((n - l_obs) / cs)), eta read as

@@ -49,6 +49,8 @@ SIGNATURES = {
     "catekv_select_workspace": (c_size, [c_int, c_int, c_int, c_i64, c_int, c_int]),
     "catekv_select_critical": (c_int, [c_int, c_void_p, c_void_p, c_int, c_int, c_int, c_i64, c_int, c_int,
                                        P_i32, c_int, c_int, c_void_p, c_void_p, c_size, c_void_p]),
+    "catekv_select_critical_noalloc": (c_int, [c_int, c_void_p, c_void_p, c_int, c_int, c_int, c_i64, c_int, c_int,
+                                               P_i32, c_int, c_int, c_void_p, c_void_p]),
     "catekv_compact_kv": (c_int, [c_int, c_void_p, c_void_p, c_int, c_i64, c_int, c_int, c_int, P_i32, c_int,
                                   c_void_p, c_int, c_void_p, c_void_p, c_void_p, c_void_p]),
     "catekv_decode_workspace": (c_size, [P_i64, c_int, c_int, c_int, c_int]),

@@ -347,6 +347,27 @@ int catekv_select_critical(int dtype, const void* q_obs, const void* k, int hq, 
   return ok();
 }
 
+int catekv_select_critical_noalloc(int dtype, const void* q_obs, const void* k, int hq, int hkv, int l_obs,
+                                   int64_t n, int d, int cs, const int32_t* sel_heads_host, int n_sel, int b,
+                                   int32_t* idx_out, void* stream) {
+  if (!valid_dtype(dtype)) return fail(CATEKV_ERR_UNSUPPORTED, "dtype %d unsupported", dtype);
+  if (!q_obs || !k || !idx_out) return fail(CATEKV_ERR_INVALID_ARG, "null tensor pointer");
+  int rc = check_selection(hq, hkv, l_obs, n, d, cs, sel_heads_host, n_sel, b);
+  if (rc) return rc;
+  const catekv::SelectGeom g = select_geom(hq, hkv, l_obs, n, cs, sel_heads_host, n_sel, b);
+  const size_t need = catekv::select_workspace_bytes(g), have = catekv::select_scratch_bytes();
+  if (need > have)
+    return fail(CATEKV_ERR_UNSUPPORTED,
+                "this selection needs %zu bytes of scratch; the allocation-free call holds %zu "
+                "(use catekv_select_critical with a workspace)", need, have);
+  void* ws = nullptr;
+  hipError_t e = catekv::select_scratch(&ws);
+  if (e != hipSuccess) return hip_fail(e, "select_critical_noalloc scratch address");
+  e = catekv::launch_select(dtype, g, q_obs, k, idx_out, ws, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "select_critical_noalloc launch");
+  return ok();
+}
+
 int catekv_compact_kv(int dtype, const void* k, const void* v, int hkv, int64_t n, int d, int cs,
                       int l_obs, const int32_t* sel_heads_host, int n_sel, const int32_t* idx, int b,
                       void* k_c, void* v_c, int64_t* lens_out, void* stream) {

@@ -86,6 +86,10 @@ struct SelectGeom {
 // Key columns per score workgroup for n_keys columns of n_heads KV heads.
 int64_t score_block_tokens(int64_t n_keys, int n_heads);
 size_t select_workspace_bytes(const SelectGeom& g);
+// The file-scope scratch of the allocation-free selection: its size, and its
+// device address on the current device.
+size_t select_scratch_bytes();
+hipError_t select_scratch(void** ptr);
 hipError_t launch_select(int dtype, const SelectGeom& g, const void* q_obs, const void* k,
                          int32_t* idx_out, void* ws, hipStream_t stream);
 hipError_t launch_compact(int dtype, const void* k, const void* v, int hkv, int64_t n, int cs,

@@ -17,6 +17,7 @@
 #include "internal.h"
 
 #include <algorithm>
+#include <mutex>
 #include <type_traits>
 
 namespace catekv {
@@ -1176,6 +1177,35 @@ static SelectLayout select_layout(const SelectGeom& g) {
 
 size_t select_workspace_bytes(const SelectGeom& g) { return select_layout(g).total; }
 
+// Scratch of catekv_select_critical_noalloc: a file-scope device array, so
+// the call allocates nothing.  Every GPU the library runs on holds its own
+// copy, at its own address, until the process ends.  In host code the
+// array's name is only a host-side stand-in: its device address comes from
+// hipGetSymbolAddress, taken once per device with that device current, and
+// only that address is handed to kernels.
+constexpr size_t kSelectScratchBytes = (size_t)16 << 20;
+static __device__ __align__(256) unsigned char scratch[kSelectScratchBytes];
+
+size_t select_scratch_bytes() { return kSelectScratchBytes; }
+
+hipError_t select_scratch(void** ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  return hipSuccess;
+}
 
 template <typename T, int MODE, int G, bool CAUSAL>
 static hipError_t launch_score_mt(int mt, dim3 grid, hipStream_t s, const ScoreArgs& a) {

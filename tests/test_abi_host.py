@@ -28,7 +28,7 @@ def declared_functions():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 16
+    assert len(names) == 17
     L = ck.lib()
     for n in names:
         assert hasattr(L, n), n
@@ -151,6 +151,20 @@ def test_select_rejects_bad_arguments():
     assert call(hq=30) == _lib.CATEKV_ERR_INVALID_ARG
     assert call(l_obs=200) == _lib.CATEKV_ERR_UNSUPPORTED     # 4 * 200 rows
     assert ck.select_workspace(32, 8, 64, 4096, 8, 2) > 0
+
+
+def test_select_noalloc_refuses_a_selection_beyond_its_scratch():
+    # cs = 12 does not divide the 64-column tile, so the per-key column mass
+    # is kept: 8 heads at 2^20 keys need more than the 16 MiB scratch
+    L = ck.lib()
+    assert ck.select_workspace(32, 8, 64, 1 << 20, 12, 8) > 16 << 20
+    heads = (ctypes.c_int32 * 8)(*range(8))
+    rc, msg = _status_and_msg(L.catekv_select_critical_noalloc(1, FAKE, FAKE, 32, 8, 64, 1 << 20, 128, 12, heads,
+                                                               8, 64, FAKE, None))
+    assert rc == _lib.CATEKV_ERR_UNSUPPORTED and "scratch" in msg
+    rc, _ = _status_and_msg(L.catekv_select_critical_noalloc(1, FAKE, FAKE, 32, 8, 64, 4096, 128, 8, heads, 8, 0,
+                                                             FAKE, None))
+    assert rc == _lib.CATEKV_ERR_INVALID_ARG                       # b = 0, as for the workspace call
 
 
 def test_compact_rejects_bad_arguments():
