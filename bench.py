@@ -41,7 +41,7 @@ TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "decode_traffic_ctx128k_bf16.md
 DECODE_SOURCES = ["paper_2608_30295_amd/csrc/decode.hip", "paper_2608_30295_amd/csrc/common.h",
                   "paper_2608_30295_amd/csrc/internal.h", "paper_2608_30295_amd/csrc/api.cpp"]
 COPY_PROBE_BYTES = 1 << 30
-DECODE_KERNELS = ("decode_stream_mfma_kernel", "decode_combine_kernel")
+DECODE_KERNELS = ("decode_stream_v2_kernel", "decode_stream_mfma_kernel", "decode_combine_kernel")
 COPY_KERNEL = "bitwise_not"
 
 # A serving loop replays one graph per generated token, holding the attention
@@ -206,6 +206,7 @@ def time_decode_shape(torch, ck, wl, dev, stream, steps):
     res = {"workload": wl.name, "batch": wl.batch, "consistent_heads_per_seq": n_cons,
            "kv_tokens": int(sum(sum(r) for r in vl)), "bytes_per_step": int(algo), "us_per_step": round(us, 2),
            "gbs": round(algo / (us * 1e-6) / 1e9, 1), "hbm_peak_frac": round(algo / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+           "kv_fraction_of_full": round(kv_bytes / (sum(lens_b) * hkv * d * 2 * 2), 4),
            "layer_copies": n_cp, "workgroups": int(plan.plan.n_workers)}
     if wl.batch > 1:
         res["tokens_per_s"] = round(wl.batch / (us * 1e-6), 1)
@@ -213,6 +214,27 @@ def time_decode_shape(torch, ck, wl, dev, stream, steps):
     del copies, g
     torch.cuda.empty_cache()
     return res
+
+
+def hbm_probes(torch, dev, stream, nbytes=1 << 30, reps=5):
+    """A streaming kernel of known traffic on the same GPU, in the same run: a
+    device-to-device copy that reads and writes nbytes (4x the 256 MB Infinity
+    Cache, so it streams from HBM)."""
+    x = torch.empty(nbytes // 2, dtype=torch.bfloat16, device=dev).normal_()
+    y = torch.empty_like(x)
+    y.copy_(x)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        y.copy_(x)
+    e1.record(stream)
+    e1.synchronize()
+    t_copy = e0.elapsed_time(e1) * 1e-3 / reps      # s
+    del x, y
+    torch.cuda.empty_cache()
+    return {"copy_gbs": round(2 * nbytes / t_copy / 1e9, 1), "bytes_each_way": nbytes,
+            "kernel": "torch copy_ of 1 GiB (reads and writes 1 GiB)"}
 
 
 def time_prefill_shape(torch, ck, wl, dev, stream):
@@ -274,7 +296,10 @@ def time_prefill_shape(torch, ck, wl, dev, stream):
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=100)
+    p.add_argument("--steps", type=int, default=100,
+                   help="decode steps to time; with HIP graphs (the default) whole graphs of at least 32 steps "
+                        "are replayed, so the timed count is --steps rounded to whole graphs, at least one "
+                        "(the JSON line reports the count timed)")
     p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--workload", default="ctx128k_bf16")
     p.add_argument("--layers", type=int, default=0, help="layer copies to rotate over (0: >= 1.2 GB of KV)")
@@ -508,6 +533,24 @@ def main():
     gbs = algo_bytes / (us * 1e-6) / 1e9
     log(f"[bench] decode {mode}: {us:.2f} us/step over {timed_steps} steps, {gbs:.1f} GB/s "
         f"({100 * gbs / HBM_PEAK_GBS:.1f}% of 8 TB/s), {n_layers} layer copies")
+
+    # per-step distribution: a second run of eager launches with an event between steps
+    n_ps = 100
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(n_ps + 1)]
+    torch.cuda.synchronize()
+    evs[0].record(stream)
+    for t in range(n_ps):
+        step(t)
+        evs[t + 1].record(stream)
+    evs[-1].synchronize()
+    per = np.array([evs[i].elapsed_time(evs[i + 1]) * 1e3 for i in range(n_ps)])
+    per_step = {"mean": round(float(per.mean()), 2), "p50": round(float(np.percentile(per, 50)), 2),
+                "p95": round(float(np.percentile(per, 95)), 2), "steps": n_ps,
+                "launch": "eager, an event recorded between consecutive steps"}
+    log(f"[bench] per-step (eager): mean {per_step['mean']} p50 {per_step['p50']} p95 {per_step['p95']} us")
+    probes = hbm_probes(torch, dev, stream)
+    log(f"[bench] streaming copy: {probes['copy_gbs']} GB/s; decode {gbs:.0f} GB/s = "
+        f"{100 * gbs / probes['copy_gbs']:.1f}% of it")
     if args.copy_probe:
         src = torch.empty(COPY_PROBE_BYTES // 2, dtype=torch.int16, device=dev)
         dst = torch.empty_like(src)
@@ -750,8 +793,11 @@ def main():
             "algorithmic_bytes_per_step": int(algo_bytes), "full_attention_bytes_per_step": int(full_bytes),
             "kv_fraction_of_full": round(kv_bytes_layer / (n * hkv * d * esz * 2), 4),
         },
+        "per_step_us": per_step,
+        "hbm_copy_probe": dict(probes, decode_frac_of_copy=round(gbs / probes["copy_gbs"], 4)),
         "roofline": {
-            "kernel": "decode step: decode_stream_mfma_kernel<G=4> + decode_combine_kernel<G=4>",
+            "kernel": f"decode step: {'decode_stream_v2_kernel' if pl.variant == 2 else 'decode_stream_mfma_kernel'}"
+                      f"<G={G}> + decode_combine_kernel<G={G}>",
             "bound": "hbm", "achieved": round(gbs, 2),
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
             "traffic": recorded_traffic(),
