@@ -281,7 +281,8 @@ def time_prefill_shape(torch, ck, wl, dev, stream):
     sel_flops = 2.0 * len(heads) * G * wl.l_obs * n_keys * d
     sel_bytes = len(heads) * n_keys * d * esz + 2 * len(heads) * cap * d * esz * 2
     roof = max(sel_flops / (BF16_MFMA_PEAK_TFLOPS * 1e12), sel_bytes / (HBM_PEAK_GBS * 1e9)) * 1e6
-    res = {"workload": wl.name, "consistent_heads": n_cons, "cv_rows": lq, "score_heads_us": round(t_cv, 1),
+    res = {"workload": wl.name, "hq": hq, "hkv": hkv, "consistent_heads": n_cons, "cv_rows": lq,
+           "score_heads_us": round(t_cv, 1),
            "select_critical_us": round(t_sel, 1), "compact_kv_us": round(t_cmp, 1),
            "select_roofline_us": round(roof, 1),
            "select_plus_compact_vs_roofline": round((t_sel + t_cmp) / roof, 3),
@@ -733,7 +734,11 @@ def main():
     if not args.no_workloads:
         other = [time_decode_shape(torch, ck, synth.WORKLOADS[name], dev, stream, args.steps)
                  for name in ("ctx32k_bf16", "batch16_ragged_bf16", "ctx1m_bf16")]
-        other_prefill = [time_prefill_shape(torch, ck, synth.WORKLOADS["ctx1m_bf16"], dev, stream)]
+        # the 1M prompt, and the 128K prompt with eight query heads per KV head
+        # (64 q / 8 KV heads: 512 observation rows per selected head)
+        g8 = synth.WORKLOADS["ctx128k_bf16"].scaled(name="ctx128k_g8_bf16", hq=64, hkv=8)
+        other_prefill = [time_prefill_shape(torch, ck, synth.WORKLOADS["ctx1m_bf16"], dev, stream),
+                         time_prefill_shape(torch, ck, g8, dev, stream)]
 
     # ---------------- CPU oracle on a bounded sample ----------------
     cpu = None

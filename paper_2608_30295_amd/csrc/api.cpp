@@ -222,7 +222,7 @@ catekv::SelectGeom select_geom(int hq, int hkv, int l_obs, int64_t n, int cs, co
   g.n = n;
   g.n_keys = n - l_obs;
   g.n_chunks = (g.n_keys + cs - 1) / cs;
-  g.cb_tokens = catekv::score_block_tokens(g.n_keys, n_sel);
+  g.cb_tokens = catekv::score_block_tokens(g.n_keys, n_sel, catekv::score_rows_pad(g.G * l_obs), device_cus());
   g.n_colblk = (int)((std::max<int64_t>(g.n_keys, 1) + g.cb_tokens - 1) / g.cb_tokens);
   for (int i = 0; i < n_sel && heads; ++i) g.heads[i] = heads[i];
   return g;
@@ -233,7 +233,7 @@ catekv::ScoreGeom score_geom(int hq, int hkv, int lq, int64_t n, int64_t l_init,
   g.hq = hq; g.hkv = hkv; g.G = hkv > 0 ? hq / hkv : 1; g.lq = lq; g.n = n;
   g.l_init = l_init; g.l_rec = l_rec;
   g.n_keys = n - l_init - l_rec;
-  g.cb_tokens = catekv::score_block_tokens(g.n_keys, hkv);
+  g.cb_tokens = catekv::score_block_tokens(g.n_keys, hkv, catekv::score_rows_pad(g.G * lq), device_cus());
   g.n_colblk = (int)((std::max<int64_t>(g.n_keys, 1) + g.cb_tokens - 1) / g.cb_tokens);
   return g;
 }

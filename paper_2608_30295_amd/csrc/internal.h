@@ -83,8 +83,20 @@ struct SelectGeom {
   int heads[128];
 };
 
-// Key columns per score workgroup for n_keys columns of n_heads KV heads.
-int64_t score_block_tokens(int64_t n_keys, int n_heads);
+// Query rows of the score passes, padded to a whole number of 16-row tiles
+// per wave: 64, 128, 256 or 512.
+inline int score_rows_pad(int rows) {
+  const int mt = (rows + 63) / 64;
+  return (mt <= 1 ? 1 : mt <= 2 ? 2 : mt <= 4 ? 4 : 8) * 64;
+}
+// Waves per score workgroup: 4, or 8 where four waves would each hold more
+// than four 16-row tiles of bf16 Q fragments (two of fp32).
+inline int score_waves(int dtype, int rows_pad) { return rows_pad > (dtype == CATEKV_F32 ? 128 : 256) ? 8 : 4; }
+// Key columns per score workgroup for n_keys columns of n_heads KV heads and
+// rows_pad query rows on a device of n_cu compute units; at most
+// kMaxBlockTokens (the kernels address a block's K rows with 32-bit offsets).
+constexpr int64_t kMaxBlockTokens = (int64_t)1 << 22;
+int64_t score_block_tokens(int64_t n_keys, int n_heads, int rows_pad, int n_cu);
 size_t select_workspace_bytes(const SelectGeom& g);
 // The file-scope scratch of the allocation-free selection: its size, and its
 // device address on the current device.
@@ -96,8 +108,6 @@ hipError_t launch_compact(int dtype, const void* k, const void* v, int hkv, int6
                           int l_obs, const int32_t* heads, int n_sel, const int32_t* idx, int b,
                           void* k_c, void* v_c, int64_t* lens_out, hipStream_t stream);
 
-// Indices of the b largest of each row of S [n_rows][n] (ties to the lower
-// index), ascending, -1 padded to b.
 // Indices of the min(b, n) largest of each row of S [n_rows][n] (ties to the
 // lower index), ascending, -1 padded to b.  ws: topk_workspace_bytes() bytes
 // (rows longer than 32768 scores are reduced slice by slice through it).

@@ -1,392 +1,14 @@
-// Prefill-time kernels of CateKV: critical-token selection (Algorithm 1,
-// pre-filling stage), compaction (Cache(K, V, i_k, L_obs)) and CV head
-// scoring (Section 3.2, Eq. 1-4).
-//
-// Both the selection and the CV score need softmax rows over a long key
-// range for the G * L query rows of one KV head (the GQA group mean of
-// Section 3.2).  The rows are short (64-512) and the key range long, so the
-// score block Q K^T is produced tile by tile with MFMA and never stored:
-//   pass 1  per row: running max m and sum l of exp(s - m)   (row statistics)
-//   merge   per row: offset = m * log2(e) / sqrt(d) + log2(l)
-//   pass 2  p = exp2(s * log2(e) / sqrt(d) - offset), then either the column
-//           mass C_j = (1/G) sum_rows p (selection) or the group-mean
-//           observation matrix A[i][j] (CV).
-// Workgroup = 4 waves sharing one 64-token K tile staged in LDS; wave w owns
-// rows [w * MT * 16, (w + 1) * MT * 16) with their Q fragments in registers.
-#include "common.h"
-#include "internal.h"
+// Prefill-time kernels of CateKV around the score passes (score.h):
+// critical-token selection (Algorithm 1, pre-filling stage) -- row-statistics
+// merge, BlockMax, top-k -- compaction (Cache(K, V, i_k, L_obs)) and the CV
+// head score (Section 3.2, Eq. 1-4) over the observation matrix.
+#include "score.h"
 
 #include <algorithm>
 #include <mutex>
 #include <type_traits>
 
 namespace catekv {
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float floatx4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) void lds_void;
-
-constexpr int kTileTok = 64;     // tokens per LDS tile (4 MFMA column tiles)
-constexpr int kSWaves = 4;       // waves per score workgroup
-constexpr float kMInit = -1e30f; // finite "minus infinity" for running maxima
-
-// MFMA fragment traits.  In k-group kg a lane holds 16 bytes of its row:
-// byte offset kg * 64 + (lane / 16) * 16, i.e. 16-byte segment kg * 4 + lane / 16.
-// The contraction runs over the head dimension, so any dim permutation that is
-// the same for Q and K gives the same dot products.
-template <typename T> struct Frag;
-template <> struct Frag<uint16_t> {
-  static constexpr int KG = 4;   // 4 x (16 x 16 x 32) per 128 dims
-  static constexpr int SEG = 16; // 16-byte segments per row
-  __device__ static __forceinline__ floatx4 mma(uint4 a, uint4 b, floatx4 acc) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
-                                                   __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
-  }
-};
-template <> struct Frag<float> {
-  static constexpr int KG = 8;   // 8 x 4 x (16 x 16 x 4) per 128 dims
-  static constexpr int SEG = 32;
-  __device__ static __forceinline__ floatx4 mma(uint4 a, uint4 b, floatx4 acc) {
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
-    return acc;
-  }
-};
-
-// XOR-swizzled slot of (token, segment) in the LDS tile: 16 consecutive
-// tokens reading the same segment hit 16 distinct bank groups.
-template <typename T>
-__device__ __forceinline__ int tile_slot(int tok, int seg) {
-  return tok * Frag<T>::SEG + (seg ^ (tok & 15));
-}
-
-enum ScoreMode { kRowStats = 0, kColMass = 1, kObsMatrix = 2 };
-
-struct ScoreArgs {
-  const void* q;          // [hq][lq][d]
-  const void* k;          // [hkv][n][d]
-  int hkv, lq, G, R;      // R = G * lq rows per KV head
-  int64_t n;
-  int64_t key_off;        // absolute position of key column 0
-  int64_t n_keys;         // key columns
-  int64_t cb_tokens;      // key columns per workgroup
-  int n_colblk;
-  int64_t q_pos0;         // absolute position of query row i = 0 (causal mask)
-  float c;                // log2(e) / sqrt(d)
-  int32_t heads[128];     // KV head per blockIdx.y
-  float2* rowpart;        // kRowStats out: [n_sel][n_colblk][R_pad] (max * c, sum)
-  const float* rowoff;    // kColMass / kObsMatrix in: [n_sel][R_pad]
-  float* colmass;         // kColMass out: [n_sel][n_keys] (when cs_fused == 0)
-  float* chunks;          // kColMass out: [n_sel][n_chunks] chunk maxima (when cs_fused > 0)
-  int cs_fused;           // chunk size when it divides the 64-column tile, else 0
-  int64_t n_chunks;
-  float* obs;             // kObsMatrix out: [n_sel][lq][n_keys]
-};
-
-template <typename T, int MT, int MODE, int G, bool CAUSAL>
-__device__ __forceinline__ void score_body(const ScoreArgs& a) {
-  using F = Frag<T>;
-  constexpr int KG = F::KG, SEG = F::SEG;
-  constexpr int RPAD = kSWaves * MT * 16;
-  constexpr int NSTAGE = kTileTok * SEG / (kSWaves * 64);   // 16-byte loads per thread per tile
-  constexpr int NRING = sizeof(T) == 2 ? 4 : 2;               // LDS stages (16 KB bf16, 32 KB fp32 each)
-  // s_waitcnt immediate: vmcnt <= NSTAGE * (NRING - 2), expcnt not waited on;
-  // lgkmcnt(0) in column-mass mode, whose column partials in LDS the barrier publishes
-  constexpr int VM = NSTAGE * (NRING - 2);
-  constexpr int LGKM = MODE == kColMass ? 0 : 0xF;
-  constexpr int kWaitRing = (VM & 0xF) | ((VM >> 4) << 14) | (0x7 << 4) | (LGKM << 8);
-  // one LDS array per ring stage: stages chosen at compile time do not alias,
-  // so the compiler adds no waits of its own between the loads and the reads
-  __shared__ uint4 s_r0[kTileTok * SEG], s_r1[kTileTok * SEG], s_r2[kTileTok * SEG], s_r3[kTileTok * SEG];
-  __shared__ float s_col[2][kSWaves][kTileTok];   // per-wave column partials, by tile parity
-
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int sel = blockIdx.y, cb = blockIdx.x;
-  const int h = a.heads[sel];
-  const int64_t col0 = (int64_t)cb * a.cb_tokens;                   // first key column
-  const int64_t col_end = min(col0 + a.cb_tokens, a.n_keys);
-  const int n_tiles = (int)((col_end - col0 + kTileTok - 1) / kTileTok);
-  const T* kh = reinterpret_cast<const T*>(a.k) + (size_t)h * a.n * kD;
-  const T* qb = reinterpret_cast<const T*>(a.q);
-
-  // Q fragments: wave-local M tile mt, lane row (lane & 15), segment kg*4 + lane/16
-  uint4 qf[MT][KG];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    const int row = (wave * MT + mt) * 16 + (lane & 15);
-    const bool ok = row < a.R;
-    const int i = row / G, g = row - (row / G) * G;
-    const T* qrow = qb + ((size_t)(h * G + g) * a.lq + (ok ? i : 0)) * kD;
-#pragma unroll
-    for (int kg = 0; kg < KG; ++kg) {
-      uint4 v = ld16(reinterpret_cast<const char*>(qrow) + (kg * 4 + (lane >> 4)) * 16);
-      qf[mt][kg] = ok ? v : make_uint4(0, 0, 0, 0);
-    }
-  }
-
-  // rows owned by this lane's accumulator registers: (mt, r) -> row
-  float st_mc[MT][4], st_l[MT][4];   // kRowStats: running max in log2 units (max * c), sum
-  float off[MT][4];                                // kColMass / kObsMatrix
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      st_mc[mt][r] = kMInit;
-      st_l[mt][r] = 0.f;
-      off[mt][r] = 0.f;
-      if (MODE != kRowStats) {
-        const int row = (wave * MT + mt) * 16 + 4 * (lane >> 4) + r;
-        off[mt][r] = a.rowoff[(size_t)sel * RPAD + row];
-      }
-    }
-
-  // K tiles arrive through a ring of NRING LDS stages filled by direct
-  // global-to-LDS loads (no staging registers).  Thread x's load i lands in
-  // slot i * 256 + x; the slot's (token, position) picks which 16-byte
-  // segment of which row it fetches, so the ring holds the XOR-swizzled
-  // layout that tile_slot() reads.
-  const int full_tiles = (int)((col_end - col0) / kTileTok);   // tiles with no column past the end
-  const char* kbase = reinterpret_cast<const char*>(kh + (size_t)(a.key_off + col0) * kD);
-  int src_off[NSTAGE];   // byte offset of each of this thread's loads inside a tile
-#pragma unroll
-  for (int i = 0; i < NSTAGE; ++i) {
-    const int slot = i * kSWaves * 64 + threadIdx.x;
-    const int tok = slot / SEG, pos = slot - (slot / SEG) * SEG;
-    src_off[i] = tok * (kD * (int)sizeof(T)) + (pos ^ (tok & 15)) * 16;
-  }
-  auto issue = [&](uint4* stage, int tile) {
-    if (tile < full_tiles) {
-      const char* tb = kbase + (size_t)tile * (kTileTok * kD * sizeof(T));
-#pragma unroll
-      for (int i = 0; i < NSTAGE; ++i)
-        __builtin_amdgcn_global_load_lds(tb + src_off[i], (lds_void*)&stage[i * kSWaves * 64 + wave * 64], 16, 0, 0);
-    } else {
-#pragma unroll
-      for (int i = 0; i < NSTAGE; ++i) {
-        const int slot = i * kSWaves * 64 + threadIdx.x;
-        const int tok = slot / SEG;
-        int64_t col = (int64_t)tile * kTileTok + tok;
-        // rows past the end (and tiles past the last) re-read row 0 of the block
-        const int64_t rowoff = col < col_end - col0 ? col * (kD * (int64_t)sizeof(T)) : 0;
-        __builtin_amdgcn_global_load_lds(kbase + rowoff + (src_off[i] - tok * (kD * (int)sizeof(T))),
-                                         (lds_void*)&stage[i * kSWaves * 64 + wave * 64], 16, 0, 0);
-      }
-    }
-  };
-  auto ring = [&](int k) -> uint4* { return k == 0 ? s_r0 : k == 1 ? s_r1 : k == 2 ? s_r2 : s_r3; };
-
-  // Column mass of tile t: the four waves' partials are summed by one wave
-  // (t mod 4) during tile t + 1, after the barrier that published them, so no
-  // wave waits for this step and no barrier of its own is needed.  With cs
-  // dividing 64 a chunk never straddles a tile and BlockMax is taken here.
-  auto finish_cols = [&](int t) {
-    const int p = t & 1;
-    float v = 0.f;
-#pragma unroll
-    for (int w = 0; w < kSWaves; ++w) v += s_col[p][w][lane];
-    v *= 1.0f / (float)G;
-    const int64_t col = col0 + (int64_t)t * kTileTok + lane;
-    if (a.cs_fused > 0) {
-      const float mx = max_in_group(col < col_end ? v : -INFINITY, a.cs_fused);
-      if ((lane & (a.cs_fused - 1)) == 0 && col < col_end)
-        a.chunks[(size_t)sel * a.n_chunks + col / a.cs_fused] = mx;
-    } else if (col < col_end) {
-      a.colmass[(size_t)sel * a.n_keys + col] = v;
-    }
-  };
-#pragma unroll
-  for (int t = 0; t < NRING - 1; ++t) issue(ring(t), t);
-
-  const int64_t qpos_min = a.q_pos0;   // position of query row 0: the smallest row position
-  for (int base = 0; base < n_tiles; base += NRING) {
-#pragma unroll
-  for (int u = 0; u < NRING; ++u) {
-    const int tile = base + u;
-    if (tile >= n_tiles) break;
-    uint4* cur = ring(u);
-    const int par = tile & 1;
-    // this tile's loads are done once at most NRING - 2 later groups are outstanding
-    // (vector memory operations retire in order); the barrier makes every wave's
-    // part of the tile visible and frees the stage the next issue overwrites
-    compiler_fence();
-    __builtin_amdgcn_s_waitcnt(kWaitRing);
-    __builtin_amdgcn_s_barrier();
-    compiler_fence();
-    issue(ring((u + NRING - 1) % NRING), tile + NRING - 1);
-    if (MODE == kColMass && tile > 0 && wave == ((tile - 1) & (kSWaves - 1))) finish_cols(tile - 1);
-    const int64_t tcol0 = col0 + (int64_t)tile * kTileTok;
-    float cmass[4] = {0.f, 0.f, 0.f, 0.f};
-
-    // one tile: the whole 64-column score block of this wave first (MFMA), then
-    // the softmax arithmetic on it (VALU); without branches inside, the
-    // scheduler overlaps the two.  Masks are needed only on a ragged last tile
-    // or where keys can lie past a row's position.
-    auto tile_body = [&](auto mask_tag) {
-      constexpr bool MASK = decltype(mask_tag)::value;
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh) {
-      floatx4 acc[2][MT];
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        uint4 bf[KG];
-#pragma unroll
-        for (int kg = 0; kg < KG; ++kg) bf[kg] = cur[tile_slot<T>((2 * hh + j) * 16 + (lane & 15), kg * 4 + (lane >> 4))];
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          floatx4 x = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-          for (int kg = 0; kg < KG; ++kg) x = F::mma(qf[mt][kg], bf[kg], x);
-          acc[j][mt] = x;
-        }
-      }
-      // from a tile's first softmax block to its end the wave runs at raised
-      // priority (reset before the next tile): measured ~1.5% per pass with
-      // two waves sharing a SIMD
-      __builtin_amdgcn_s_setprio(1);
-      if (MASK) {
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int64_t col = tcol0 + (2 * hh + j) * 16 + (lane & 15);
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const int row = (wave * MT + mt) * 16 + 4 * (lane >> 4) + r;
-              bool ok = col < col_end;
-              if (CAUSAL) ok = ok && (a.key_off + col <= a.q_pos0 + row / G);
-              acc[j][mt][r] = ok ? acc[j][mt][r] : -INFINITY;
-            }
-        }
-      }
-
-      if (MODE == kRowStats) {
-        // lazy running maximum: the pair's terms are taken against the current
-        // maximum, which moves (to the pair's maximum) only when a term would
-        // exceed 2^64 -- on a row's first scores (the maximum starts at
-        // kMInit) or a score 64 log2 units above it; sums stay below 2^82,
-        // and one compare per pair replaces a maximum search
-        float part[MT][4];
-        bool upd = false;
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            part[mt][r] = fast_exp2(__builtin_fmaf(acc[0][mt][r], a.c, -st_mc[mt][r])) +
-                          fast_exp2(__builtin_fmaf(acc[1][mt][r], a.c, -st_mc[mt][r]));
-            upd |= !(part[mt][r] <= 0x1p64f);
-          }
-        if (__builtin_amdgcn_ballot_w64(upd)) {
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-              if (!(part[mt][r] <= 0x1p64f)) {
-                const float tmc = fmaxf(acc[0][mt][r], acc[1][mt][r]) * a.c;
-                st_l[mt][r] *= fast_exp2(st_mc[mt][r] - tmc);
-                st_mc[mt][r] = tmc;
-                part[mt][r] = fast_exp2(__builtin_fmaf(acc[0][mt][r], a.c, -tmc)) +
-                              fast_exp2(__builtin_fmaf(acc[1][mt][r], a.c, -tmc));
-              }
-        }
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) st_l[mt][r] += part[mt][r];
-      } else if (MODE == kColMass) {
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-              cmass[2 * hh + j] += fast_exp2(__builtin_fmaf(acc[j][mt][r], a.c, -off[mt][r]));
-      } else {  // kObsMatrix: group mean over the G rows of each query i
-        const float invG = 1.0f / (float)G;
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int64_t col = tcol0 + (2 * hh + j) * 16 + (lane & 15);
-          const bool colok = col < col_end;
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt) {
-            float p[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) p[r] = fast_exp2(__builtin_fmaf(acc[j][mt][r], a.c, -off[mt][r]));
-            const int rbase = (wave * MT + mt) * 16 + 4 * (lane >> 4);
-            if (G == 1 || G == 2 || G == 4) {
-#pragma unroll
-              for (int r0 = 0; r0 < 4; r0 += G) {
-                const int i = (rbase + r0) / G;
-                float v = 0.f;
-#pragma unroll
-                for (int r = 0; r < G; ++r) v += p[r0 + r];
-                if (i < a.lq && colok) a.obs[((size_t)sel * a.lq + i) * a.n_keys + col] = v * invG;
-              }
-            } else {  // G == 8: the 8 rows of a query span lane groups 2k and 2k + 1
-              const float v = add_xor16(p[0] + p[1] + p[2] + p[3]);
-              const int i = rbase / 8;
-              if (((lane >> 4) & 1) == 0 && i < a.lq && colok)
-                a.obs[((size_t)sel * a.lq + i) * a.n_keys + col] = v * invG;
-            }
-          }
-        }
-      }
-      }
-    };
-
-    __builtin_amdgcn_s_setprio(0);
-    const bool need_mask = tcol0 + kTileTok > col_end || (CAUSAL && a.key_off + tcol0 + kTileTok - 1 > qpos_min);
-    if (need_mask) tile_body(std::true_type{});
-    else tile_body(std::false_type{});
-
-    if (MODE == kColMass) {
-      // sum over the four row groups of lanes; each wave leaves its partial in LDS
-#pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        const float v = add_xor32(add_xor16(cmass[nt]));
-        if (lane < 16) s_col[par][wave][nt * 16 + lane] = v;
-      }
-    }
-  }
-  }
-
-  if (MODE == kColMass) {
-    barrier_lds_only();
-    if (n_tiles > 0 && wave == ((n_tiles - 1) & (kSWaves - 1))) finish_cols(n_tiles - 1);
-  }
-
-  // the ring's trailing loads must land before the workgroup's LDS is released
-  __builtin_amdgcn_s_waitcnt(0);
-  compiler_fence();
-
-  if (MODE == kRowStats) {
-    // merge the 16 lanes that share each row (maxima in log2 units)
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float m = st_mc[mt][r];
-        const float M = max16(m);
-        const float lsum = sum16(st_l[mt][r] * fast_exp2(m - M));
-        const int row = (wave * MT + mt) * 16 + 4 * (lane >> 4) + r;
-        if ((lane & 15) == 0)
-          a.rowpart[((size_t)sel * a.n_colblk + cb) * RPAD + row] = make_float2(M, lsum);
-      }
-  }
-}
-
-// Up to 256 query rows the body fits two waves per SIMD; 512 rows (MT = 8)
-// keep the compiler's own register budget rather than spill.
-template <typename T, int MT, int MODE, int G, bool CAUSAL>
-__global__ __launch_bounds__(kSWaves * 64) __attribute__((amdgpu_waves_per_eu(2)))
-void score_kernel(ScoreArgs a) {
-  score_body<T, MT, MODE, G, CAUSAL>(a);
-}
-template <typename T, int MODE, int G, bool CAUSAL>
-__global__ __launch_bounds__(kSWaves * 64) void score_kernel_wide(ScoreArgs a) {
-  score_body<T, 8, MODE, G, CAUSAL>(a);
-}
 
 // Merge the per-column-block row statistics: offset = m c + log2(l), +inf
 // for rows with no visible key and for padding rows.  16 lanes share a row
@@ -1141,20 +763,18 @@ __global__ void cv_final_kernel(const CvState* __restrict__ st, int64_t n_keys, 
 // ---------------------------------------------------------------------------
 
 static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
-static inline int rows_pad(int R) {
-  const int mt = (R + 63) / 64;
-  return (mt <= 1 ? 1 : mt <= 2 ? 2 : mt <= 4 ? 4 : 8) * 64;
-}
-// Score workgroups run in a single round: at most kScoreSlots of them (two per
-// compute unit, the residency their registers and LDS allow), each over whole
-// 64-column tiles and at least four of them.
-constexpr int64_t kScoreSlots = 512;
-
-int64_t score_block_tokens(int64_t n_keys, int n_heads) {
-  const int64_t per_head = std::max<int64_t>(1, kScoreSlots / std::max(1, n_heads));
+// Score workgroups run in a single round: as many as the device holds at once
+// (two waves per SIMD: two 4-wave workgroups or one 8-wave workgroup per
+// compute unit, the bf16 residency; fp32 at 256 rows runs in two rounds),
+// each over whole 64-column tiles, at least four and at most kMaxBlockTokens
+// columns (more rounds beyond).  The count
+// depends on the rows but not on the dtype, so workspace sizes do not either.
+int64_t score_block_tokens(int64_t n_keys, int n_heads, int rows_pad, int n_cu) {
+  const int64_t slots = (int64_t)std::max(1, n_cu) * (8 / score_waves(CATEKV_BF16, rows_pad));
+  const int64_t per_head = std::max<int64_t>(1, slots / std::max(1, n_heads));
   int64_t cb = (std::max<int64_t>(n_keys, 1) + per_head - 1) / per_head;
   cb = (cb + kTileTok - 1) / kTileTok * kTileTok;
-  return std::max<int64_t>(cb, 4 * kTileTok);
+  return std::min<int64_t>(std::max<int64_t>(cb, 4 * kTileTok), kMaxBlockTokens);
 }
 
 struct SelectLayout {
@@ -1162,7 +782,7 @@ struct SelectLayout {
 };
 static SelectLayout select_layout(const SelectGeom& g) {
   SelectLayout L{};
-  const int rp = rows_pad(g.G * g.l_obs);
+  const int rp = score_rows_pad(g.G * g.l_obs);
   size_t o = 0;
   L.rowpart = o; o += align256((size_t)g.n_sel * g.n_colblk * rp * sizeof(float2));
   L.rowoff = o; o += align256((size_t)g.n_sel * rp * sizeof(float));
@@ -1207,38 +827,12 @@ hipError_t select_scratch(void** ptr) {
   return hipSuccess;
 }
 
-template <typename T, int MODE, int G, bool CAUSAL>
-static hipError_t launch_score_mt(int mt, dim3 grid, hipStream_t s, const ScoreArgs& a) {
-  switch (mt) {
-    case 1: hipLaunchKernelGGL((score_kernel<T, 1, MODE, G, CAUSAL>), grid, dim3(kSWaves * 64), 0, s, a); break;
-    case 2: hipLaunchKernelGGL((score_kernel<T, 2, MODE, G, CAUSAL>), grid, dim3(kSWaves * 64), 0, s, a); break;
-    case 4: hipLaunchKernelGGL((score_kernel<T, 4, MODE, G, CAUSAL>), grid, dim3(kSWaves * 64), 0, s, a); break;
-    case 8: hipLaunchKernelGGL((score_kernel_wide<T, MODE, G, CAUSAL>), grid, dim3(kSWaves * 64), 0, s, a); break;
-    default: return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
-}
-
-template <int MODE, bool CAUSAL>
-static hipError_t launch_score_any(int dtype, int G, int mt, dim3 grid, hipStream_t s, const ScoreArgs& a) {
-#define CATEKV_SC(T, GG) \
-  if (G == GG) return launch_score_mt<T, MODE, GG, CAUSAL>(mt, grid, s, a);
-  if (dtype == CATEKV_BF16) {
-    CATEKV_SC(uint16_t, 1) CATEKV_SC(uint16_t, 2) CATEKV_SC(uint16_t, 4) CATEKV_SC(uint16_t, 8)
-  } else {
-    CATEKV_SC(float, 1) CATEKV_SC(float, 2) CATEKV_SC(float, 4) CATEKV_SC(float, 8)
-  }
-#undef CATEKV_SC
-  return hipErrorInvalidValue;
-}
-
 hipError_t launch_select(int dtype, const SelectGeom& g, const void* q_obs, const void* k,
                          int32_t* idx_out, void* ws, hipStream_t stream) {
   const SelectLayout L = select_layout(g);
   char* w = reinterpret_cast<char*>(ws);
   const int R = g.G * g.l_obs;
-  const int rp = rows_pad(R);
-  const int mt = rp / 64;
+  const int rp = score_rows_pad(R);
   ScoreArgs a{};
   a.q = q_obs; a.k = k; a.hkv = g.hkv; a.lq = g.l_obs; a.G = g.G; a.R = R; a.n = g.n;
   a.key_off = 0; a.n_keys = g.n_keys; a.cb_tokens = g.cb_tokens; a.n_colblk = g.n_colblk;
@@ -1248,7 +842,7 @@ hipError_t launch_select(int dtype, const SelectGeom& g, const void* q_obs, cons
   a.rowoff = reinterpret_cast<const float*>(w + L.rowoff);
   a.colmass = reinterpret_cast<float*>(w + L.colmass);
   const dim3 grid(g.n_colblk, g.n_sel);
-  hipError_t e = launch_score_any<kRowStats, false>(dtype, g.G, mt, grid, stream, a);
+  hipError_t e = launch_score_rowstats(dtype, g.G, false, rp, grid, stream, a);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(rowstats_merge_kernel, dim3((rp + kMergeRows - 1) / kMergeRows, g.n_sel), dim3(256), 0, stream,
                      a.rowpart, g.n_colblk, R, rp, reinterpret_cast<float*>(w + L.rowoff));
@@ -1256,7 +850,7 @@ hipError_t launch_select(int dtype, const SelectGeom& g, const void* q_obs, cons
   a.chunks = S;
   a.n_chunks = g.n_chunks;
   a.cs_fused = (kTileTok % g.cs == 0) ? g.cs : 0;
-  e = launch_score_any<kColMass, false>(dtype, g.G, mt, grid, stream, a);
+  e = launch_score_colmass(dtype, rp, grid, stream, a);
   if (e != hipSuccess) return e;
   if (!a.cs_fused)
     hipLaunchKernelGGL(chunk_max_kernel, dim3((unsigned)((g.n_chunks + 255) / 256), g.n_sel), dim3(256), 0,
@@ -1363,7 +957,7 @@ static uint32_t cand_cap(const ScoreGeom& g) {
 }
 static ScoreLayout score_layout(const ScoreGeom& g) {
   ScoreLayout L{};
-  const int rp = rows_pad(g.G * g.lq);
+  const int rp = score_rows_pad(g.G * g.lq);
   size_t o = 0;
   L.rowpart = o; o += align256((size_t)g.hkv * g.n_colblk * rp * sizeof(float2));
   L.rowoff = o; o += align256((size_t)g.hkv * rp * sizeof(float));
@@ -1382,8 +976,7 @@ hipError_t launch_score(int dtype, const ScoreGeom& g, const void* q_rows, const
   const ScoreLayout L = score_layout(g);
   char* w = reinterpret_cast<char*>(ws);
   const int R = g.G * g.lq;
-  const int rp = rows_pad(R);
-  const int mt = rp / 64;
+  const int rp = score_rows_pad(R);
   ScoreArgs a{};
   a.q = q_rows; a.k = k; a.hkv = g.hkv; a.lq = g.lq; a.G = g.G; a.R = R; a.n = g.n;
   a.key_off = g.l_init; a.n_keys = g.n_keys; a.cb_tokens = g.cb_tokens; a.n_colblk = g.n_colblk;
@@ -1393,13 +986,11 @@ hipError_t launch_score(int dtype, const ScoreGeom& g, const void* q_rows, const
   a.rowoff = reinterpret_cast<const float*>(w + L.rowoff);
   a.obs = reinterpret_cast<float*>(w + L.obs);
   const dim3 grid(g.n_colblk, g.hkv);
-  hipError_t e = g.causal ? launch_score_any<kRowStats, true>(dtype, g.G, mt, grid, stream, a)
-                          : launch_score_any<kRowStats, false>(dtype, g.G, mt, grid, stream, a);
+  hipError_t e = launch_score_rowstats(dtype, g.G, g.causal, rp, grid, stream, a);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(rowstats_merge_kernel, dim3((rp + kMergeRows - 1) / kMergeRows, g.hkv), dim3(256), 0, stream,
                      a.rowpart, g.n_colblk, R, rp, reinterpret_cast<float*>(w + L.rowoff));
-  e = g.causal ? launch_score_any<kObsMatrix, true>(dtype, g.G, mt, grid, stream, a)
-               : launch_score_any<kObsMatrix, false>(dtype, g.G, mt, grid, stream, a);
+  e = launch_score_obs(dtype, g.G, g.causal, rp, grid, stream, a);
   if (e != hipSuccess) return e;
 
   const int64_t N = (int64_t)g.lq * g.n_keys;

@@ -1,0 +1,491 @@
+// Score passes of the prefill kernels (Algorithm 1, pre-filling stage, and
+// the observation matrix of Section 3.2): the softmax rows of the G * L query
+// rows of one KV head over a long key range, tile by tile with MFMA, never
+// storing the score block:
+//   pass 1  per row: maximum m and sum l of exp(s - m)   (row statistics)
+//   merge   per row: offset = m * log2(e) / sqrt(d) + log2(l)
+//   pass 2  p = exp2(s * log2(e) / sqrt(d) - offset), then either the column
+//           mass C_j = (1/G) sum_rows p (selection) or the group-mean
+//           observation matrix A[i][j] (CV).
+// Workgroup = 4 waves sharing one 64-token K tile staged in LDS; wave w owns
+// rows [w * MT * 16, (w + 1) * MT * 16) with their Q fragments in registers.
+// Each pass is instantiated in a source file of its own (score_*.hip).
+#pragma once
+
+#include "common.h"
+#include "internal.h"
+
+#include <type_traits>
+
+namespace catekv {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+
+constexpr int kTileTok = 64;     // tokens per LDS tile (4 MFMA column tiles)
+constexpr float kMInit = -1e30f; // finite "minus infinity" for running maxima
+
+// MFMA fragment traits.  In k-group kg a lane holds 16 bytes of its row:
+// byte offset kg * 64 + (lane / 16) * 16, i.e. 16-byte segment kg * 4 + lane / 16.
+// The contraction runs over the head dimension, so any dim permutation that is
+// the same for Q and K gives the same dot products.
+template <typename T> struct Frag;
+template <> struct Frag<uint16_t> {
+  static constexpr int KG = 4;   // 4 x (16 x 16 x 32) per 128 dims
+  static constexpr int SEG = 16; // 16-byte segments per row
+  __device__ static __forceinline__ floatx4 mma(uint4 a, uint4 b, floatx4 acc) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
+  }
+};
+template <> struct Frag<float> {
+  static constexpr int KG = 8;   // 8 x 4 x (16 x 16 x 4) per 128 dims
+  static constexpr int SEG = 32;
+  __device__ static __forceinline__ floatx4 mma(uint4 a, uint4 b, floatx4 acc) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
+    return acc;
+  }
+};
+
+// XOR-swizzled slot of (token, segment) in the LDS tile: 16 consecutive
+// tokens reading the same segment hit 16 distinct bank groups.
+template <typename T>
+__device__ __forceinline__ int tile_slot(int tok, int seg) {
+  return tok * Frag<T>::SEG + (seg ^ (tok & 15));
+}
+
+enum ScoreMode { kRowStats = 0, kColMass = 1, kObsMatrix = 2 };
+enum RowStatsVar { kRsSum = 0, kRsMax = 1 };
+
+struct ScoreArgs {
+  const void* q;          // [hq][lq][d]
+  const void* k;          // [hkv][n][d]
+  int hkv, lq, G, R;      // R = G * lq rows per KV head
+  int64_t n;
+  int64_t key_off;        // absolute position of key column 0
+  int64_t n_keys;         // key columns
+  int64_t cb_tokens;      // key columns per workgroup
+  int n_colblk;
+  int64_t q_pos0;         // absolute position of query row i = 0 (causal mask)
+  float c;                // log2(e) / sqrt(d)
+  int32_t heads[128];     // KV head per blockIdx.y
+  float2* rowpart;        // kRowStats out: [n_sel][n_colblk][R_pad] (max * c, sum)
+  const float* rowoff;    // kColMass / kObsMatrix in: [n_sel][R_pad]
+  float* colmass;         // kColMass out: [n_sel][n_keys] (when cs_fused == 0)
+  float* chunks;          // kColMass out: [n_sel][n_chunks] chunk maxima (when cs_fused > 0)
+  int cs_fused;           // chunk size when it divides the 64-column tile, else 0
+  int64_t n_chunks;
+  float* obs;             // kObsMatrix out: [n_sel][lq][n_keys]
+};
+
+template <typename T, int W, int MT, int MODE, int G, bool CAUSAL>
+__device__ __forceinline__ void score_body(const ScoreArgs& a) {
+  using F = Frag<T>;
+  constexpr int KG = F::KG, SEG = F::SEG;
+  // G = 0: the group size is taken at run time (a.G); only the passes whose
+  // arithmetic never splits a group's rows (row statistics without a causal
+  // mask, column mass) are built that way
+  static_assert(G > 0 || (!CAUSAL && MODE != kObsMatrix), "G must be fixed for masks and the group mean");
+  const int GR = G > 0 ? G : a.G;
+  constexpr int RPAD = W * MT * 16;
+  constexpr int NSTAGE = kTileTok * SEG / (W * 64);   // 16-byte loads per thread per tile
+  constexpr int NRING = sizeof(T) == 2 ? 4 : 2;               // LDS stages (16 KB bf16, 32 KB fp32 each)
+  // s_waitcnt immediate: vmcnt <= NSTAGE * (NRING - 2), expcnt not waited on;
+  // lgkmcnt(0) in column-mass mode, whose column partials in LDS the barrier publishes
+  constexpr int VM = NSTAGE * (NRING - 2);
+  constexpr int LGKM = MODE == kColMass ? 0 : 0xF;
+  constexpr int kWaitRing = (VM & 0xF) | ((VM >> 4) << 14) | (0x7 << 4) | (LGKM << 8);
+  // one LDS array per ring stage: stages chosen at compile time do not alias,
+  // so the compiler adds no waits of its own between the loads and the reads
+  __shared__ uint4 s_r0[kTileTok * SEG], s_r1[kTileTok * SEG], s_r2[kTileTok * SEG], s_r3[kTileTok * SEG];
+  __shared__ float s_col[2][W][kTileTok];   // per-wave column partials, by tile parity
+
+  // the wave index is uniform: kept in a scalar register, LDS stage addresses
+  // (M0 of the global-to-LDS loads) are formed on the scalar unit
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int sel = blockIdx.y, cb = blockIdx.x;
+  const int h = a.heads[sel];
+  const int64_t col0 = (int64_t)cb * a.cb_tokens;                   // first key column
+  const int64_t col_end = min(col0 + a.cb_tokens, a.n_keys);
+  const int n_tiles = (int)((col_end - col0 + kTileTok - 1) / kTileTok);
+  const T* kh = reinterpret_cast<const T*>(a.k) + (size_t)h * a.n * kD;
+  const T* qb = reinterpret_cast<const T*>(a.q);
+
+  // Q fragments: wave-local M tile mt, lane row (lane & 15), segment kg*4 + lane/16
+  uint4 qf[MT][KG];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    const int row = (wave * MT + mt) * 16 + (lane & 15);
+    const bool ok = row < a.R;
+    const int i = row / GR, g = row - (row / GR) * GR;
+    const T* qrow = qb + ((size_t)(h * GR + g) * a.lq + (ok ? i : 0)) * kD;
+#pragma unroll
+    for (int kg = 0; kg < KG; ++kg) {
+      uint4 v = ld16(reinterpret_cast<const char*>(qrow) + (kg * 4 + (lane >> 4)) * 16);
+      qf[mt][kg] = ok ? v : make_uint4(0, 0, 0, 0);
+    }
+  }
+
+  // rows owned by this lane's accumulator registers: (mt, r) -> row
+  float st_mc[MT][4], st_l[MT][4];   // kRowStats: running max in log2 units (max * c), sum
+  float off[MT][4];                                // kColMass / kObsMatrix
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      st_mc[mt][r] = kMInit;
+      st_l[mt][r] = 0.f;
+      off[mt][r] = 0.f;
+      if (MODE != kRowStats) {
+        const int row = (wave * MT + mt) * 16 + 4 * (lane >> 4) + r;
+        off[mt][r] = a.rowoff[(size_t)sel * RPAD + row];
+      }
+    }
+
+  // K tiles arrive through a ring of NRING LDS stages filled by direct
+  // global-to-LDS loads (no staging registers).  Thread x's load i lands in
+  // slot i * 64 W + x; the slot's (token, position) picks which 16-byte
+  // segment of which row it fetches, so the ring holds the XOR-swizzled
+  // layout that tile_slot() reads.
+  const int full_tiles = (int)((col_end - col0) / kTileTok);   // tiles with no column past the end
+  const char* kbase = reinterpret_cast<const char*>(kh + (size_t)(a.key_off + col0) * kD);
+  // byte offset of each of this thread's loads inside a tile (unsigned: the
+  // loads take a scalar base plus a 32-bit vector offset)
+  uint32_t src_off[NSTAGE];
+#pragma unroll
+  for (int i = 0; i < NSTAGE; ++i) {
+    const int slot = i * W * 64 + threadIdx.x;
+    const int tok = slot / SEG, pos = slot - (slot / SEG) * SEG;
+    src_off[i] = (uint32_t)(tok * (kD * (int)sizeof(T)) + (pos ^ (tok & 15)) * 16);
+  }
+  // block-relative 32-bit offsets: a block spans at most kMaxBlockTokens
+  // columns, under 2 GiB of K rows
+  constexpr uint32_t ROWB = kD * sizeof(T);                  // bytes per K row (a power of two)
+  const int n_cols = (int)(col_end - col0);
+  // branch-free: a row past the end (or in a tile past the last) re-reads
+  // row 0 of the block
+  auto issue = [&](uint4* stage, int tile) {
+#pragma unroll
+    for (int i = 0; i < NSTAGE; ++i) {
+      const int col = tile * kTileTok + (int)(src_off[i] / ROWB);
+      const uint32_t o = col < n_cols ? (uint32_t)tile * (kTileTok * ROWB) + src_off[i] : (src_off[i] & (ROWB - 1));
+      __builtin_amdgcn_global_load_lds(kbase + o, (lds_void*)&stage[i * W * 64 + wave * 64], 16, 0, 0);
+    }
+  };
+  auto ring = [&](int k) -> uint4* { return k == 0 ? s_r0 : k == 1 ? s_r1 : k == 2 ? s_r2 : s_r3; };
+
+  // Column mass of tile t: the four waves' partials are summed by one wave
+  // (t mod 4) during tile t + 1, after the barrier that published them, so no
+  // wave waits for this step and no barrier of its own is needed.  With cs
+  // dividing 64 a chunk never straddles a tile and BlockMax is taken here.
+  auto finish_cols = [&](int t) {
+    const int p = t & 1;
+    float v = 0.f;
+#pragma unroll
+    for (int w = 0; w < W; ++w) v += s_col[p][w][lane];
+    v *= 1.0f / (float)GR;
+    const int64_t col = col0 + (int64_t)t * kTileTok + lane;
+    if (a.cs_fused > 0) {
+      const float mx = max_in_group(col < col_end ? v : -INFINITY, a.cs_fused);
+      if ((lane & (a.cs_fused - 1)) == 0 && col < col_end)
+        a.chunks[(size_t)sel * a.n_chunks + col / a.cs_fused] = mx;
+    } else if (col < col_end) {
+      a.colmass[(size_t)sel * a.n_keys + col] = v;
+    }
+  };
+  // keys at or past column col_end, and (causal) keys past a row's position,
+  // score -inf.  Columns count from col0; a row at query index i sees
+  // columns up to lim_rel + i (lim_rel clamped: every column of a block lies
+  // within 2^30 of its start).
+  const int lim_rel = (int)max((int64_t)-(1 << 30), min((int64_t)(1 << 30), a.q_pos0 - a.key_off - col0));
+  auto mask_acc = [&](floatx4& x, int col_rel, int mt) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = (wave * MT + mt) * 16 + 4 * (lane >> 4) + r;
+      bool ok = col_rel < n_cols;
+      if (CAUSAL) ok = ok && (col_rel - row / G <= lim_rel);
+      x[r] = ok ? x[r] : -INFINITY;
+    }
+  };
+
+  // One tile: the whole 64-column score block of this wave first (MFMA), then
+  // the softmax arithmetic on it (VALU); without branches inside, the
+  // scheduler overlaps the two.  Masks are needed only on a ragged last tile
+  // or where keys can lie past a row's position.  In row-statistics mode VAR
+  // picks what a tile adds to the row state: kRsSum the terms exp2(s c - m)
+  // against the lane's offset m = st_mc, kRsMax the maximum s c itself.
+  auto do_tile = [&](const uint4* cur, int tile, auto var_tag, auto mask_tag) {
+    constexpr int VAR = decltype(var_tag)::value;
+    const int64_t tcol0 = col0 + (int64_t)tile * kTileTok;
+    float cmass[4] = {0.f, 0.f, 0.f, 0.f};
+    auto tile_body = [&](auto mask_tag) {
+      constexpr bool MASK = decltype(mask_tag)::value;
+      // the MFMA work of one half tile (32 columns)
+      auto mfma_half = [&](int hh, floatx4 (&acc)[2][MT]) {
+        // k-group outer, row tile inner: a B fragment is live for MT MFMAs,
+        // and the MT accumulator chains interleave
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+#pragma unroll
+          for (int kg = 0; kg < KG; ++kg) {
+            const uint4 bf = cur[tile_slot<T>((2 * hh + j) * 16 + (lane & 15), kg * 4 + (lane >> 4))];
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+              acc[j][mt] = F::mma(qf[mt][kg], bf, kg == 0 ? floatx4{0.f, 0.f, 0.f, 0.f} : acc[j][mt]);
+          }
+        }
+      };
+      // the softmax arithmetic of one half tile
+      auto valu_half = [&](int hh, floatx4 (&acc)[2][MT]) {
+      if (MASK) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) mask_acc(acc[j][mt], tile * kTileTok + (2 * hh + j) * 16 + (lane & 15), mt);
+      }
+
+      if (MODE == kRowStats && VAR == kRsSum) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            st_l[mt][r] += fast_exp2(__builtin_fmaf(acc[0][mt][r], a.c, -st_mc[mt][r])) +
+                           fast_exp2(__builtin_fmaf(acc[1][mt][r], a.c, -st_mc[mt][r]));
+      } else if (MODE == kRowStats) {
+        // c > 0, so the maximum of s c is c times the maximum of s; masked
+        // scores (-inf) leave the state alone
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) st_mc[mt][r] = fmaxf(st_mc[mt][r], fmaxf(acc[0][mt][r], acc[1][mt][r]) * a.c);
+      } else if (MODE == kColMass) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              cmass[2 * hh + j] += fast_exp2(__builtin_fmaf(acc[j][mt][r], a.c, -off[mt][r]));
+      } else {  // kObsMatrix: group mean over the G rows of each query i
+        const float invG = 1.0f / (float)G;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int64_t col = tcol0 + (2 * hh + j) * 16 + (lane & 15);
+          const bool colok = !MASK || col < col_end;
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) {
+            float p[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) p[r] = fast_exp2(__builtin_fmaf(acc[j][mt][r], a.c, -off[mt][r]));
+            const int rbase = (wave * MT + mt) * 16 + 4 * (lane >> 4);
+            if (G == 1 || G == 2 || G == 4) {
+#pragma unroll
+              for (int r0 = 0; r0 < 4; r0 += G) {
+                const int i = (rbase + r0) / G;
+                float v = 0.f;
+#pragma unroll
+                for (int r = 0; r < G; ++r) v += p[r0 + r];
+                if (i < a.lq && colok) a.obs[((size_t)sel * a.lq + i) * a.n_keys + col] = v * invG;
+              }
+            } else {  // G == 8: the 8 rows of a query span lane groups 2k and 2k + 1
+              const float v = add_xor16(p[0] + p[1] + p[2] + p[3]);
+              const int i = rbase / 8;
+              if (((lane >> 4) & 1) == 0 && i < a.lq && colok)
+                a.obs[((size_t)sel * a.lq + i) * a.n_keys + col] = v * invG;
+            }
+          }
+        }
+      }
+      };
+      floatx4 acc0[2][MT], acc1[2][MT];
+      mfma_half(0, acc0);
+      valu_half(0, acc0);
+      mfma_half(1, acc1);
+      valu_half(1, acc1);
+    };
+
+    tile_body(mask_tag);
+
+    if (MODE == kColMass) {
+      // sum over the four row groups of lanes; each wave leaves its partial in LDS
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) {
+        const float v = add_xor32(add_xor16(cmass[nt]));
+        if (lane < 16) s_col[tile & 1][wave][nt * 16 + lane] = v;
+      }
+    }
+  };
+
+  // One step of the ring: wait for tile `tile` (stage S), publish it to the
+  // workgroup, refill the stage the previous step freed, run the tile.
+  // Vector memory operations retire in order, so the tile's loads are done
+  // once at most NRING - 2 later groups are outstanding; the barrier makes
+  // every wave's part of the tile visible and frees the stage the issue
+  // overwrites.
+  auto step = [&](int S, int tile, auto&& body) {
+    compiler_fence();
+    __builtin_amdgcn_s_waitcnt(kWaitRing);
+    __builtin_amdgcn_s_barrier();
+    compiler_fence();
+    issue(ring((S + NRING - 1) % NRING), tile + NRING - 1);
+    if (MODE == kColMass && tile > 0 && wave == ((tile - 1) & (W - 1))) finish_cols(tile - 1);
+    body(ring(S), tile);
+  };
+  auto prime = [&]() {
+#pragma unroll
+    for (int t = 0; t < NRING - 1; ++t) issue(ring(t), t);
+  };
+  // Tiles [0, n_plain) need no mask: every column lies before col_end and
+  // (causal) at or before the position of every row.  The rest -- a ragged
+  // last tile, the diagonal of a causal block -- come after them.
+  int n_plain = full_tiles;
+  if (CAUSAL) {
+    const int64_t lim = a.q_pos0 - a.key_off - col0 + 1;   // columns [0, lim) are visible to every row
+    n_plain = (int)min((int64_t)n_plain, lim <= 0 ? (int64_t)0 : lim / kTileTok);
+  }
+  using Plain = std::false_type;
+  using Masked = std::true_type;
+  // tiles [S0, n_tiles): the plain ones in whole turns of the ring with the
+  // stage known at compile time (S0 is 0 or 1; no branch inside a turn, so a
+  // tile's MFMA and VALU work share one basic block), the rest of the plain
+  // ones, then the masked ones
+  auto run = [&](auto s0_tag, auto var_tag) {
+    constexpr int S0 = decltype(s0_tag)::value;
+    int tile = S0;
+    for (; tile + NRING <= n_plain; tile += NRING) {
+#pragma unroll
+      for (int u = 0; u < NRING; ++u)
+        step((S0 + u) % NRING, tile + u, [&](const uint4* cur, int t) { do_tile(cur, t, var_tag, Plain{}); });
+    }
+    for (; tile < n_plain; ++tile)
+      step(tile % NRING, tile, [&](const uint4* cur, int t) { do_tile(cur, t, var_tag, Plain{}); });
+    for (; tile < n_tiles; ++tile)
+      step(tile % NRING, tile, [&](const uint4* cur, int t) { do_tile(cur, t, var_tag, Masked{}); });
+  };
+  using RsSum = std::integral_constant<int, kRsSum>;
+  using RsMax = std::integral_constant<int, kRsMax>;
+  // every wave is done with the ring and the ring's trailing loads have landed
+  auto drain = [&]() {
+    compiler_fence();
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_s_barrier();
+    compiler_fence();
+  };
+
+  prime();
+  if (MODE == kRowStats) {
+    // Each row's offset is its maximum over tile 0 of the block (log2 units;
+    // kMInit for a row that sees no key there -- it then sees none in the
+    // whole block, as a row's visible keys form a prefix of the key range).
+    // Later tiles add their terms against that offset with no running
+    // maximum: terms up to 2^128 stay finite in fp32.  A sum that overflows
+    // anyway sends the workgroup through two more sweeps of its block: the
+    // exact maximum, then the sum against it.
+    __shared__ int s_overflow;
+    if (threadIdx.x == 0) s_overflow = 0;   // published by the first step's barrier
+    if (n_tiles > 0) {
+      auto first = [&](auto mask_tag) {
+        step(0, 0, [&](const uint4* cur, int t) {
+          do_tile(cur, t, RsMax{}, mask_tag);
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) st_mc[mt][r] = max16(st_mc[mt][r]);
+          do_tile(cur, t, RsSum{}, mask_tag);
+        });
+      };
+      if (n_plain > 0) first(Plain{});
+      else first(Masked{});
+      run(std::integral_constant<int, 1>{}, RsSum{});
+      bool bad = false;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) bad |= !(st_l[mt][r] <= 0x1.fffffep127f);   // inf or NaN
+      if (__builtin_amdgcn_ballot_w64(bad) && lane == 0) s_overflow = 1;
+      drain();
+      if (__builtin_amdgcn_readfirstlane(s_overflow)) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            st_mc[mt][r] = kMInit;
+            st_l[mt][r] = 0.f;
+          }
+        prime();
+        run(std::integral_constant<int, 0>{}, RsMax{});
+        drain();
+        prime();
+        run(std::integral_constant<int, 0>{}, RsSum{});
+      }
+    }
+  } else {
+    run(std::integral_constant<int, 0>{}, RsSum{});
+  }
+
+  if (MODE == kColMass) {
+    barrier_lds_only();
+    if (n_tiles > 0 && wave == ((n_tiles - 1) & (W - 1))) finish_cols(n_tiles - 1);
+  }
+
+  // the ring's trailing loads must land before the workgroup's LDS is released
+  __builtin_amdgcn_s_waitcnt(0);
+  compiler_fence();
+
+  if (MODE == kRowStats) {
+    // merge the 16 lanes that share each row (maxima in log2 units)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float m = st_mc[mt][r];
+        const float M = max16(m);
+        const float lsum = sum16(st_l[mt][r] * fast_exp2(m - M));
+        const int row = (wave * MT + mt) * 16 + 4 * (lane >> 4) + r;
+        if ((lane & 15) == 0)
+          a.rowpart[((size_t)sel * a.n_colblk + cb) * RPAD + row] = make_float2(M, lsum);
+      }
+  }
+}
+
+// Two waves per SIMD (256 registers each): W = 4 waves of up to 4 row tiles
+// (256 rows) run two workgroups per compute unit; 512 rows take W = 8 waves
+// of 4 row tiles, one workgroup per compute unit.  fp32 fragments are twice
+// as wide, so fp32 takes W = 8 from 256 rows on.
+template <typename T, int W, int MT, int MODE, int G, bool CAUSAL>
+__global__ __launch_bounds__(W * 64) __attribute__((amdgpu_waves_per_eu(2)))
+void score_kernel(ScoreArgs a) {
+  score_body<T, W, MT, MODE, G, CAUSAL>(a);
+}
+
+template <typename T, int MODE, int G, bool CAUSAL>
+inline hipError_t launch_score_mt(int rows_pad, dim3 grid, hipStream_t s, const ScoreArgs& a) {
+  constexpr bool F32 = std::is_same<T, float>::value;
+  const int w = score_waves(F32 ? CATEKV_F32 : CATEKV_BF16, rows_pad);
+  const dim3 block(w * 64);
+#define CATEKV_SK(WW, MM) hipLaunchKernelGGL((score_kernel<T, WW, MM, MODE, G, CAUSAL>), grid, block, 0, s, a)
+  if (rows_pad == 64) CATEKV_SK(4, 1);
+  else if (rows_pad == 128) CATEKV_SK(4, 2);
+  else if (rows_pad == 256) {
+    if constexpr (F32) CATEKV_SK(8, 2);
+    else CATEKV_SK(4, 4);
+  }
+  else if (rows_pad == 512) CATEKV_SK(8, 4);
+  else return hipErrorInvalidValue;
+#undef CATEKV_SK
+  return hipGetLastError();
+}
+
+// Launch one score pass over grid (column blocks, heads) for rows_pad query
+// rows (64, 128, 256 or 512; see score_waves).
+hipError_t launch_score_rowstats(int dtype, int G, bool causal, int rows_pad, dim3 grid, hipStream_t s,
+                                 const ScoreArgs& a);
+hipError_t launch_score_colmass(int dtype, int rows_pad, dim3 grid, hipStream_t s, const ScoreArgs& a);
+hipError_t launch_score_obs(int dtype, int G, bool causal, int rows_pad, dim3 grid, hipStream_t s,
+                            const ScoreArgs& a);
+
+}  // namespace catekv

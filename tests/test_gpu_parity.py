@@ -235,13 +235,16 @@ SEL_CASES = [
 ]
 
 
-def test_select_score_spikes_move_the_row_maximum():
+@pytest.mark.parametrize("hq", [8, 16])
+def test_select_score_spikes_move_the_row_maximum(hq):
     """Five keys along each group's mean query direction, scaled so that
     most rows score them 60-900 nats above the other keys, sit after the
-    rows' first tiles: the running row maximum has to move in mid-row (the
-    terms would otherwise leave fp32's range), and the selection still
-    matches the oracle's."""
-    wl = _small("ctx32k_bf16", n=9000 + 37, hq=8, hkv=2)
+    rows' first tiles.  The first spike's terms stay inside fp32's range
+    against the offset the first tile fixed; the others overflow it and send
+    their column blocks through the exact-maximum sweep.  Either way the
+    selection matches the oracle's, for 256 rows (G = 4) and for 512 rows
+    (G = 8, eight-wave workgroups)."""
+    wl = _small("ctx32k_bf16", n=9000 + 37, hq=hq, hkv=2)
     seq = synth.make_sequence(wl)
     G, d = wl.group, 128
     k32 = synth.bf16_bits_to_f32(seq.k)
@@ -355,6 +358,25 @@ def test_score_heads(name, kw, causal):
     cv = cv.cpu().numpy().astype(np.float64)
     ref = O.score_heads(f64(seq.q_cv), seq.q_cv_pos0, f64(seq.k), wl.l_init, wl.l_rec, wl.k_pct, wl.alpha,
                         causal=causal)
+    say("  gpu", np.round(cv, 6), "\n  ref", np.round(ref, 6))
+    np.testing.assert_allclose(cv, ref, rtol=1e-4, atol=1e-6)
+
+
+def test_score_heads_rows_mid_sequence_causal():
+    """Observation rows in the middle of the sequence: under the causal mask
+    each row sees a prefix of the keys, whole column blocks past the rows are
+    invisible to all of them, and the blocks across the diagonal are partly
+    visible."""
+    wl = _small("ctx32k_bf16", n=6000)
+    seq = synth.make_sequence(wl)
+    q_pos0 = 2500
+    say(f"score_heads rows at {q_pos0}.. of n={seq.n}, causal")
+    cv = ck.score_heads(to_dev(seq.q_cv), to_dev(seq.k), q_pos0=q_pos0, l_init=wl.l_init,
+                        l_rec=wl.l_rec, k_pct=wl.k_pct, alpha=wl.alpha, causal=True)
+    torch.cuda.synchronize()
+    cv = cv.cpu().numpy().astype(np.float64)
+    ref = O.score_heads(f64(seq.q_cv), q_pos0, f64(seq.k), wl.l_init, wl.l_rec, wl.k_pct, wl.alpha,
+                        causal=True)
     say("  gpu", np.round(cv, 6), "\n  ref", np.round(ref, 6))
     np.testing.assert_allclose(cv, ref, rtol=1e-4, atol=1e-6)
 
