@@ -89,9 +89,12 @@ inline int score_rows_pad(int rows) {
   const int mt = (rows + 63) / 64;
   return (mt <= 1 ? 1 : mt <= 2 ? 2 : mt <= 4 ? 4 : 8) * 64;
 }
-// Waves per score workgroup: 4, or 8 where four waves would each hold more
-// than four 16-row tiles of bf16 Q fragments (two of fp32).
-inline int score_waves(int dtype, int rows_pad) { return rows_pad > (dtype == CATEKV_F32 ? 128 : 256) ? 8 : 4; }
+// Waves per score workgroup.  bf16: 4 up to 64 rows, 8 up to 256, 16 for
+// 512 (four waves per SIMD from 128 rows on); fp32: 4 up to 128 rows, else 8.
+inline int score_waves(int dtype, int rows_pad) {
+  if (dtype == CATEKV_F32) return rows_pad > 128 ? 8 : 4;
+  return rows_pad <= 64 ? 4 : rows_pad <= 256 ? 8 : 16;
+}
 // Key columns per score workgroup for n_keys columns of n_heads KV heads and
 // rows_pad query rows on a device of n_cu compute units; at most
 // kMaxBlockTokens (the kernels address a block's K rows with 32-bit offsets).

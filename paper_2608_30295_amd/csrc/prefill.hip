@@ -10,18 +10,53 @@
 
 namespace catekv {
 
+// Exact row statistics (max of s c over the visible columns, log2 units, and
+// the sum of exp2(s c - max)) of one query row over one column block, by the
+// 16 lanes of a row group; for the blocks whose sum overflowed fp32 in the
+// score pass (a score over 2^128 times the offset that pass took from the
+// block's first columns).  Plain fp32 dot products: this path is rare.
+template <typename T>
+__device__ float2 rowstats_exact(const ScoreArgs& a, int sel, int row, int b, int ln) {
+  const int h = a.heads[sel];
+  const int i = row / a.G, g = row - (row / a.G) * a.G;
+  const T* q = reinterpret_cast<const T*>(a.q) + ((size_t)(h * a.G + g) * a.lq + i) * kD;
+  const T* kh = reinterpret_cast<const T*>(a.k) + (size_t)h * a.n * kD;
+  const int64_t c0 = (int64_t)b * a.cb_tokens, c1 = min(c0 + a.cb_tokens, a.n_keys);
+  auto ld = [](const T* p, int d) -> float {
+    if constexpr (sizeof(T) == 2) return __uint_as_float((uint32_t)p[d] << 16);
+    else return p[d];
+  };
+  auto score = [&](int64_t col) -> float {   // s c, or -inf where the mask hides the key
+    if (a.causal && a.key_off + col > a.q_pos0 + i) return -INFINITY;
+    const T* kr = kh + (size_t)(a.key_off + col) * kD;
+    float s = 0.f;
+    for (int d = 0; d < kD; ++d) s = __builtin_fmaf(ld(q, d), ld(kr, d), s);
+    return s * a.c;
+  };
+  float m = -INFINITY;
+  for (int64_t col = c0 + ln; col < c1; col += 16) m = fmaxf(m, score(col));
+  m = max16(m);
+  if (m == -INFINITY) return make_float2(kMInit, 0.f);
+  float l = 0.f;
+  for (int64_t col = c0 + ln; col < c1; col += 16) l += fast_exp2(score(col) - m);
+  return make_float2(m, sum16(l));
+}
+
 // Merge the per-column-block row statistics: offset = m c + log2(l), +inf
 // for rows with no visible key and for padding rows.  16 lanes share a row
 // and walk its column blocks with independent loads, then reduce over DPP.
+// A block whose sum overflowed is recomputed exactly first.
 constexpr int kMergeRows = 16;    // rows per 256-thread workgroup
-__global__ __launch_bounds__(256) void rowstats_merge_kernel(const float2* __restrict__ part, int n_colblk,
-                                                             int R, int rpad, float* __restrict__ off) {
+template <typename T>
+__global__ __launch_bounds__(256) void rowstats_merge_kernel(ScoreArgs a, int rpad, float* __restrict__ off) {
   const int sel = blockIdx.y;
+  const int n_colblk = a.n_colblk, R = a.R;
   const int row = blockIdx.x * kMergeRows + (threadIdx.x >> 4);
   const int ln = threadIdx.x & 15;
   const bool ok = row < R;
-  const float2* p = part + (size_t)sel * n_colblk * rpad + (ok ? row : 0);
+  const float2* p = a.rowpart + (size_t)sel * n_colblk * rpad + (ok ? row : 0);
   float M = kMInit, L = 0.f;
+  bool bad = false;
   constexpr int UNR = 8;
   for (int b0 = ln; b0 < n_colblk; b0 += 16 * UNR) {
     float2 v[UNR];
@@ -29,6 +64,10 @@ __global__ __launch_bounds__(256) void rowstats_merge_kernel(const float2* __res
     for (int u = 0; u < UNR; ++u) {
       const int b = b0 + 16 * u;
       v[u] = (ok && b < n_colblk) ? p[(size_t)b * rpad] : make_float2(kMInit, 0.f);
+      if (!(v[u].y <= 0x1.fffffep127f)) {   // overflowed: merged below
+        bad = true;
+        v[u] = make_float2(kMInit, 0.f);
+      }
     }
     float mb = M;
 #pragma unroll
@@ -37,6 +76,20 @@ __global__ __launch_bounds__(256) void rowstats_merge_kernel(const float2* __res
 #pragma unroll
     for (int u = 0; u < UNR; ++u) L += v[u].y * fast_exp2(v[u].x - mb);
     M = mb;
+  }
+  // any overflowed block of this row: the 16 lanes recompute each of them
+  // together, and lane 0 merges the exact statistics
+  const uint64_t any = __ballot(bad);
+  if ((any >> (threadIdx.x & 48)) & 0xffffull) {
+    for (int b = 0; b < n_colblk; ++b) {
+      if (p[(size_t)b * rpad].y <= 0x1.fffffep127f) continue;   // the same for the row's 16 lanes
+      const float2 e = rowstats_exact<T>(a, sel, row, b, ln);
+      if (ln == 0 && e.y > 0.f) {
+        const float mb = fmaxf(M, e.x);
+        L = L * fast_exp2(M - mb) + e.y * fast_exp2(e.x - mb);
+        M = mb;
+      }
+    }
   }
   const float M16 = max16(M);
   L = sum16(L * fast_exp2(M - M16));
@@ -764,13 +817,13 @@ __global__ void cv_final_kernel(const CvState* __restrict__ st, int64_t n_keys, 
 
 static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // Score workgroups run in a single round: as many as the device holds at once
-// (two waves per SIMD: two 4-wave workgroups or one 8-wave workgroup per
-// compute unit, the bf16 residency; fp32 at 256 rows runs in two rounds),
-// each over whole 64-column tiles, at least four and at most kMaxBlockTokens
-// columns (more rounds beyond).  The count
+// (the bf16 residency: two workgroups per compute unit, whose LDS rings fill
+// 128 KB of its 160 KB, or one 16-wave workgroup at 512 rows; fp32 beyond 128
+// rows runs in two rounds), each over whole 64-column tiles, at least four
+// and at most kMaxBlockTokens columns (more rounds beyond).  The count
 // depends on the rows but not on the dtype, so workspace sizes do not either.
 int64_t score_block_tokens(int64_t n_keys, int n_heads, int rows_pad, int n_cu) {
-  const int64_t slots = (int64_t)std::max(1, n_cu) * (8 / score_waves(CATEKV_BF16, rows_pad));
+  const int64_t slots = (int64_t)std::max(1, n_cu) * (score_waves(CATEKV_BF16, rows_pad) > 8 ? 1 : 2);
   const int64_t per_head = std::max<int64_t>(1, slots / std::max(1, n_heads));
   int64_t cb = (std::max<int64_t>(n_keys, 1) + per_head - 1) / per_head;
   cb = (cb + kTileTok - 1) / kTileTok * kTileTok;
@@ -836,7 +889,7 @@ hipError_t launch_select(int dtype, const SelectGeom& g, const void* q_obs, cons
   ScoreArgs a{};
   a.q = q_obs; a.k = k; a.hkv = g.hkv; a.lq = g.l_obs; a.G = g.G; a.R = R; a.n = g.n;
   a.key_off = 0; a.n_keys = g.n_keys; a.cb_tokens = g.cb_tokens; a.n_colblk = g.n_colblk;
-  a.q_pos0 = g.n - g.l_obs; a.c = kLog2e / sqrtf((float)kD);
+  a.q_pos0 = g.n - g.l_obs; a.causal = 0; a.c = kLog2e / sqrtf((float)kD);
   for (int i = 0; i < g.n_sel; ++i) a.heads[i] = g.heads[i];
   a.rowpart = reinterpret_cast<float2*>(w + L.rowpart);
   a.rowoff = reinterpret_cast<const float*>(w + L.rowoff);
@@ -844,8 +897,12 @@ hipError_t launch_select(int dtype, const SelectGeom& g, const void* q_obs, cons
   const dim3 grid(g.n_colblk, g.n_sel);
   hipError_t e = launch_score_rowstats(dtype, g.G, false, rp, grid, stream, a);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(rowstats_merge_kernel, dim3((rp + kMergeRows - 1) / kMergeRows, g.n_sel), dim3(256), 0, stream,
-                     a.rowpart, g.n_colblk, R, rp, reinterpret_cast<float*>(w + L.rowoff));
+  if (dtype == CATEKV_BF16)
+    hipLaunchKernelGGL(rowstats_merge_kernel<uint16_t>, dim3((rp + kMergeRows - 1) / kMergeRows, g.n_sel), dim3(256), 0,
+                       stream, a, rp, reinterpret_cast<float*>(w + L.rowoff));
+  else
+    hipLaunchKernelGGL(rowstats_merge_kernel<float>, dim3((rp + kMergeRows - 1) / kMergeRows, g.n_sel), dim3(256), 0,
+                       stream, a, rp, reinterpret_cast<float*>(w + L.rowoff));
   float* S = reinterpret_cast<float*>(w + L.chunks);
   a.chunks = S;
   a.n_chunks = g.n_chunks;
@@ -980,7 +1037,7 @@ hipError_t launch_score(int dtype, const ScoreGeom& g, const void* q_rows, const
   ScoreArgs a{};
   a.q = q_rows; a.k = k; a.hkv = g.hkv; a.lq = g.lq; a.G = g.G; a.R = R; a.n = g.n;
   a.key_off = g.l_init; a.n_keys = g.n_keys; a.cb_tokens = g.cb_tokens; a.n_colblk = g.n_colblk;
-  a.q_pos0 = g.q_pos0; a.c = kLog2e / sqrtf((float)kD);
+  a.q_pos0 = g.q_pos0; a.causal = g.causal; a.c = kLog2e / sqrtf((float)kD);
   for (int i = 0; i < g.hkv; ++i) a.heads[i] = i;
   a.rowpart = reinterpret_cast<float2*>(w + L.rowpart);
   a.rowoff = reinterpret_cast<const float*>(w + L.rowoff);
@@ -988,8 +1045,12 @@ hipError_t launch_score(int dtype, const ScoreGeom& g, const void* q_rows, const
   const dim3 grid(g.n_colblk, g.hkv);
   hipError_t e = launch_score_rowstats(dtype, g.G, g.causal, rp, grid, stream, a);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(rowstats_merge_kernel, dim3((rp + kMergeRows - 1) / kMergeRows, g.hkv), dim3(256), 0, stream,
-                     a.rowpart, g.n_colblk, R, rp, reinterpret_cast<float*>(w + L.rowoff));
+  if (dtype == CATEKV_BF16)
+    hipLaunchKernelGGL(rowstats_merge_kernel<uint16_t>, dim3((rp + kMergeRows - 1) / kMergeRows, g.hkv), dim3(256), 0,
+                       stream, a, rp, reinterpret_cast<float*>(w + L.rowoff));
+  else
+    hipLaunchKernelGGL(rowstats_merge_kernel<float>, dim3((rp + kMergeRows - 1) / kMergeRows, g.hkv), dim3(256), 0,
+                       stream, a, rp, reinterpret_cast<float*>(w + L.rowoff));
   e = launch_score_obs(dtype, g.G, g.causal, rp, grid, stream, a);
   if (e != hipSuccess) return e;
 

@@ -58,6 +58,28 @@ __device__ __forceinline__ int tile_slot(int tok, int seg) {
   return tok * Frag<T>::SEG + (seg ^ (tok & 15));
 }
 
+// Output-tile shape of the score block: 16 x 16 tiles
+// (v_mfma_f32_16x16x32_bf16 / 4 x v_mfma_f32_16x16x4f32).  At k-step ks a
+// lane's A (Q) and B (K) fragments are 16 bytes of tile row / column
+// frag_rc(lane): 16-byte segment seg(ks, lane) of that row of Q or K (the
+// same segment for both, so every dot product covers all 128 dims).
+// Accumulator register r of a lane holds the score of tile row row(lane, r)
+// and tile column col(lane).
+template <typename T> struct Shape {
+  using Acc = floatx4;
+  static constexpr int TR = 16, TC = 16, NR = 4, KS = Frag<T>::KG;
+  static constexpr int kPair8 = 16;   // lanes l and l ^ 16 hold the two halves of an aligned group of 8 rows
+  __device__ static __forceinline__ int frag_rc(int lane) { return lane & 15; }
+  __device__ static __forceinline__ int seg(int ks, int lane) { return ks * 4 + (lane >> 4); }
+  __device__ static __forceinline__ int row(int lane, int r) { return 4 * (lane >> 4) + r; }
+  __device__ static __forceinline__ int col(int lane) { return lane & 15; }
+  __device__ static __forceinline__ Acc zero() { return Acc{0.f, 0.f, 0.f, 0.f}; }
+  __device__ static __forceinline__ Acc mma(uint4 a, uint4 b, Acc c) { return Frag<T>::mma(a, b, c); }
+  // over the lanes holding one row (its 16 columns) / one column (its 16 rows)
+  __device__ static __forceinline__ float row_max(float x) { return max16(x); }
+  __device__ static __forceinline__ float row_sum(float x) { return sum16(x); }
+  __device__ static __forceinline__ float col_sum(float x) { return add_xor32(add_xor16(x)); }
+};
 enum ScoreMode { kRowStats = 0, kColMass = 1, kObsMatrix = 2 };
 enum RowStatsVar { kRsSum = 0, kRsMax = 1 };
 
@@ -71,6 +93,7 @@ struct ScoreArgs {
   int64_t cb_tokens;      // key columns per workgroup
   int n_colblk;
   int64_t q_pos0;         // absolute position of query row i = 0 (causal mask)
+  int causal;             // the causal mask applies (the score kernels take it as a template argument)
   float c;                // log2(e) / sqrt(d)
   int32_t heads[128];     // KV head per blockIdx.y
   float2* rowpart;        // kRowStats out: [n_sel][n_colblk][R_pad] (max * c, sum)
@@ -84,14 +107,16 @@ struct ScoreArgs {
 
 template <typename T, int W, int MT, int MODE, int G, bool CAUSAL>
 __device__ __forceinline__ void score_body(const ScoreArgs& a) {
-  using F = Frag<T>;
-  constexpr int KG = F::KG, SEG = F::SEG;
+  using S = Shape<T>;
+  using Acc = typename S::Acc;
+  constexpr int SEG = Frag<T>::SEG, KS = S::KS, TR = S::TR, TC = S::TC, NR = S::NR;
+  constexpr int NCT = 32 / TC;            // column tiles per half tile (32 columns)
   // G = 0: the group size is taken at run time (a.G); only the passes whose
   // arithmetic never splits a group's rows (row statistics without a causal
   // mask, column mass) are built that way
   static_assert(G > 0 || (!CAUSAL && MODE != kObsMatrix), "G must be fixed for masks and the group mean");
   const int GR = G > 0 ? G : a.G;
-  constexpr int RPAD = W * MT * 16;
+  constexpr int RPAD = W * MT * TR;
   constexpr int NSTAGE = kTileTok * SEG / (W * 64);   // 16-byte loads per thread per tile
   constexpr int NRING = sizeof(T) == 2 ? 4 : 2;               // LDS stages (16 KB bf16, 32 KB fp32 each)
   // s_waitcnt immediate: vmcnt <= NSTAGE * (NRING - 2), expcnt not waited on;
@@ -115,35 +140,33 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
   const T* kh = reinterpret_cast<const T*>(a.k) + (size_t)h * a.n * kD;
   const T* qb = reinterpret_cast<const T*>(a.q);
 
-  // Q fragments: wave-local M tile mt, lane row (lane & 15), segment kg*4 + lane/16
-  uint4 qf[MT][KG];
+  // Q fragments: the wave's row tile mt, tile row frag_rc(lane), segment seg(ks, lane)
+  uint4 qf[MT][KS];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
-    const int row = (wave * MT + mt) * 16 + (lane & 15);
+    const int row = (wave * MT + mt) * TR + S::frag_rc(lane);
     const bool ok = row < a.R;
     const int i = row / GR, g = row - (row / GR) * GR;
     const T* qrow = qb + ((size_t)(h * GR + g) * a.lq + (ok ? i : 0)) * kD;
 #pragma unroll
-    for (int kg = 0; kg < KG; ++kg) {
-      uint4 v = ld16(reinterpret_cast<const char*>(qrow) + (kg * 4 + (lane >> 4)) * 16);
-      qf[mt][kg] = ok ? v : make_uint4(0, 0, 0, 0);
+    for (int ks = 0; ks < KS; ++ks) {
+      uint4 v = ld16(reinterpret_cast<const char*>(qrow) + S::seg(ks, lane) * 16);
+      qf[mt][ks] = ok ? v : make_uint4(0, 0, 0, 0);
     }
   }
+  // the row of this lane's accumulator register r in row tile mt
+  auto row_of = [&](int mt, int r) { return (wave * MT + mt) * TR + S::row(lane, r); };
 
-  // rows owned by this lane's accumulator registers: (mt, r) -> row
-  float st_mc[MT][4], st_l[MT][4];   // kRowStats: running max in log2 units (max * c), sum
-  float off[MT][4];                                // kColMass / kObsMatrix
+  float st_mc[MT][NR], st_l[MT][NR];   // kRowStats: row offset (log2 units), sum
+  float off[MT][NR];                   // kColMass / kObsMatrix
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
+    for (int r = 0; r < NR; ++r) {
       st_mc[mt][r] = kMInit;
       st_l[mt][r] = 0.f;
       off[mt][r] = 0.f;
-      if (MODE != kRowStats) {
-        const int row = (wave * MT + mt) * 16 + 4 * (lane >> 4) + r;
-        off[mt][r] = a.rowoff[(size_t)sel * RPAD + row];
-      }
+      if (MODE != kRowStats) off[mt][r] = a.rowoff[(size_t)sel * RPAD + row_of(mt, r)];
     }
 
   // K tiles arrive through a ring of NRING LDS stages filled by direct
@@ -202,10 +225,10 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
   // columns up to lim_rel + i (lim_rel clamped: every column of a block lies
   // within 2^30 of its start).
   const int lim_rel = (int)max((int64_t)-(1 << 30), min((int64_t)(1 << 30), a.q_pos0 - a.key_off - col0));
-  auto mask_acc = [&](floatx4& x, int col_rel, int mt) {
+  auto mask_acc = [&](Acc& x, int col_rel, int mt) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = (wave * MT + mt) * 16 + 4 * (lane >> 4) + r;
+    for (int r = 0; r < NR; ++r) {
+      const int row = row_of(mt, r);
       bool ok = col_rel < n_cols;
       if (CAUSAL) ok = ok && (col_rel - row / G <= lim_rel);
       x[r] = ok ? x[r] : -INFINITY;
@@ -218,104 +241,118 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
   // or where keys can lie past a row's position.  In row-statistics mode VAR
   // picks what a tile adds to the row state: kRsSum the terms exp2(s c - m)
   // against the lane's offset m = st_mc, kRsMax the maximum s c itself.
-  auto do_tile = [&](const uint4* cur, int tile, auto var_tag, auto mask_tag) {
+  auto do_tile = [&](const uint4* cur, int tile, auto var_tag, auto mask_tag, bool first_half_only = false) {
     constexpr int VAR = decltype(var_tag)::value;
     const int64_t tcol0 = col0 + (int64_t)tile * kTileTok;
-    float cmass[4] = {0.f, 0.f, 0.f, 0.f};
-    auto tile_body = [&](auto mask_tag) {
-      constexpr bool MASK = decltype(mask_tag)::value;
-      // the MFMA work of one half tile (32 columns)
-      auto mfma_half = [&](int hh, floatx4 (&acc)[2][MT]) {
-        // k-group outer, row tile inner: a B fragment is live for MT MFMAs,
-        // and the MT accumulator chains interleave
+    float cmass[kTileTok / TC];
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
+    for (int t = 0; t < kTileTok / TC; ++t) cmass[t] = -0.f;   // -0 + x folds to x
+    // the MFMA work of one half tile (32 columns: NCT column tiles); k-step
+    // outer, row tile inner: a B fragment is live for MT MFMAs, and the MT
+    // accumulator chains interleave
+    auto mfma_half = [&](int hh, Acc (&acc)[NCT][MT]) {
 #pragma unroll
-          for (int kg = 0; kg < KG; ++kg) {
-            const uint4 bf = cur[tile_slot<T>((2 * hh + j) * 16 + (lane & 15), kg * 4 + (lane >> 4))];
+      for (int ct = 0; ct < NCT; ++ct) {
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-              acc[j][mt] = F::mma(qf[mt][kg], bf, kg == 0 ? floatx4{0.f, 0.f, 0.f, 0.f} : acc[j][mt]);
-          }
+        for (int ks = 0; ks < KS; ++ks) {
+          const uint4 bf = cur[tile_slot<T>(hh * 32 + ct * TC + S::frag_rc(lane), S::seg(ks, lane))];
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) acc[ct][mt] = S::mma(qf[mt][ks], bf, ks == 0 ? S::zero() : acc[ct][mt]);
         }
-      };
-      // the softmax arithmetic of one half tile
-      auto valu_half = [&](int hh, floatx4 (&acc)[2][MT]) {
+      }
+    };
+    // the softmax arithmetic of one half tile
+    auto valu_half = [&](int hh, Acc (&acc)[NCT][MT], auto mask_tag) {
+      constexpr bool MASK = decltype(mask_tag)::value;
       if (MASK) {
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
-          for (int mt = 0; mt < MT; ++mt) mask_acc(acc[j][mt], tile * kTileTok + (2 * hh + j) * 16 + (lane & 15), mt);
+          for (int mt = 0; mt < MT; ++mt) mask_acc(acc[ct][mt], tile * kTileTok + hh * 32 + ct * TC + S::col(lane), mt);
       }
-
       if (MODE == kRowStats && VAR == kRsSum) {
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-          for (int r = 0; r < 4; ++r)
-            st_l[mt][r] += fast_exp2(__builtin_fmaf(acc[0][mt][r], a.c, -st_mc[mt][r])) +
-                           fast_exp2(__builtin_fmaf(acc[1][mt][r], a.c, -st_mc[mt][r]));
+          for (int r = 0; r < NR; ++r) {
+            float t = fast_exp2(__builtin_fmaf(acc[0][mt][r], a.c, -st_mc[mt][r]));
+#pragma unroll
+            for (int ct = 1; ct < NCT; ++ct) t += fast_exp2(__builtin_fmaf(acc[ct][mt][r], a.c, -st_mc[mt][r]));
+            st_l[mt][r] += t;
+          }
       } else if (MODE == kRowStats) {
         // c > 0, so the maximum of s c is c times the maximum of s; masked
         // scores (-inf) leave the state alone
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) st_mc[mt][r] = fmaxf(st_mc[mt][r], fmaxf(acc[0][mt][r], acc[1][mt][r]) * a.c);
+          for (int r = 0; r < NR; ++r) {
+            float m = acc[0][mt][r];
+#pragma unroll
+            for (int ct = 1; ct < NCT; ++ct) m = fmaxf(m, acc[ct][mt][r]);
+            st_mc[mt][r] = fmaxf(st_mc[mt][r], m * a.c);
+          }
       } else if (MODE == kColMass) {
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-              cmass[2 * hh + j] += fast_exp2(__builtin_fmaf(acc[j][mt][r], a.c, -off[mt][r]));
+            for (int r = 0; r < NR; ++r)
+              cmass[hh * NCT + ct] += fast_exp2(__builtin_fmaf(acc[ct][mt][r], a.c, -off[mt][r]));
       } else {  // kObsMatrix: group mean over the G rows of each query i
         const float invG = 1.0f / (float)G;
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const int64_t col = tcol0 + (2 * hh + j) * 16 + (lane & 15);
+        for (int ct = 0; ct < NCT; ++ct) {
+          const int64_t col = tcol0 + hh * 32 + ct * TC + S::col(lane);
           const bool colok = !MASK || col < col_end;
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) {
-            float p[4];
+            float p[NR];
 #pragma unroll
-            for (int r = 0; r < 4; ++r) p[r] = fast_exp2(__builtin_fmaf(acc[j][mt][r], a.c, -off[mt][r]));
-            const int rbase = (wave * MT + mt) * 16 + 4 * (lane >> 4);
+            for (int r = 0; r < NR; ++r) p[r] = fast_exp2(__builtin_fmaf(acc[ct][mt][r], a.c, -off[mt][r]));
             if (G == 1 || G == 2 || G == 4) {
+              // the lane's NR registers hold NR consecutive rows from a multiple of 4:
+              // queries i0 .. i0 + NR / G - 1, one store base for all of them
+              const int i0 = row_of(mt, 0) / G;
+              float* ob = a.obs + ((size_t)sel * a.lq + i0) * a.n_keys + col;
 #pragma unroll
-              for (int r0 = 0; r0 < 4; r0 += G) {
-                const int i = (rbase + r0) / G;
-                float v = 0.f;
+              for (int r0 = 0; r0 < NR; r0 += G) {
+                float v = p[r0];
 #pragma unroll
-                for (int r = 0; r < G; ++r) v += p[r0 + r];
-                if (i < a.lq && colok) a.obs[((size_t)sel * a.lq + i) * a.n_keys + col] = v * invG;
+                for (int r = 1; r < G; ++r) v += p[r0 + r];
+                if (i0 + r0 / G < a.lq && colok) ob[(size_t)(r0 / G) * a.n_keys] = v * invG;
               }
-            } else {  // G == 8: the 8 rows of a query span lane groups 2k and 2k + 1
-              const float v = add_xor16(p[0] + p[1] + p[2] + p[3]);
-              const int i = rbase / 8;
-              if (((lane >> 4) & 1) == 0 && i < a.lq && colok)
-                a.obs[((size_t)sel * a.lq + i) * a.n_keys + col] = v * invG;
+            } else {  // G == 8: lanes l and l ^ kPair8 hold the two halves of each group of 8 rows
+#pragma unroll
+              for (int b4 = 0; b4 < NR; b4 += 4) {
+                const float q4 = p[b4] + p[b4 + 1] + p[b4 + 2] + p[b4 + 3];
+                const float v = S::kPair8 == 16 ? add_xor16(q4) : add_xor32(q4);
+                const int i = row_of(mt, b4) / 8;
+                if ((lane & S::kPair8) == 0 && i < a.lq && colok)
+                  a.obs[((size_t)sel * a.lq + i) * a.n_keys + col] = v * invG;
+              }
             }
           }
         }
       }
-      };
-      floatx4 acc0[2][MT], acc1[2][MT];
-      mfma_half(0, acc0);
-      valu_half(0, acc0);
-      mfma_half(1, acc1);
-      valu_half(1, acc1);
     };
-
-    tile_body(mask_tag);
+    // one half's accumulators live at a time: the second half's MFMAs stay
+    // after the first half's softmax work
+    Acc acc0[NCT][MT], acc1[NCT][MT];
+    mfma_half(0, acc0);
+    valu_half(0, acc0, mask_tag);
+    if (first_half_only) return;
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_half(1, acc1);
+    valu_half(1, acc1, mask_tag);
 
     if (MODE == kColMass) {
-      // sum over the four row groups of lanes; each wave leaves its partial in LDS
+      // sum over the lanes holding each column; each wave leaves its partial in LDS
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
-        const float v = add_xor32(add_xor16(cmass[nt]));
-        if (lane < 16) s_col[tile & 1][wave][nt * 16 + lane] = v;
+      for (int t = 0; t < kTileTok / TC; ++t) {
+        const float v = S::col_sum(cmass[t]);
+        if (lane < TC) s_col[tile & 1][wave][t * TC + lane] = v;
       }
     }
   };
@@ -368,60 +405,30 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
   };
   using RsSum = std::integral_constant<int, kRsSum>;
   using RsMax = std::integral_constant<int, kRsMax>;
-  // every wave is done with the ring and the ring's trailing loads have landed
-  auto drain = [&]() {
-    compiler_fence();
-    __builtin_amdgcn_s_waitcnt(0);
-    __builtin_amdgcn_s_barrier();
-    compiler_fence();
-  };
 
   prime();
   if (MODE == kRowStats) {
-    // Each row's offset is its maximum over tile 0 of the block (log2 units;
-    // kMInit for a row that sees no key there -- it then sees none in the
-    // whole block, as a row's visible keys form a prefix of the key range).
-    // Later tiles add their terms against that offset with no running
-    // maximum: terms up to 2^128 stay finite in fp32.  A sum that overflows
-    // anyway sends the workgroup through two more sweeps of its block: the
-    // exact maximum, then the sum against it.
-    __shared__ int s_overflow;
-    if (threadIdx.x == 0) s_overflow = 0;   // published by the first step's barrier
+    // Each row's offset is its maximum over the first 32 columns of the block
+    // (log2 units; kMInit for a row that sees no key there -- it then sees
+    // none in the whole block, as a row's visible keys form a prefix of the
+    // key range).  Later tiles add their terms against that offset with no
+    // running maximum: terms up to 2^128 stay finite in fp32.  A sum that
+    // overflows anyway is written as it is (inf); the merge recomputes that
+    // block's statistics exactly.
     if (n_tiles > 0) {
       auto first = [&](auto mask_tag) {
         step(0, 0, [&](const uint4* cur, int t) {
-          do_tile(cur, t, RsMax{}, mask_tag);
+          do_tile(cur, t, RsMax{}, mask_tag, true);
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) st_mc[mt][r] = max16(st_mc[mt][r]);
+            for (int r = 0; r < NR; ++r) st_mc[mt][r] = S::row_max(st_mc[mt][r]);
           do_tile(cur, t, RsSum{}, mask_tag);
         });
       };
       if (n_plain > 0) first(Plain{});
       else first(Masked{});
       run(std::integral_constant<int, 1>{}, RsSum{});
-      bool bad = false;
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) bad |= !(st_l[mt][r] <= 0x1.fffffep127f);   // inf or NaN
-      if (__builtin_amdgcn_ballot_w64(bad) && lane == 0) s_overflow = 1;
-      drain();
-      if (__builtin_amdgcn_readfirstlane(s_overflow)) {
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            st_mc[mt][r] = kMInit;
-            st_l[mt][r] = 0.f;
-          }
-        prime();
-        run(std::integral_constant<int, 0>{}, RsMax{});
-        drain();
-        prime();
-        run(std::integral_constant<int, 0>{}, RsSum{});
-      }
     }
   } else {
     run(std::integral_constant<int, 0>{}, RsSum{});
@@ -437,27 +444,31 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
   compiler_fence();
 
   if (MODE == kRowStats) {
-    // merge the 16 lanes that share each row (maxima in log2 units)
+    // merge the lanes that share each row (maxima in log2 units)
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
+      for (int r = 0; r < NR; ++r) {
         const float m = st_mc[mt][r];
-        const float M = max16(m);
-        const float lsum = sum16(st_l[mt][r] * fast_exp2(m - M));
-        const int row = (wave * MT + mt) * 16 + 4 * (lane >> 4) + r;
-        if ((lane & 15) == 0)
-          a.rowpart[((size_t)sel * a.n_colblk + cb) * RPAD + row] = make_float2(M, lsum);
+        const float M = S::row_max(m);
+        const float lsum = S::row_sum(st_l[mt][r] * fast_exp2(m - M));
+        if (S::col(lane) == 0)
+          a.rowpart[((size_t)sel * a.n_colblk + cb) * RPAD + row_of(mt, r)] = make_float2(M, lsum);
       }
   }
 }
 
-// Two waves per SIMD (256 registers each): W = 4 waves of up to 4 row tiles
-// (256 rows) run two workgroups per compute unit; 512 rows take W = 8 waves
-// of 4 row tiles, one workgroup per compute unit.  fp32 fragments are twice
-// as wide, so fp32 takes W = 8 from 256 rows on.
-template <typename T, int W, int MT, int MODE, int G, bool CAUSAL>
-__global__ __launch_bounds__(W * 64) __attribute__((amdgpu_waves_per_eu(2)))
+// Workgroup shapes, W waves of MT 16-row tiles (W * MT * 16 = rows), WPE
+// waves per SIMD (registers: 512 / WPE per wave).  The LDS ring (64 KB)
+// allows two workgroups per compute unit.  bf16 runs four waves per SIMD from
+// 128 rows on: 8-wave workgroups of one or two row tiles per wave, two per
+// CU; 512 rows in one 16-wave workgroup per CU.  Measured at 256 rows (5
+// heads, 128K keys): pass times 53 / 57 us against 58 / 61 us for 4 waves of
+// 4 row tiles at two waves per SIMD.  fp32 fragments are twice as wide and
+// keep two waves per SIMD.  The block count (score_block_tokens) follows
+// the bf16 residency; the other shapes run in more rounds.
+template <typename T, int W, int MT, int MODE, int G, bool CAUSAL, int WPE>
+__global__ __launch_bounds__(W * 64) __attribute__((amdgpu_waves_per_eu(WPE)))
 void score_kernel(ScoreArgs a) {
   score_body<T, W, MT, MODE, G, CAUSAL>(a);
 }
@@ -465,17 +476,30 @@ void score_kernel(ScoreArgs a) {
 template <typename T, int MODE, int G, bool CAUSAL>
 inline hipError_t launch_score_mt(int rows_pad, dim3 grid, hipStream_t s, const ScoreArgs& a) {
   constexpr bool F32 = std::is_same<T, float>::value;
-  const int w = score_waves(F32 ? CATEKV_F32 : CATEKV_BF16, rows_pad);
-  const dim3 block(w * 64);
-#define CATEKV_SK(WW, MM) hipLaunchKernelGGL((score_kernel<T, WW, MM, MODE, G, CAUSAL>), grid, block, 0, s, a)
-  if (rows_pad == 64) CATEKV_SK(4, 1);
-  else if (rows_pad == 128) CATEKV_SK(4, 2);
-  else if (rows_pad == 256) {
-    if constexpr (F32) CATEKV_SK(8, 2);
-    else CATEKV_SK(4, 4);
+  // one query per row (G = 1) stores every row of the observation matrix on
+  // its own: those passes keep two waves per SIMD
+  constexpr bool NARROW = MODE == kObsMatrix && G == 1;
+#define CATEKV_SK(WW, MM, PP) \
+  hipLaunchKernelGGL((score_kernel<T, WW, MM, MODE, G, CAUSAL, PP>), grid, dim3((WW) * 64), 0, s, a)
+  if constexpr (F32) {
+    if (rows_pad == 64) CATEKV_SK(4, 1, 2);
+    else if (rows_pad == 128) CATEKV_SK(4, 2, 2);
+    else if (rows_pad == 256) CATEKV_SK(8, 2, 2);
+    else if (rows_pad == 512) CATEKV_SK(8, 4, 2);
+    else return hipErrorInvalidValue;
+  } else if constexpr (NARROW) {
+    if (rows_pad == 64) CATEKV_SK(4, 1, 2);
+    else if (rows_pad == 128) CATEKV_SK(8, 1, 4);
+    else if (rows_pad == 256) CATEKV_SK(8, 2, 2);
+    else if (rows_pad == 512) CATEKV_SK(8, 4, 2);
+    else return hipErrorInvalidValue;
+  } else {
+    if (rows_pad == 64) CATEKV_SK(4, 1, 2);
+    else if (rows_pad == 128) CATEKV_SK(8, 1, 4);
+    else if (rows_pad == 256) CATEKV_SK(8, 2, 4);
+    else if (rows_pad == 512) CATEKV_SK(16, 2, 4);
+    else return hipErrorInvalidValue;
   }
-  else if (rows_pad == 512) CATEKV_SK(8, 4);
-  else return hipErrorInvalidValue;
 #undef CATEKV_SK
   return hipGetLastError();
 }
