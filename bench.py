@@ -263,19 +263,21 @@ def time_prefill_shape(torch, ck, wl, dev, stream):
     v_c = torch.empty_like(k_c)
 
     def time_it(fn, reps):
+        # median of per-call event pairs after two warm-up calls (us)
         fn()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(reps):
+        fn()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for e0, e1 in evs:
+            e0.record(stream)
             fn()
-        e1.record(stream)
-        e1.synchronize()
-        return e0.elapsed_time(e1) * 1e3 / reps
+            e1.record(stream)
+        evs[-1][1].synchronize()
+        return float(np.median([e0.elapsed_time(e1) * 1e3 for e0, e1 in evs]))
     t_cv = time_it(lambda: ck.score_heads(q_cv, k, q_pos0=q_pos0, l_init=wl.l_init, l_rec=wl.l_rec,
-                                          k_pct=wl.k_pct, alpha=wl.alpha, ws=cv_ws), 2)
+                                          k_pct=wl.k_pct, alpha=wl.alpha, ws=cv_ws), 5)
     idx = ck.select_critical(q_obs, k, heads, wl.cs, b, ws=sel_ws)
-    t_sel = time_it(lambda: ck.select_critical(q_obs, k, heads, wl.cs, b, ws=sel_ws), 3)
-    t_cmp = time_it(lambda: ck.compact_kv(k, v, heads, idx, wl.cs, wl.l_obs, lens, out=(k_c, v_c)), 3)
+    t_sel = time_it(lambda: ck.select_critical(q_obs, k, heads, wl.cs, b, ws=sel_ws), 7)
+    t_cmp = time_it(lambda: ck.compact_kv(k, v, heads, idx, wl.cs, wl.l_obs, lens, out=(k_c, v_c)), 7)
     n_keys = n - wl.l_obs
     esz = 2
     sel_flops = 2.0 * len(heads) * G * wl.l_obs * n_keys * d
@@ -394,16 +396,18 @@ def main():
             eta_caches.append((eta, ba, k_a, v_a, lens_a.cpu().numpy(), e0.elapsed_time(e1) * 1e3 / 3))
 
     def time_it(fn, reps):
+        # median of per-call event pairs after two warm-up calls (us)
         fn()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(reps):
+        fn()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for e0, e1 in evs:
+            e0.record(stream)
             fn()
-        e1.record(stream)
-        e1.synchronize()
-        return e0.elapsed_time(e1) * 1e3 / reps     # us
+            e1.record(stream)
+        evs[-1][1].synchronize()
+        return float(np.median([e0.elapsed_time(e1) * 1e3 for e0, e1 in evs]))
 
-    reps = 5
+    reps = 20
     t_cv = time_it(lambda: ck.score_heads(q_cv, k_full, q_pos0=seq.q_cv_pos0, l_init=wl.l_init, l_rec=wl.l_rec,
                                           k_pct=wl.k_pct, alpha=wl.alpha, ws=cv_ws), reps)
     idx_out = torch.empty_like(idx)
