@@ -1,0 +1,950 @@
+// CV head score (Section 3.2, Eq. 2-4) over the observation matrix A of each
+// KV head (Eq. 1; [lq][n_keys] fp32, row-major, written by the score pass):
+// Phi = alpha times the k-th percentile of A's N = lq n_keys entries (linear
+// interpolation between the order statistics x_(lo) and x_(lo+1),
+// lo = floor((N - 1) k)), C_j = #{i : A[i][j] >= Phi}, and the score is the
+// population standard deviation of C over its mean.
+//
+// Bracket route: a sample of A gives a key range [k_lo, k_hi] expected to
+// hold ranks lo and lo + 1, and with it a range [t_lo, t_hi) that then holds
+// Phi.  One walk over A, column by column, counts the entries below the key
+// range, counts per column the entries at or above t_hi (at or above Phi
+// whatever its exact value) and gathers the few entries inside either range
+// with their columns.  x_(lo), x_(lo+1) and Phi are resolved over the
+// gathered entries, and the gathered values at or above Phi join their
+// columns' counts.
+// Radix route: when the sample's range misses a rank, or the gathered
+// entries overflow their buffer (heavy ties), exact radix passes over A
+// take over for that head.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+
+#include "internal.h"
+
+namespace catekv {
+namespace {
+
+constexpr int kBins = 2048;
+constexpr uint32_t kNone = 0xFFFFFFFFu;
+
+// Ordered integer key of a float: key order is float order (-0 < +0).
+__device__ __forceinline__ uint32_t ord_key(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float key_to_float(uint32_t key) {
+  return __uint_as_float((key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key);
+}
+
+struct CvState {                   // per KV head, in the workspace
+  int64_t rank;                    // lo = floor((N - 1) k), 0-based
+  uint32_t k_lo, k_hi;             // the bracket: ordered keys [k_lo, k_hi]
+  float t_lo, t_hi;                // Phi lies in [t_lo, t_hi)
+  int shift1;                      // (key - k_lo) >> shift1: first digit over the bracket
+  uint32_t phi_over;               // a workgroup's gathered pairs overflowed its buffer
+  unsigned long long n_cand;       // entries inside the bracket
+  unsigned long long below_br;     // entries below the bracket
+  unsigned long long sum_c, sum_c2;  // sums of C_j and C_j^2 (bracket route)
+  double phi;
+  uint32_t min2;                   // bracket route: smallest key offset above x_(lo)'s first-digit bin
+  uint32_t n_list;                 // bracket route: entries of x_(lo)'s first-digit bin
+  uint32_t arrive_r;               // bracket route: listing workgroups done
+  uint32_t arrive_f;               // radix route: workgroups done in the launch that ends the head
+  uint32_t fb_min;                 // radix route: smallest key above x_(lo)'s 22-bit bucket
+  uint32_t fb_prefix[2];           // radix route: key prefix after the first and second digit
+  int64_t fb_rem[2];               //   rank left inside that prefix
+  unsigned long long fb_lt[2];     //   entries below that prefix
+  unsigned long long fb_sum_c, fb_sum_c2;
+};
+
+__device__ __forceinline__ uint32_t mbcnt(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+// LDS histogram update by a wave: the lanes that share the leading active
+// lane's bin add with one atomic, the rest one by one.  act = ballot(valid).
+__device__ __forceinline__ void hist_add_act(uint32_t* s_h, uint64_t act, bool valid, uint32_t bin) {
+  const int lead = __builtin_ctzll(act);
+  const uint32_t lb = (uint32_t)__builtin_amdgcn_readlane((int)bin, lead);
+  const uint64_t same = __builtin_amdgcn_ballot_w64(valid && bin == lb);
+  const int lane = threadIdx.x & 63;
+  if (lane == lead) atomicAdd(&s_h[lb], (uint32_t)__builtin_popcountll(same));
+  else if (valid && bin != lb) atomicAdd(&s_h[bin], 1u);
+}
+__device__ __forceinline__ void hist_add(uint32_t* s_h, bool valid, uint32_t bin) {
+  const uint64_t act = __builtin_amdgcn_ballot_w64(valid);
+  if (act) hist_add_act(s_h, act, valid, bin);
+}
+
+// For a histogram hh[0, nb) (LDS or global) and 0-based ranks r0, r1 below
+// its total: the bins holding them (s_bin[0], s_bin[1]), their positions
+// inside those bins (s_pos[0], s_pos[1]) and the first non-empty bin above
+// s_bin[0] (s_bin[2], kNone if none).  A 64-bit block prefix over NT
+// threads, kBins / NT bins each.  Called by the whole workgroup.
+template <int NT>
+__device__ void locate_ranks(const uint32_t* hh, int nb, int64_t r0, int64_t r1, int64_t* s_tot, uint32_t* s_bin,
+                             int64_t* s_pos) {
+  constexpr int BPT = kBins / NT;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  __syncthreads();                 // earlier readers of s_bin / s_pos are done
+  uint32_t c[BPT];
+  int64_t mine = 0;
+#pragma unroll
+  for (int i = 0; i < BPT; ++i) {
+    const int b = t * BPT + i;
+    c[i] = b < nb ? hh[b] : 0u;
+    mine += c[i];
+  }
+  int64_t x = mine;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int64_t y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  if (lane == 63) s_tot[wave] = x;
+  if (t == 0) {
+    s_bin[0] = s_bin[1] = (uint32_t)(nb - 1);
+    s_bin[2] = kNone;
+    s_pos[0] = s_pos[1] = 0;
+  }
+  __syncthreads();
+  int64_t before = x - mine;
+  for (int w = 0; w < wave; ++w) before += s_tot[w];
+#pragma unroll
+  for (int i = 0; i < BPT; ++i) {
+    const int64_t b0 = before, b1 = before + c[i];   // ranks [b0, b1) fall in this bin
+    if (b0 <= r0 && r0 < b1) { s_bin[0] = t * BPT + i; s_pos[0] = r0 - b0; }
+    if (b0 <= r1 && r1 < b1) { s_bin[1] = t * BPT + i; s_pos[1] = r1 - b0; }
+    before = b1;
+  }
+  __syncthreads();
+  const uint32_t b = s_bin[0];
+  uint32_t nxt = kNone;
+#pragma unroll
+  for (int i = 0; i < BPT; ++i)
+    if ((uint32_t)(t * BPT + i) > b && c[i] != 0u) nxt = min(nxt, (uint32_t)(t * BPT + i));
+  for (int off = 32; off > 0; off >>= 1) nxt = min(nxt, (uint32_t)__shfl_xor((int)nxt, off));
+  if (lane == 0 && nxt != kNone) atomicMin(&s_bin[2], nxt);
+  __syncthreads();
+}
+
+// Sum over a workgroup of 256 threads (4 waves); s holds 4 partials.
+__device__ __forceinline__ unsigned long long block_sum256(unsigned long long v, unsigned long long* s) {
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) s[threadIdx.x >> 6] = v;
+  __syncthreads();
+  return s[0] + s[1] + s[2] + s[3];
+}
+
+// Eq. 4 from exact integer sums: sqrt(E[C^2] - E[C]^2) / E[C].
+__device__ __forceinline__ float cv_value(unsigned long long s1, unsigned long long s2, int64_t n_keys) {
+  const double N = (double)n_keys;
+  const double mu = (double)s1 / N;
+  if (mu == 0.0) return 0.f;
+  double var = (double)s2 / N - mu * mu;
+  var = var < 0.0 ? 0.0 : var;
+  return (float)(sqrt(var) / mu);
+}
+
+// Called by thread 0 of every workgroup of the launch that ends head h, after
+// its own additions to *sum_c and *sum_c2: the last to arrive writes the
+// score.  Nothing waits; the sums are read with atomics, after a fence.
+__device__ void arrive_and_finish(CvState& S, unsigned long long* sum_c, unsigned long long* sum_c2, int64_t n_keys,
+                                  float* cv_out, int h) {
+  __threadfence();
+  const uint32_t done = atomicAdd(&S.arrive_f, 1u);
+  if (done == gridDim.x - 1) {
+    __threadfence();
+    const unsigned long long s1 = atomicAdd(sum_c, 0ull), s2 = atomicAdd(sum_c2, 0ull);
+    cv_out[h] = cv_value(s1, s2, n_keys);
+  }
+}
+
+// Phi = alpha (x_lo + frac (x_hi - x_lo)) in fp64 (Eq. 2 with the
+// interpolated percentile).
+__device__ __forceinline__ double phi_of(double xlo, double xhi, int64_t N, double k_pct, double alpha, int64_t lo) {
+  const double pos = (double)(N - 1) * k_pct;
+  const double frac = pos - (double)lo;
+  return alpha * (xlo + frac * (xhi - xlo));
+}
+
+// ---------------------------------------------------------------------------
+// 1. Sample: state, and the bracket from 8192 entries of A in runs of 8
+// ---------------------------------------------------------------------------
+
+// The sample's first two radix digits give the 22-bit key prefixes holding
+// sample ranks lo s / N -+ (8 sigma + 32), sigma the binomial spread of a
+// sample rank; the bracket is every key with a prefix in that range.  Phi's
+// range follows from the bracket's floats, widened by 2^-40 relative (far
+// beyond the rounding of the fp64 interpolation) and rounded outward to floats.
+constexpr int kSampleThreads = 1024;
+constexpr int kSamplePer = 8;
+constexpr int64_t kSampleSize = kSampleThreads * kSamplePer;
+
+__global__ __launch_bounds__(kSampleThreads) void cv_sample_kernel(const float* __restrict__ A, int64_t N,
+                                                                   double k_pct, double alpha, CvState* st,
+                                                                   uint32_t* __restrict__ hist, int hkv) {
+  __shared__ uint32_t s_h[kBins];
+  __shared__ uint32_t s_h2[2][kBins];
+  __shared__ int64_t s_tot[kSampleThreads / 64];
+  __shared__ uint32_t s_bin[3];
+  __shared__ int64_t s_pos[2];
+  const int h = blockIdx.x;
+  const int t = threadIdx.x;
+  for (int p = 0; p < 4; ++p)
+    for (int i = t; i < kBins; i += kSampleThreads) hist[((size_t)p * hkv + h) * kBins + i] = 0;
+  for (int i = t; i < kBins; i += kSampleThreads) s_h[i] = 0;
+  for (int i = t; i < 2 * kBins; i += kSampleThreads) s_h2[i / kBins][i % kBins] = 0;
+  const int64_t rank = (int64_t)floor((double)(N - 1) * k_pct);
+  __syncthreads();
+  const int64_t ns = N < kSampleSize ? N : kSampleSize;
+  const int64_t stride = N < kSampleSize ? kSamplePer : (N / kSampleThreads) & ~(int64_t)(kSamplePer - 1);
+  const float* Ah = A + (size_t)h * N;
+  float v[kSamplePer];
+#pragma unroll
+  for (int u = 0; u < kSamplePer; ++u) v[u] = Ah[std::min<int64_t>((int64_t)t * stride + u, N - 1)];
+#pragma unroll
+  for (int u = 0; u < kSamplePer; ++u) hist_add(s_h, (int64_t)t * stride + u < N, ord_key(v[u]) >> 21);
+  const double rs = (double)rank * (double)ns / (double)N;
+  const double pq = (double)rank / (double)N;
+  const double m = 8.0 * sqrt((double)ns * pq * (1.0 - pq)) + 32.0;
+  const int64_t lo_s = (int64_t)fmax(0.0, floor(rs - m)), hi_s = (int64_t)fmin((double)(ns - 1), ceil(rs + m));
+  locate_ranks<kSampleThreads>(s_h, kBins, lo_s, hi_s, s_tot, s_bin, s_pos);
+  const uint32_t bl = s_bin[0], bh = s_bin[1];
+  const int64_t rl = s_pos[0], rh = s_pos[1];
+#pragma unroll
+  for (int u = 0; u < kSamplePer; ++u) {
+    const bool ok = (int64_t)t * stride + u < N;
+    const uint32_t key = ord_key(v[u]);
+    if (ok && (key >> 21) == bl) atomicAdd(&s_h2[0][(key >> 10) & 0x7FF], 1u);
+    if (ok && (key >> 21) == bh) atomicAdd(&s_h2[1][(key >> 10) & 0x7FF], 1u);
+  }
+  locate_ranks<kSampleThreads>(s_h2[0], kBins, rl, rl, s_tot, s_bin, s_pos);
+  const uint32_t d_lo = s_bin[0];
+  locate_ranks<kSampleThreads>(s_h2[1], kBins, rh, rh, s_tot, s_bin, s_pos);
+  const uint32_t d_hi = s_bin[0];
+  if (t == 0) {
+    CvState& s = st[h];
+    const uint32_t p_lo = (bl << 11) | d_lo, p_hi = (bh << 11) | d_hi;
+    const uint32_t k_lo = p_lo << 10;
+    const uint32_t k_hi = p_hi == 0x3FFFFFu ? 0xFFFFFFFFu : ((p_hi + 1) << 10) - 1;
+    const float f_lo = key_to_float(k_lo);
+    float f_hi = k_hi == 0xFFFFFFFFu ? INFINITY : key_to_float(k_hi + 1);
+    if (f_hi != f_hi) f_hi = INFINITY;     // the bracket reaches the top of the finite floats
+    const double dl = alpha * (double)f_lo - fabs(alpha * (double)f_lo) * 0x1p-40;
+    const double dh = alpha * (double)f_hi + fabs(alpha * (double)f_hi) * 0x1p-40;
+    float tl = (float)dl, th = (float)dh;
+    if ((double)tl > dl) tl = nextafterf(tl, -INFINITY);
+    if ((double)th < dh) th = nextafterf(th, INFINITY);
+    const uint32_t span = k_hi - k_lo;
+    const int bits = span ? 32 - __clz((int)span) : 0;
+    s.rank = rank;
+    s.k_lo = k_lo;
+    s.k_hi = k_hi;
+    s.t_lo = tl;
+    s.t_hi = th;
+    s.shift1 = bits > 11 ? bits - 11 : 0;
+    s.phi_over = 0;
+    s.n_cand = 0;
+    s.below_br = 0;
+    s.sum_c = 0;
+    s.sum_c2 = 0;
+    s.phi = 0.0;
+    s.min2 = kNone;
+    s.n_list = 0;
+    s.arrive_r = 0;
+    s.arrive_f = 0;
+    s.fb_min = kNone;
+    s.fb_prefix[0] = s.fb_prefix[1] = 0;
+    s.fb_rem[0] = s.fb_rem[1] = 0;
+    s.fb_lt[0] = s.fb_lt[1] = 0;
+    s.fb_sum_c = 0;
+    s.fb_sum_c2 = 0;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// 2. The bracketing pass over A, column by column
+// ---------------------------------------------------------------------------
+
+// Workgroup x owns column blocks x, x + cb, x + 2 cb, ... (64 columns each);
+// its waves take turns over them, and a wave walks all lq rows of its block
+// itself (one column per lane, each row read 256 contiguous bytes, 16 rows
+// loaded together per step), so a column's count stays in its lane.  Per
+// entry: below the bracket (counted), at or above t_hi (counted for the
+// column), inside the union of the bracket and Phi's range (staged in LDS as
+// (value, the column's index among the workgroup's columns)).  A wave writes
+// its stage out in one run to the workgroup's own share of the pair buffer
+// before a step that would overflow it; the entries written out that lie in
+// the bracket are counted and enter the workgroup's histogram of the first
+// digit then, 64 at a time.  Entries are probabilities (A >= +0), so the
+// floats compare like their keys.
+constexpr int kStepRows = 16;     // rows per lane loaded together
+constexpr int kCountRows = 16;    // the same for the radix route's column walk
+constexpr int kStage = 512;       // pairs a wave stages
+
+// Column walk: ~2048 workgroups over all heads, and enough that none owns
+// more than 8192 columns.
+int64_t col_blocks(int64_t n_keys, int hkv) {
+  const int64_t blocks = (n_keys + 63) / 64;
+  const int64_t want = std::max<int64_t>(256, 2048 / std::max(1, hkv));
+  return std::max<int64_t>(1, std::max(std::min(blocks, want), (blocks + 127) / 128));
+}
+
+__device__ __forceinline__ float bracket_top(uint32_t k_hi) {   // first float above the bracket's keys
+  const float f = k_hi == kNone ? INFINITY : key_to_float(k_hi + 1);
+  return f != f ? INFINITY : f;
+}
+
+__global__ __launch_bounds__(256) void cv_bracket_kernel(const float* __restrict__ A, int lq, int64_t n_keys,
+                                                         CvState* st, uint32_t* __restrict__ hist0,
+                                                         uint2* __restrict__ pairs, uint32_t* __restrict__ pfill,
+                                                         uint32_t capw, uint32_t* __restrict__ colcnt) {
+  __shared__ uint32_t s_h[kBins];
+  __shared__ uint2 s_pair[4][kStage];
+  __shared__ uint32_t s_fill;
+  __shared__ unsigned long long s_red[4];
+  const int h = blockIdx.y;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  CvState& S = st[h];
+  for (int i = threadIdx.x; i < kBins; i += 256) s_h[i] = 0;
+  if (threadIdx.x == 0) s_fill = 0;
+  const uint32_t k_lo = S.k_lo, span = S.k_hi - S.k_lo;
+  const float f_lo = key_to_float(k_lo), f_hi = bracket_top(S.k_hi);
+  const float t_lo = S.t_lo, t_hi = S.t_hi;
+  const float u_lo = fminf(f_lo, t_lo), u_hi = fmaxf(f_hi, t_hi);
+  const int sh1 = S.shift1;
+  __syncthreads();
+  const size_t wg = (size_t)h * gridDim.x + blockIdx.x;
+  uint2* ph = pairs + wg * capw;
+  uint32_t np = 0, nin = 0;        // wave-uniform: staged pairs, bracket entries written out
+  uint32_t below = 0;
+  unsigned long long a1 = 0, a2 = 0;
+  // reserve n slots of the workgroup's share (one LDS atomic per wave)
+  auto reserve = [&](uint32_t n) {
+    uint32_t base = 0;
+    if (lane == 0) base = atomicAdd(&s_fill, n);
+    return __shfl(base, 0);
+  };
+  auto flush = [&]() {
+    for (uint32_t i = lane; i < ((np + 63) & ~63u); i += 64) {
+      const uint32_t o = i < np ? (s_pair[wave][i].x | 0x80000000u) - k_lo : kNone;
+      const bool in = o <= span;
+      nin += (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(in));
+      hist_add(s_h, in, o >> sh1);
+    }
+    const uint32_t base = reserve(np);
+    for (uint32_t i = lane; i < np; i += 64)
+      if (base + i < capw) ph[base + i] = s_pair[wave][i];
+    np = 0;
+  };
+  const float* Ah = A + (size_t)h * lq * n_keys;
+  const int64_t blocks = (n_keys + 63) / 64;
+  const int kb = (int)((blocks - blockIdx.x + gridDim.x - 1) / gridDim.x);   // blocks of this workgroup
+  const int nch = (lq + kStepRows - 1) / kStepRows;                          // row steps per block
+  const int nq = (kb > wave ? (kb - wave + 3) / 4 : 0) * nch;                // this wave's steps
+  unsigned int c = 0;
+  for (int q = 0; q < nq; ++q) {
+    // step q: block k = wave + 4 (q / nch), rows [kStepRows (q % nch), +kStepRows)
+    const int k = wave + 4 * (q / nch), i0 = (q % nch) * kStepRows;
+    const int64_t j = ((int64_t)blockIdx.x + (int64_t)k * gridDim.x) * 64 + lane;
+    const bool jv = j < n_keys;
+    // every load issued (clamped to the last column and row), then used
+    const float* p = Ah + std::min<int64_t>(j, n_keys - 1);
+    float v[kStepRows];
+#pragma unroll
+    for (int u = 0; u < kStepRows; ++u) v[u] = p[(size_t)std::min(i0 + u, lq - 1) * n_keys];
+    // a lane past the last column meets thresholds no entry reaches
+    const float lo_u = jv ? u_lo : INFINITY, lo_b = jv ? f_lo : 0.f, hi_c = jv ? t_hi : INFINITY;
+    uint64_t bu[kStepRows];
+    uint32_t tu = 0;
+#pragma unroll
+    for (int u = 0; u < kStepRows; ++u) {
+      const bool row = i0 + u < lq;          // uniform
+      const float x = v[u];
+      c += row && x >= hi_c;
+      below += row && x < lo_b;
+      bu[u] = __builtin_amdgcn_ballot_w64(row && x >= lo_u && x < u_hi);
+      tu += (uint32_t)__builtin_popcountll(bu[u]);
+    }
+    if (tu) {
+      const uint32_t local = (uint32_t)k * 64 + lane;
+      if (np + tu > (uint32_t)kStage) flush();
+      if (tu <= (uint32_t)kStage) {
+#pragma unroll
+        for (int u = 0; u < kStepRows; ++u) {
+          if ((bu[u] >> lane) & 1) s_pair[wave][np + mbcnt(bu[u])] = make_uint2(__float_as_uint(v[u]), local);
+          np += (uint32_t)__builtin_popcountll(bu[u]);
+        }
+      } else {             // more than a stage in one step (heavy ties): straight out, then counted
+        uint32_t base = reserve(tu);
+#pragma unroll
+        for (int u = 0; u < kStepRows; ++u) {
+          const bool in_u = (bu[u] >> lane) & 1;
+          const uint32_t at = base + mbcnt(bu[u]);
+          if (in_u && at < capw) ph[at] = make_uint2(__float_as_uint(v[u]), local);
+          const uint32_t o = in_u ? (__float_as_uint(v[u]) | 0x80000000u) - k_lo : kNone;
+          nin += (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(o <= span));
+          hist_add(s_h, o <= span, o >> sh1);
+          base += (uint32_t)__builtin_popcountll(bu[u]);
+        }
+      }
+    }
+    if (q % nch == nch - 1) {      // the block's last rows: the column count is complete
+      if (jv) {
+        colcnt[(size_t)h * n_keys + j] = c;
+        a1 += c;
+        a2 += (unsigned long long)c * c;
+      }
+      c = 0;
+    }
+  }
+  if (np) flush();
+  const unsigned long long tb = block_sum256(below, s_red);
+  const unsigned long long t1 = block_sum256(a1, s_red);
+  const unsigned long long t2 = block_sum256(a2, s_red);
+  const unsigned long long tn = block_sum256(lane == 0 ? nin : 0u, s_red);
+  if (threadIdx.x == 0) {
+    if (tb) atomicAdd(&S.below_br, tb);
+    if (tn) atomicAdd(&S.n_cand, tn);
+    if (t1) {
+      atomicAdd(&S.sum_c, t1);
+      atomicAdd(&S.sum_c2, t2);
+    }
+    pfill[wg] = min(s_fill, capw);
+    if (s_fill > capw) atomicOr(&S.phi_over, 1u);
+  }
+  for (int i = threadIdx.x; i < kBins; i += 256)
+    if (s_h[i]) atomicAdd(&hist0[(size_t)h * kBins + i], s_h[i]);
+}
+
+// The head takes the bracket route when the bracket holds ranks lo and lo + 1
+// (lo only, when lo = N - 1) and every gathered pair fit its buffer.
+// Decided alike by every launch after the bracketing pass.
+__device__ __forceinline__ bool bracket_route(const CvState& S, int64_t N) {
+  const int64_t lo = S.rank;
+  const unsigned long long top = (unsigned long long)(lo + 1 <= N - 1 ? lo + 1 : lo);
+  return S.phi_over == 0 && S.below_br <= (unsigned long long)lo && top < S.below_br + S.n_cand;
+}
+
+// ---------------------------------------------------------------------------
+// 3. Bracket route: workgroup x takes the pairs of column-walk workgroups
+//    [kRegions x, kRegions (x + 1)) and lists the bracket entries in
+//    x_(lo)'s first-digit bin; it also keeps the smallest bracket entry above
+//    that bin.  The last workgroup of a head to finish takes x_(lo), x_(lo+1)
+//    and Phi.  Radix route: histogram of the top key digit over A.
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ void hist_over_A(const float* __restrict__ Ah, int64_t N, uint32_t* s_h, uint32_t mask,
+                                            uint32_t want, int shift, uint32_t dmask, uint32_t above, uint32_t* mn) {
+  const int64_t n4 = (N & 3) == 0 && ((reinterpret_cast<uintptr_t>(Ah) & 15) == 0) ? N / 4 : 0;
+  const int64_t step = (int64_t)gridDim.x * blockDim.x;
+  auto visit = [&](float f) {
+    const uint32_t key = ord_key(f);
+    hist_add(s_h, (key & mask) == want, (key >> shift) & dmask);
+    if ((key & mask) > above) *mn = min(*mn, key);
+  };
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += step) {
+    const float4 v = *reinterpret_cast<const float4*>(Ah + 4 * i);
+    visit(v.x);
+    visit(v.y);
+    visit(v.z);
+    visit(v.w);
+  }
+  for (int64_t i = 4 * n4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N; i += step) visit(Ah[i]);
+}
+
+__device__ __forceinline__ void flush_hist(const uint32_t* s_h, uint32_t* __restrict__ g) {
+  for (int i = threadIdx.x; i < kBins; i += blockDim.x)
+    if (s_h[i]) atomicAdd(&g[i], s_h[i]);
+}
+
+constexpr int kListCap = 65536;    // entries of x_(lo)'s first-digit bin listed, at most
+constexpr int kRegions = 2;        // pair buffers per listing workgroup
+constexpr int kShortList = 1024;   // lists resolved by counting ranks
+constexpr int kListStage = 2048;   // entries staged before a reservation (a round adds <= 1024)
+
+// Offsets key - k_lo of one workgroup's gathered pairs, 4 per thread and
+// round (the same trip count on every lane); f(inside the bracket, offset).
+template <typename F>
+__device__ __forceinline__ void for_pairs(const uint2* __restrict__ ph, uint32_t fill, uint32_t k_lo, uint32_t span,
+                                          F&& f) {
+  for (uint32_t i0 = 0; i0 < fill; i0 += 4 * 256) {
+    uint32_t o[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {   // every load issued (clamped), then used
+      const uint32_t i = i0 + u * 256 + threadIdx.x;
+      const uint32_t x = ph[min(i, fill - 1)].x;
+      o[u] = i < fill ? (x | 0x80000000u) - k_lo : kNone;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) f(o[u] <= span, o[u]);
+  }
+}
+
+// x_(lo) and the key after it, by the last listing workgroup of a head: its
+// offset key - k_lo is b1's bin (first digit) followed by the rank-rem entry
+// of the list.  A short list is resolved by counting each entry's rank (LDS
+// broadcasts), a longer one by its remaining digits, 11 bits at a time (over
+// every workgroup's pairs again if the list overflowed).  The list, its
+// count and min2 are read with atomic loads.  Returns (in thread 0) Phi.
+__device__ double resolve_phi(CvState& S, const uint32_t* __restrict__ hist0, const uint32_t* __restrict__ lh,
+                              const uint2* __restrict__ pairs, const uint32_t* __restrict__ pfill, uint32_t capw,
+                              int cb, int h, int64_t N, double k_pct, double alpha, uint32_t b1, uint32_t next1,
+                              int64_t rem, unsigned long long lt, uint32_t* s_h, int64_t* s_tot, uint32_t* s_bin,
+                              int64_t* s_pos, uint32_t* s_x) {
+  const int t = threadIdx.x, lane = t & 63;
+  const int64_t lo = S.rank;
+  const uint32_t k_lo = S.k_lo, span = S.k_hi - S.k_lo;
+  const int sh1 = S.shift1;
+  uint32_t P = b1, eq = 0, next = next1;
+  if (sh1 == 0) {
+    eq = hist0[(size_t)h * kBins + b1];
+  } else {
+    const uint32_t nl = __hip_atomic_load(&S.n_list, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint32_t min2 = __hip_atomic_load(&S.min2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (nl <= (uint32_t)kShortList) {
+      uint32_t* s_l = s_h;
+      __syncthreads();
+      for (uint32_t i = t; i < nl; i += 256) s_l[i] = __hip_atomic_load(&lh[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (t == 0) {
+        s_x[0] = kNone;
+        s_x[3] = kNone;
+      }
+      __syncthreads();
+      for (uint32_t i = t; i < nl; i += 256) {
+        const uint32_t e = s_l[i];
+        uint32_t n_lt = 0, n_eq = 0;
+        for (uint32_t m = 0; m < nl; ++m) {
+          const uint32_t f = s_l[m];
+          n_lt += f < e;
+          n_eq += f == e;
+        }
+        if ((int64_t)n_lt <= rem && rem < (int64_t)(n_lt + n_eq)) {   // every entry of the run writes the same
+          s_x[0] = e;
+          s_x[1] = n_lt;
+          s_x[2] = n_eq;
+        }
+      }
+      __syncthreads();
+      const uint32_t x = s_x[0];
+      uint32_t mn = kNone;
+      for (uint32_t i = t; i < nl; i += 256)
+        if (s_l[i] > x) mn = min(mn, s_l[i]);
+      for (int off = 32; off > 0; off >>= 1) mn = min(mn, (uint32_t)__shfl_xor((int)mn, off));
+      if (lane == 0 && mn != kNone) atomicMin(&s_x[3], mn);
+      __syncthreads();
+      P = x;
+      lt += s_x[1];
+      eq = s_x[2];
+      next = min(s_x[3], min2);
+    } else {
+      const bool from_list = nl <= (uint32_t)kListCap;
+      int bits = sh1;
+      while (bits > 0) {
+        const int d = bits > 11 ? 11 : bits;
+        const int nsh = bits - d;
+        const uint32_t dmask = (1u << d) - 1u;
+        const bool last = nsh == 0;
+        __syncthreads();
+        for (int i = t; i < kBins; i += 256) s_h[i] = 0;
+        if (t == 0) s_x[3] = kNone;
+        __syncthreads();
+        uint32_t mn = kNone;
+        auto visit = [&](bool ok, uint32_t o) {
+          const uint32_t hi = o >> bits;
+          hist_add(s_h, ok && hi == P, (o >> nsh) & dmask);
+          if (last && ok && hi > P) mn = min(mn, o);
+        };
+        if (from_list) {
+          for (uint32_t k0 = 0; k0 < nl; k0 += 4 * 256) {
+            uint32_t o[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const uint32_t x =
+                  __hip_atomic_load(&lh[min(k0 + u * 256 + t, nl - 1)], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              o[u] = k0 + u * 256 + t < nl ? x : kNone;
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) visit(o[u] != kNone, o[u]);
+          }
+        } else {
+          for (int r = 0; r < cb; ++r) {
+            const size_t wr = (size_t)h * cb + r;
+            for_pairs(pairs + wr * capw, pfill[wr], k_lo, span, visit);
+          }
+        }
+        for (int off = 32; off > 0; off >>= 1) mn = min(mn, (uint32_t)__shfl_xor((int)mn, off));
+        if (lane == 0 && mn != kNone) atomicMin(&s_x[3], mn);
+        locate_ranks<256>(s_h, 1 << d, rem, rem, s_tot, s_bin, s_pos);
+        const uint32_t b = s_bin[0];
+        lt += (unsigned long long)(rem - s_pos[0]);
+        rem = s_pos[0];
+        P = (P << d) | b;
+        if (last) {
+          eq = s_h[b];
+          next = s_bin[2] != kNone ? ((P & ~dmask) | s_bin[2]) : min(s_x[3], min2);
+        }
+        bits = nsh;
+      }
+    }
+  }
+  const double xlo = (double)key_to_float(k_lo + P);
+  double xhi = xlo;
+  if ((int64_t)(lt + eq) < lo + 2 && lo + 1 <= N - 1 && next != kNone) xhi = (double)key_to_float(k_lo + next);
+  return phi_of(xlo, xhi, N, k_pct, alpha, lo);
+}
+
+__global__ __launch_bounds__(256) void cv_list_kernel(const float* __restrict__ A, int64_t N, CvState* st,
+                                                      const uint32_t* __restrict__ hist0, uint32_t* __restrict__ hist1,
+                                                      const uint2* __restrict__ pairs,
+                                                      const uint32_t* __restrict__ pfill, uint32_t capw, int cb,
+                                                      uint32_t* __restrict__ list, double k_pct, double alpha) {
+  __shared__ uint32_t s_h[kBins];
+  __shared__ int64_t s_tot[4];
+  __shared__ uint32_t s_bin[3];
+  __shared__ int64_t s_pos[2];
+  __shared__ uint32_t s_min;
+  __shared__ uint32_t s_stage[kListStage];
+  __shared__ uint32_t s_nl, s_lbase;
+  __shared__ uint32_t s_x[4];
+  __shared__ int s_last;
+  const int h = blockIdx.y;
+  const int t = threadIdx.x, lane = t & 63;
+  CvState& S = st[h];
+  if (!bracket_route(S, N)) {
+    for (int i = t; i < kBins; i += 256) s_h[i] = 0;
+    __syncthreads();
+    uint32_t mn = kNone;
+    hist_over_A(A + (size_t)h * N, N, s_h, 0u, 0u, 21, 0x7FFu, kNone, &mn);
+    __syncthreads();
+    flush_hist(s_h, hist1 + (size_t)h * kBins);
+    return;
+  }
+  const int sh1 = S.shift1;
+  const int nwg = sh1 == 0 ? 1 : (cb + kRegions - 1) / kRegions;
+  if ((int)blockIdx.x >= nwg) return;
+  const uint32_t k_lo = S.k_lo, span = S.k_hi - S.k_lo;
+  const unsigned long long below = S.below_br;
+  const int64_t rem0 = S.rank - (int64_t)below;
+  locate_ranks<256>(hist0 + (size_t)h * kBins, kBins, rem0, rem0, s_tot, s_bin, s_pos);
+  const uint32_t b1 = s_bin[0], next1 = s_bin[2];
+  const int64_t rem1 = s_pos[0];
+  uint32_t* lh = list + (size_t)h * kListCap;
+  if (sh1 > 0) {
+    if (t == 0) {
+      s_nl = 0;
+      s_min = kNone;
+    }
+    __syncthreads();
+    uint32_t mn = kNone;
+    auto out = [&]() {             // the staged entries to the list, one reservation
+      const uint32_t nst = s_nl;
+      if (nst) {
+        if (t == 0) s_lbase = atomicAdd(&S.n_list, nst);
+        __syncthreads();
+        // atomic writes: each entry is at the coherence point when it returns
+        for (uint32_t i = t; i < nst; i += 256)
+          if (s_lbase + i < (uint32_t)kListCap) atomicExch(&lh[s_lbase + i], s_stage[i]);
+      }
+      __syncthreads();
+      if (t == 0) s_nl = 0;
+      __syncthreads();
+    };
+    const int r0 = blockIdx.x * kRegions, r1 = min(cb, r0 + kRegions);
+    for (int r = r0; r < r1; ++r) {
+      const size_t wr = (size_t)h * cb + r;
+      const uint2* ph = pairs + wr * capw;
+      const uint32_t fill = pfill[wr];
+      for (uint32_t i0 = 0; i0 < fill; i0 += 4 * 256) {   // the same trip count on every lane
+        uint32_t o[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {   // every load issued (clamped), then used
+          const uint32_t i = i0 + u * 256 + t;
+          const uint32_t x = ph[min(i, fill - 1)].x;
+          o[u] = i < fill ? (x | 0x80000000u) - k_lo : kNone;
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const bool ok = o[u] <= span;
+          const bool in = ok && (o[u] >> sh1) == b1;
+          if (ok && (o[u] >> sh1) > b1) mn = min(mn, o[u]);
+          const uint64_t bal = __builtin_amdgcn_ballot_w64(in);
+          if (bal) {
+            uint32_t base = 0;
+            if (lane == 0) base = atomicAdd(&s_nl, (uint32_t)__builtin_popcountll(bal));
+            base = __shfl(base, 0) + mbcnt(bal);
+            if (in) s_stage[base] = o[u];
+          }
+        }
+        __syncthreads();
+        if (s_nl > (uint32_t)(kListStage - 4 * 256)) out();   // room for the next round
+      }
+    }
+    out();
+    for (int off = 32; off > 0; off >>= 1) mn = min(mn, (uint32_t)__shfl_xor((int)mn, off));
+    if (lane == 0 && mn != kNone) atomicMin(&s_min, mn);
+    __syncthreads();
+    if (t == 0 && s_min != kNone) atomicMin(&S.min2, s_min);
+  }
+  // arrival once this workgroup's list entries, minimum and count have all
+  // completed (device-scope atomics, waited for); the last one takes Phi
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (t == 0) s_last = atomicAdd(&S.arrive_r, 1u) == (uint32_t)nwg - 1;
+  __syncthreads();
+  if (!s_last) return;
+  const double phi = resolve_phi(S, hist0, lh, pairs, pfill, capw, cb, h, N, k_pct, alpha, b1, next1, rem1,
+                                 below + (unsigned long long)(rem0 - rem1), s_h, s_tot, s_bin, s_pos, s_x);
+  if (t == 0) S.phi = phi;
+}
+
+// ---------------------------------------------------------------------------
+// 4. Bracket route: each workgroup of the column walk adds its own gathered
+//    values in [Phi, t_hi) to its columns (LDS counts) and the change to the
+//    sums of C_j and C_j^2.  Radix route: the second key digit over A.
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(256) void cv_columns_kernel(const float* __restrict__ A, int64_t N, CvState* st,
+                                                         const uint32_t* __restrict__ hist1,
+                                                         uint32_t* __restrict__ hist2, const uint2* __restrict__ pairs,
+                                                         const uint32_t* __restrict__ pfill, uint32_t capw, int cb,
+                                                         const uint32_t* __restrict__ colcnt, int64_t n_keys) {
+  extern __shared__ uint32_t s_e[];   // max(columns owned, kBins) entries
+  __shared__ int64_t s_tot[4];
+  __shared__ uint32_t s_bin[3];
+  __shared__ int64_t s_pos[2];
+  __shared__ unsigned long long s_red[4];
+  const int h = blockIdx.y;
+  const int t = threadIdx.x;
+  CvState& S = st[h];
+  if (!bracket_route(S, N)) {
+    const int64_t rank = S.rank;
+    locate_ranks<256>(hist1 + (size_t)h * kBins, kBins, rank, rank, s_tot, s_bin, s_pos);
+    const uint32_t b0 = s_bin[0];
+    if (blockIdx.x == 0 && t == 0) {
+      S.fb_prefix[0] = b0 << 21;
+      S.fb_rem[0] = s_pos[0];
+      S.fb_lt[0] = (unsigned long long)(rank - s_pos[0]);
+    }
+    uint32_t* s_h = s_e;
+    for (int i = t; i < kBins; i += 256) s_h[i] = 0;
+    __syncthreads();
+    uint32_t mn = kNone;
+    hist_over_A(A + (size_t)h * N, N, s_h, 0xFFE00000u, b0 << 21, 10, 0x7FFu, kNone, &mn);
+    __syncthreads();
+    flush_hist(s_h, hist2 + (size_t)h * kBins);
+    return;
+  }
+  const double phi = S.phi;
+  const float t_hi = S.t_hi;
+  const int64_t blocks = (n_keys + 63) / 64;
+  const int nloc = (int)((blocks - blockIdx.x + cb - 1) / cb) * 64;   // this workgroup's columns
+  for (int i = t; i < nloc; i += 256) s_e[i] = 0;
+  __syncthreads();
+  const size_t wg = (size_t)h * cb + blockIdx.x;
+  const uint2* ph = pairs + wg * capw;
+  const uint32_t fill = pfill[wg];
+  for (uint32_t i0 = 0; i0 < fill; i0 += 4 * 256) {
+    uint2 e[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) e[u] = ph[min(i0 + u * 256 + t, fill - 1)];   // every load issued, then used
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float x = __uint_as_float(e[u].x);
+      if (i0 + u * 256 + t < fill && x < t_hi && (double)x >= phi)   // entries >= t_hi are in C already
+        atomicAdd(&s_e[e[u].y], 1u);
+    }
+  }
+  __syncthreads();
+  const uint32_t* cc = colcnt + (size_t)h * n_keys;
+  unsigned long long a1 = 0, a2 = 0;
+  for (int l = t; l < nloc; l += 256) {
+    const unsigned long long e = s_e[l];
+    if (e) {
+      const unsigned long long c = cc[((int64_t)blockIdx.x + (int64_t)(l >> 6) * cb) * 64 + (l & 63)];
+      a1 += e;
+      a2 += 2 * c * e + e * e;         // (c + e)^2 - c^2
+    }
+  }
+  const unsigned long long t1 = block_sum256(a1, s_red);
+  const unsigned long long t2 = block_sum256(a2, s_red);
+  if (t == 0 && t1) {
+    atomicAdd(&S.sum_c, t1);
+    atomicAdd(&S.sum_c2, t2);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// 5-6. Radix route: the last key digit over A (and the smallest key above
+//      x_(lo)'s 22-bit bucket), then Phi, C_j over A and the score.  The
+//      bracket route's score is written by the first of the two.
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(256) void cv_digit2_kernel(const float* __restrict__ A, int64_t N, CvState* st,
+                                                        const uint32_t* __restrict__ hist2,
+                                                        uint32_t* __restrict__ hist3, int64_t n_keys,
+                                                        float* __restrict__ cv_out) {
+  __shared__ uint32_t s_h[kBins];
+  __shared__ int64_t s_tot[4];
+  __shared__ uint32_t s_bin[3];
+  __shared__ int64_t s_pos[2];
+  __shared__ uint32_t s_min;
+  const int h = blockIdx.y;
+  CvState& S = st[h];
+  if (bracket_route(S, N)) {  // the bracket route's score, from the previous launch's sums
+    if (blockIdx.x == 0 && threadIdx.x == 0) cv_out[h] = cv_value(S.sum_c, S.sum_c2, n_keys);
+    return;
+  }
+  const int64_t rem0 = S.fb_rem[0];
+  locate_ranks<256>(hist2 + (size_t)h * kBins, kBins, rem0, rem0, s_tot, s_bin, s_pos);
+  const uint32_t prefix = S.fb_prefix[0] | (s_bin[0] << 10);
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    S.fb_prefix[1] = prefix;
+    S.fb_rem[1] = s_pos[0];
+    S.fb_lt[1] = S.fb_lt[0] + (unsigned long long)(rem0 - s_pos[0]);
+  }
+  for (int i = threadIdx.x; i < kBins; i += 256) s_h[i] = 0;
+  if (threadIdx.x == 0) s_min = kNone;
+  __syncthreads();
+  uint32_t mn = kNone;
+  hist_over_A(A + (size_t)h * N, N, s_h, 0xFFFFFC00u, prefix, 0, 0x3FFu, prefix, &mn);
+  for (int off = 32; off > 0; off >>= 1) mn = min(mn, (uint32_t)__shfl_xor((int)mn, off));
+  if ((threadIdx.x & 63) == 0 && mn != kNone) atomicMin(&s_min, mn);
+  __syncthreads();
+  flush_hist(s_h, hist3 + (size_t)h * kBins);
+  if (threadIdx.x == 0 && s_min != kNone) atomicMin(&S.fb_min, s_min);
+}
+
+__global__ __launch_bounds__(256) void cv_count_kernel(const float* __restrict__ A, int lq, int64_t n_keys,
+                                                       CvState* st, const uint32_t* __restrict__ hist3, double k_pct,
+                                                       double alpha, float* __restrict__ cv_out) {
+  __shared__ int64_t s_tot[4];
+  __shared__ uint32_t s_bin[3];
+  __shared__ int64_t s_pos[2];
+  __shared__ unsigned int s_c[4][64];
+  __shared__ unsigned long long s_red[4];
+  const int h = blockIdx.y;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  CvState& S = st[h];
+  const int64_t N = (int64_t)lq * n_keys;
+  if (bracket_route(S, N)) return;
+  const int64_t lo = S.rank, rem1 = S.fb_rem[1];
+  const uint32_t* hh = hist3 + (size_t)h * kBins;
+  locate_ranks<256>(hh, 1024, rem1, rem1, s_tot, s_bin, s_pos);
+  const uint32_t prefix = S.fb_prefix[1];
+  const uint32_t xk = prefix | s_bin[0];
+  const unsigned long long le = S.fb_lt[1] + (unsigned long long)(rem1 - s_pos[0]) + hh[s_bin[0]];
+  const uint32_t above = s_bin[2] != kNone ? (prefix | s_bin[2]) : S.fb_min;
+  const double xlo = (double)key_to_float(xk);
+  double xhi = xlo;
+  if ((int64_t)le < lo + 2 && lo + 1 <= N - 1 && above != kNone) xhi = (double)key_to_float(above);
+  const double phi = phi_of(xlo, xhi, N, k_pct, alpha, lo);
+  if (blockIdx.x == 0 && threadIdx.x == 0) S.phi = phi;
+  const float* Ah = A + (size_t)h * lq * n_keys;
+  const int rpg = (lq + 3) / 4;
+  const int r0 = min(lq, wave * rpg), r1 = min(lq, r0 + rpg);
+  unsigned long long a1 = 0, a2 = 0;
+  for (int64_t j0 = (int64_t)blockIdx.x * 64; j0 < n_keys; j0 += (int64_t)gridDim.x * 64) {
+    const int64_t j = j0 + lane;
+    unsigned int c = 0;
+    if (j < n_keys) {
+      for (int i0 = r0; i0 < r1; i0 += kCountRows) {
+        float v[kCountRows];
+#pragma unroll
+        for (int u = 0; u < kCountRows; ++u)
+          if (i0 + u < r1) v[u] = Ah[(size_t)(i0 + u) * n_keys + j];
+#pragma unroll
+        for (int u = 0; u < kCountRows; ++u)
+          if (i0 + u < r1) c += (double)v[u] >= phi;
+      }
+    }
+    s_c[wave][lane] = c;
+    __syncthreads();
+    if (wave == 0 && j < n_keys) {
+      const unsigned int cj = s_c[0][lane] + s_c[1][lane] + s_c[2][lane] + s_c[3][lane];
+      a1 += cj;
+      a2 += (unsigned long long)cj * cj;
+    }
+    __syncthreads();
+  }
+  const unsigned long long t1 = block_sum256(a1, s_red);
+  const unsigned long long t2 = block_sum256(a2, s_red);
+  if (threadIdx.x == 0) {
+    if (t1) {
+      atomicAdd(&S.fb_sum_c, t1);
+      atomicAdd(&S.fb_sum_c2, t2);
+    }
+    arrive_and_finish(S, &S.fb_sum_c, &S.fb_sum_c2, n_keys, cv_out, h);
+  }
+}
+
+// Gathered pairs: a sixteenth of A per head, split evenly over the
+// workgroups of the column walk (the union of bracket and Phi's range holds
+// about 1-2% of A at the sample's margins; a workgroup's overflow sends the
+// head the radix route).
+uint32_t pair_cap(int64_t N, int64_t cb) {
+  const int64_t c = std::max<int64_t>(256, ((N + 15) / 16 + cb - 1) / cb);
+  return (uint32_t)((c + 3) & ~(int64_t)3);
+}
+
+struct CvLayout {
+  size_t hist, list, pairs, pfill, colcnt, state, total;
+};
+size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
+CvLayout cv_layout(int hkv, int lq, int64_t n_keys) {
+  const int64_t N = (int64_t)lq * n_keys;
+  const int64_t cb = col_blocks(n_keys, hkv);
+  CvLayout L{};
+  size_t o = 0;
+  L.hist = o; o += al256((size_t)4 * hkv * kBins * sizeof(uint32_t));
+  L.list = o; o += al256((size_t)hkv * kListCap * sizeof(uint32_t));
+  L.pairs = o; o += al256((size_t)hkv * cb * pair_cap(N, cb) * sizeof(uint2));
+  L.pfill = o; o += al256((size_t)hkv * cb * sizeof(uint32_t));
+  L.colcnt = o; o += al256((size_t)hkv * n_keys * sizeof(uint32_t));
+  L.state = o; o += al256((size_t)hkv * sizeof(CvState));
+  L.total = o;
+  return L;
+}
+
+}  // namespace
+
+size_t cv_workspace_bytes(int hkv, int lq, int64_t n_keys) { return cv_layout(hkv, lq, n_keys).total; }
+
+hipError_t launch_cv(const float* A, int hkv, int lq, int64_t n_keys, double k_pct, double alpha, void* ws,
+                     float* cv_out, hipStream_t stream) {
+  const CvLayout L = cv_layout(hkv, lq, n_keys);
+  char* w = reinterpret_cast<char*>(ws);
+  const int64_t N = (int64_t)lq * n_keys;
+  const int64_t cb = col_blocks(n_keys, hkv);
+  const uint32_t capw = pair_cap(N, cb);
+  uint32_t* hist = reinterpret_cast<uint32_t*>(w + L.hist);
+  const size_t hs = (size_t)hkv * kBins;
+  uint32_t* list = reinterpret_cast<uint32_t*>(w + L.list);
+  uint2* pairs = reinterpret_cast<uint2*>(w + L.pairs);
+  uint32_t* pfill = reinterpret_cast<uint32_t*>(w + L.pfill);
+  uint32_t* colcnt = reinterpret_cast<uint32_t*>(w + L.colcnt);
+  CvState* st = reinterpret_cast<CvState*>(w + L.state);
+  // radix-route passes over A in entry order: enough workgroups per head to fill the device
+  const unsigned hb = (unsigned)std::max<int64_t>(1, std::min<int64_t>(512, (N + 1023) / 1024));
+  const int64_t blocks = (n_keys + 63) / 64;
+  const size_t col_lds = (size_t)std::max<int64_t>(kBins, (blocks + cb - 1) / cb * 64) * sizeof(uint32_t);
+  const unsigned lw = (unsigned)std::max<int64_t>(hb, (cb + kRegions - 1) / kRegions);
+  const dim3 walk((unsigned)cb, hkv), flat(hb, hkv);
+  hipLaunchKernelGGL(cv_sample_kernel, dim3(hkv), dim3(kSampleThreads), 0, stream, A, N, k_pct, alpha, st, hist, hkv);
+  hipLaunchKernelGGL(cv_bracket_kernel, walk, dim3(256), 0, stream, A, lq, n_keys, st, hist, pairs, pfill, capw, colcnt);
+  hipLaunchKernelGGL(cv_list_kernel, dim3(lw, hkv), dim3(256), 0, stream, A, N, st, hist, hist + hs, pairs, pfill, capw,
+                     (int)cb, list, k_pct, alpha);
+  hipLaunchKernelGGL(cv_columns_kernel, walk, dim3(256), col_lds, stream, A, N, st, hist + hs, hist + 2 * hs, pairs,
+                     pfill, capw, (int)cb, colcnt, n_keys);
+  hipLaunchKernelGGL(cv_digit2_kernel, flat, dim3(256), 0, stream, A, N, st, hist + 2 * hs, hist + 3 * hs, n_keys,
+                     cv_out);
+  hipLaunchKernelGGL(cv_count_kernel, walk, dim3(256), 0, stream, A, lq, n_keys, st, hist + 3 * hs, k_pct, alpha,
+                     cv_out);
+  return hipGetLastError();
+}
+
+}  // namespace catekv

@@ -453,365 +453,6 @@ __global__ void compact_kernel(CompactArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// CV: exact order statistics of the observation matrix, counts, score
-// ---------------------------------------------------------------------------
-
-struct CvState {                 // per KV head, in the workspace
-  uint32_t prefix;               // radix prefix of the order statistic x_(lo)
-  int64_t remaining;             // 0-based rank still to resolve inside the prefix (up to N - 1 >= 2^31)
-  uint32_t min_above_key;        // smallest ordered key strictly above x_(lo)
-  uint32_t need_scan;            // 1: min_above_key must come from a pass over A
-  unsigned long long cnt_lt;     // entries strictly below x_(lo)
-  double phi;
-  unsigned long long sum_c, sum_c2;
-  unsigned long long c0;         // entries in x_(lo)'s top-digit bin (known after the first pass)
-  uint32_t n_cand;               // those entries, gathered by the second pass when they fit
-};
-
-constexpr int kRadixBins = 2048;   // digits: bits [31:21], [20:10] (11 bits), [9:0] (10 bits)
-
-__device__ __forceinline__ int digit_shift(int pass) { return pass == 0 ? 21 : (pass == 1 ? 10 : 0); }
-__device__ __forceinline__ uint32_t digit_mask_above(int pass) {
-  return pass == 0 ? 0u : (pass == 1 ? 0xFFE00000u : 0xFFFFFC00u);
-}
-__device__ __forceinline__ float key_to_float(uint32_t key) {
-  return __uint_as_float((key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key);
-}
-
-__global__ void cv_init_kernel(CvState* st, uint32_t* hist, int64_t N, double k_pct, int hkv) {
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < 3 * hkv * kRadixBins; i += gridDim.x * blockDim.x)
-    hist[i] = 0;
-  if (blockIdx.x == 0 && threadIdx.x < hkv) {
-    CvState& s = st[threadIdx.x];
-    s.prefix = 0;
-    s.remaining = (int64_t)floor((double)(N - 1) * k_pct);
-    s.min_above_key = 0xFFFFFFFFu;
-    s.need_scan = 0;
-    s.cnt_lt = 0;
-    s.phi = 0.0;
-    s.sum_c = 0;
-    s.sum_c2 = 0;
-    s.c0 = 0;
-    s.n_cand = 0;
-  }
-}
-
-// Histogram of one radix digit over the entries whose higher digits match
-// the prefix found so far.  hist: [hkv][kRadixBins] for this pass.  The
-// probabilities of A crowd into a few digits, so each wave first counts the
-// lanes that share its leading lane's digit with one ballot and one atomic;
-// only the other lanes add one by one.  16-byte loads, 4 entries per lane.
-__device__ __forceinline__ void hist_add_act(uint32_t* s_h, uint64_t act, bool valid, uint32_t bin) {
-  const int lead = __builtin_ctzll(act);
-  const uint32_t lb = (uint32_t)__builtin_amdgcn_readlane((int)bin, lead);
-  const uint64_t same = __builtin_amdgcn_ballot_w64(valid && bin == lb);
-  const int lane = threadIdx.x & 63;
-  if (lane == lead) atomicAdd(&s_h[lb], (uint32_t)__builtin_popcountll(same));
-  else if (valid && bin != lb) atomicAdd(&s_h[bin], 1u);
-}
-__device__ __forceinline__ void hist_add(uint32_t* s_h, bool valid, uint32_t bin) {
-  const uint64_t act = __builtin_amdgcn_ballot_w64(valid);
-  if (act) hist_add_act(s_h, act, valid, bin);
-}
-
-// The entries of x_(lo)'s top-digit bin (c0 of them, counted by the first
-// pass) are all that the last two digits are resolved over.  When c0 fits the
-// candidate buffer (cap keys per head), the second pass also gathers them, so
-// the third pass and the search for the next key above x_(lo) read the
-// candidates instead of A.  Gathering rides on the histogram's own ballot:
-// a wave with no matching lane skips both.
-constexpr int kGatherWave = 512;     // candidates a wave stages in LDS before writing them out
-
-__global__ __launch_bounds__(256) void radix_hist_kernel(const float* __restrict__ A, int64_t N, int pass,
-                                                         CvState* st, uint32_t* __restrict__ hist,
-                                                         uint32_t* __restrict__ cand, uint32_t cap) {
-  __shared__ uint32_t s_h[kRadixBins];
-  __shared__ uint32_t s_buf[4][kGatherWave];
-  __shared__ uint32_t s_wc[4];
-  __shared__ uint32_t s_base;
-  const int h = blockIdx.y;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const bool use_cand = st[h].c0 <= (unsigned long long)cap;   // uniform over the launch for head h
-  const bool gather = pass == 1 && use_cand;
-  for (int i = threadIdx.x; i < kRadixBins; i += blockDim.x) s_h[i] = 0;
-  __syncthreads();
-  const uint32_t pm = digit_mask_above(pass), pv = st[h].prefix & pm;
-  const int shift = digit_shift(pass);
-  const uint32_t dmask = pass == 2 ? 0x3FFu : 0x7FFu;
-  uint32_t* ch = cand + (size_t)h * cap;
-  // a wave-uniform count of the wave's candidates (from the ballots, no
-  // atomics in the loop); a wave's stage holds kGatherWave, any beyond go
-  // straight to the buffer
-  uint32_t wcnt = 0;
-  auto visit = [&](bool match, uint32_t key) {
-    const uint64_t act = __builtin_amdgcn_ballot_w64(match);
-    if (act == 0) return;
-    hist_add_act(s_h, act, match, (key >> shift) & dmask);
-    if (gather) {
-      if (match) {
-        const uint32_t off = wcnt + (uint32_t)__builtin_popcountll(act & __lanemask_lt());
-        if (off < (uint32_t)kGatherWave) s_buf[wave][off] = key;
-        else ch[atomicAdd(&st[h].n_cand, 1u)] = key;
-      }
-      wcnt += (uint32_t)__builtin_popcountll(act);
-    }
-  };
-  if (pass == 2 && use_cand) {
-    const int64_t nc = st[h].n_cand;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nc;
-         i += (int64_t)gridDim.x * blockDim.x) {
-      const uint32_t key = ch[i];
-      hist_add(s_h, (key & pm) == pv, (key >> shift) & dmask);
-    }
-  } else {
-    const float* Ah = A + (size_t)h * N;
-    const int64_t n4 = (N & 3) == 0 && ((reinterpret_cast<uintptr_t>(Ah) & 15) == 0) ? N / 4 : 0;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4;
-         i += (int64_t)gridDim.x * blockDim.x) {
-      const float4 v = *reinterpret_cast<const float4*>(Ah + 4 * i);
-      const float f[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint32_t key = ord_key(f[e]);
-        visit((key & pm) == pv, key);
-      }
-    }
-    // entries not covered by the 16-byte loads (N not a multiple of 4, or an unaligned head)
-    for (int64_t i = 4 * n4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N;
-         i += (int64_t)gridDim.x * blockDim.x) {
-      const uint32_t key = ord_key(Ah[i]);
-      visit((key & pm) == pv, key);
-    }
-  }
-  if (gather && lane == 0) s_wc[wave] = min(wcnt, (uint32_t)kGatherWave);
-  __syncthreads();
-  for (int i = threadIdx.x; i < kRadixBins; i += blockDim.x)
-    if (s_h[i]) atomicAdd(&hist[(size_t)h * kRadixBins + i], s_h[i]);
-  if (gather) {
-    if (threadIdx.x == 0) {
-      const uint32_t tot = s_wc[0] + s_wc[1] + s_wc[2] + s_wc[3];
-      s_base = tot ? atomicAdd(&st[h].n_cand, tot) : 0u;
-    }
-    __syncthreads();
-    uint32_t dst = s_base;
-    for (int w = 0; w < wave; ++w) dst += s_wc[w];
-    for (uint32_t i = lane; i < s_wc[wave]; i += 64) ch[dst + i] = s_buf[wave][i];
-  }
-}
-
-// Pick the digit that holds the target rank: one 256-thread workgroup per
-// head, 8 bins per thread, a block scan of the per-thread sums.  The entries
-// of lower digits are strictly below x_(lo) and are counted.  After the last
-// pass the smallest key above x_(lo) is read off the same histogram when it
-// lies in x_(lo)'s bucket; otherwise a pass over A is requested.
-constexpr int kPickThreads = 256;
-__global__ __launch_bounds__(kPickThreads) void radix_pick_kernel(const uint32_t* __restrict__ hist, int pass,
-                                                                  CvState* st, int hkv) {
-  constexpr int BPT = kRadixBins / kPickThreads;
-  __shared__ int64_t s_tot[kPickThreads / 64];
-  __shared__ int s_bin;
-  __shared__ int64_t s_cum;
-  __shared__ uint32_t s_bcnt;
-  __shared__ int s_next;
-  const int h = blockIdx.x;
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const uint32_t* hh = hist + (size_t)h * kRadixBins;
-  const int nb = pass == 2 ? 1024 : kRadixBins;
-  const int64_t rem = st[h].remaining;
-  uint32_t c[BPT];
-  int64_t mine = 0;
-#pragma unroll
-  for (int i = 0; i < BPT; ++i) {
-    const int bin = t * BPT + i;
-    c[i] = bin < nb ? hh[bin] : 0u;
-    mine += c[i];
-  }
-  // exclusive prefix of `mine` over the workgroup
-  int64_t x = mine;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const int64_t y = __shfl_up(x, off);
-    if (lane >= off) x += y;
-  }
-  if (lane == 63) s_tot[wave] = x;
-  if (t == 0) { s_bin = -1; s_next = 0x7FFFFFFF; }
-  __syncthreads();
-  int64_t before = x - mine;
-#pragma unroll
-  for (int w = 0; w < kPickThreads / 64; ++w) before += w < wave ? s_tot[w] : 0;
-  if (before <= rem && rem < before + mine) {
-    int64_t cum = before;
-    int i = 0;
-    for (i = 0; i < BPT - 1; ++i) {
-      if (cum + c[i] > rem) break;
-      cum += c[i];
-    }
-    s_bin = t * BPT + i;
-    s_cum = cum;
-    s_bcnt = c[i];
-  }
-  __syncthreads();
-  if (s_bin < 0) {            // rank beyond the counts (not reached with consistent counts): last bin
-    if (t == 0) {
-      int64_t cum = 0;
-      for (int b = 0; b < nb - 1; ++b) cum += hh[b];
-      s_bin = nb - 1;
-      s_cum = cum;
-      s_bcnt = hh[nb - 1];
-    }
-    __syncthreads();
-  }
-  const int bin = s_bin;
-  if (pass == 2) {
-    // first non-empty bin above the chosen one, within x_(lo)'s 22-bit bucket
-#pragma unroll
-    for (int i = 0; i < BPT; ++i) {
-      const int b = t * BPT + i;
-      if (b > bin && b < nb && c[i] != 0u) atomicMin(&s_next, b);
-    }
-  }
-  __syncthreads();
-  if (t == 0) {
-    const uint32_t prefix = st[h].prefix | ((uint32_t)bin << digit_shift(pass));
-    st[h].prefix = prefix;
-    st[h].remaining = rem - s_cum;
-    st[h].cnt_lt += (unsigned long long)s_cum;
-    if (pass == 0) st[h].c0 = s_bcnt;
-    if (pass == 2) {
-      if (s_next != 0x7FFFFFFF) st[h].min_above_key = (prefix & ~0x3FFu) | (uint32_t)s_next;
-      else st[h].need_scan = 1;
-    }
-  }
-}
-
-// Smallest ordered key strictly above x_(lo) (needed when x_(lo + 1) differs).
-// from_cand: over the gathered candidates (x_(lo)'s top-digit bin), when they
-// were gathered; otherwise, and when no candidate lies above x_(lo) (then the
-// key sits in a higher top-digit bin), over A.
-__global__ __launch_bounds__(256) void radix_min_above_kernel(const float* __restrict__ A, int64_t N, CvState* st,
-                                                              const uint32_t* __restrict__ cand, uint32_t cap,
-                                                              int from_cand) {
-  __shared__ uint32_t s_min;
-  const int h = blockIdx.y;
-  if (!st[h].need_scan) return;       // found in the last radix histogram
-  const bool use_cand = st[h].c0 <= (unsigned long long)cap;
-  if (from_cand ? !use_cand : (use_cand && st[h].min_above_key != 0xFFFFFFFFu)) return;
-  if (threadIdx.x == 0) s_min = 0xFFFFFFFFu;
-  __syncthreads();
-  const uint32_t x = st[h].prefix;
-  uint32_t mn = 0xFFFFFFFFu;
-  if (from_cand) {
-    const uint32_t* ch = cand + (size_t)h * cap;
-    const int64_t nc = st[h].n_cand;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nc; i += (int64_t)gridDim.x * blockDim.x) {
-      const uint32_t key = ch[i];
-      if (key > x) mn = min(mn, key);
-    }
-  } else {
-    const float* Ah = A + (size_t)h * N;
-    const int64_t n4 = (N & 3) == 0 && ((reinterpret_cast<uintptr_t>(Ah) & 15) == 0) ? N / 4 : 0;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (int64_t)gridDim.x * blockDim.x) {
-      const float4 v = *reinterpret_cast<const float4*>(Ah + 4 * i);
-      const uint32_t k4[4] = {ord_key(v.x), ord_key(v.y), ord_key(v.z), ord_key(v.w)};
-#pragma unroll
-      for (int e = 0; e < 4; ++e)
-        if (k4[e] > x) mn = min(mn, k4[e]);
-    }
-    for (int64_t i = 4 * n4 + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N;
-         i += (int64_t)gridDim.x * blockDim.x) {
-      const uint32_t key = ord_key(Ah[i]);
-      if (key > x) mn = min(mn, key);
-    }
-  }
-  atomicMin(&s_min, mn);
-  __syncthreads();
-  if (threadIdx.x == 0 && s_min != 0xFFFFFFFFu) atomicMin(&st[h].min_above_key, s_min);
-}
-
-// Phi = alpha * (x_(lo) + frac * (x_(lo+1) - x_(lo))) in fp64 (Eq. 2).
-__global__ void cv_threshold_kernel(CvState* st, const uint32_t* __restrict__ hist_last, int64_t N,
-                                    double k_pct, double alpha, int hkv) {
-  const int h = blockIdx.x * blockDim.x + threadIdx.x;
-  if (h >= hkv) return;
-  const double pos = (double)(N - 1) * k_pct;
-  const int64_t lo = (int64_t)floor(pos);
-  const double frac = pos - (double)lo;
-  const uint32_t xk = st[h].prefix;
-  const unsigned long long eq = hist_last[(size_t)h * kRadixBins + (xk & 0x3FFu)];
-  const unsigned long long le = st[h].cnt_lt + eq;        // entries <= x_(lo)
-  const double xlo = (double)key_to_float(xk);
-  double xhi = xlo;
-  if ((int64_t)le < lo + 2 && lo + 1 <= N - 1) xhi = (double)key_to_float(st[h].min_above_key);
-  st[h].phi = alpha * (xlo + frac * (xhi - xlo));
-}
-
-// C_j = #{i : A[i][j] >= Phi} (Eq. 2-3); exact integer sums of C and C^2.
-// A workgroup takes 64 adjacent columns at a time (one per lane, so every
-// row read is 256 contiguous bytes, whatever the row stride) and its four
-// waves split the rows, each with up to kCountRows loads in flight per lane;
-// the four partial counts of a column meet in LDS before C_j is squared.
-// The comparison stays in fp64 against Phi.
-constexpr int kCountRows = 16;
-__global__ __launch_bounds__(256) void cv_count_kernel(const float* __restrict__ A, int lq, int64_t n_keys,
-                                                        CvState* st) {
-  __shared__ unsigned int s_c[4][64];
-  __shared__ unsigned long long s1, s2;
-  const int h = blockIdx.y;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;   // wave = row group
-  if (threadIdx.x == 0) { s1 = 0; s2 = 0; }
-  __syncthreads();
-  const double phi = st[h].phi;
-  const float* Ah = A + (size_t)h * lq * n_keys;
-  const int rpg = (lq + 3) / 4;
-  const int r0 = wave * rpg, r1 = min(lq, r0 + rpg);
-  unsigned long long a1 = 0, a2 = 0;
-  for (int64_t j0 = (int64_t)blockIdx.x * 64; j0 < n_keys; j0 += (int64_t)gridDim.x * 64) {
-    const int64_t j = j0 + lane;
-    unsigned int c = 0;
-    if (j < n_keys) {
-      for (int i0 = r0; i0 < r1; i0 += kCountRows) {
-        float v[kCountRows];
-#pragma unroll
-        for (int u = 0; u < kCountRows; ++u)
-          if (i0 + u < r1) v[u] = Ah[(size_t)(i0 + u) * n_keys + j];
-#pragma unroll
-        for (int u = 0; u < kCountRows; ++u)
-          if (i0 + u < r1) c += (double)v[u] >= phi;
-      }
-    }
-    s_c[wave][lane] = c;
-    __syncthreads();
-    if (wave == 0 && j < n_keys) {
-      const unsigned int cj = s_c[0][lane] + s_c[1][lane] + s_c[2][lane] + s_c[3][lane];
-      a1 += cj;
-      a2 += (unsigned long long)cj * cj;
-    }
-    __syncthreads();
-  }
-  if (wave == 0) {              // only wave 0 holds sums
-    atomicAdd(&s1, a1);
-    atomicAdd(&s2, a2);
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    atomicAdd(&st[h].sum_c, s1);
-    atomicAdd(&st[h].sum_c2, s2);
-  }
-}
-
-// Eq. 4: population standard deviation over the mean, from exact integers.
-__global__ void cv_final_kernel(const CvState* __restrict__ st, int64_t n_keys, float* cv_out, int hkv) {
-  const int h = blockIdx.x * blockDim.x + threadIdx.x;
-  if (h >= hkv) return;
-  const double N = (double)n_keys;
-  const double mu = (double)st[h].sum_c / N;
-  if (mu == 0.0) { cv_out[h] = 0.f; return; }
-  double var = (double)st[h].sum_c2 / N - mu * mu;
-  var = var < 0.0 ? 0.0 : var;
-  cv_out[h] = (float)(sqrt(var) / mu);
-}
-
-// ---------------------------------------------------------------------------
 // host-side launchers
 // ---------------------------------------------------------------------------
 
@@ -1004,14 +645,8 @@ hipError_t launch_compact(int dtype, const void* k, const void* v, int hkv, int6
 }
 
 struct ScoreLayout {
-  size_t rowpart, rowoff, obs, hist, cand, state, total;
+  size_t rowpart, rowoff, obs, cv, total;
 };
-// Candidate keys per head: an eighth of the observation matrix (the top-digit
-// bin of a high quantile holds far fewer; larger bins take the path over A).
-static uint32_t cand_cap(const ScoreGeom& g) {
-  const int64_t N = (int64_t)g.lq * g.n_keys;
-  return (uint32_t)std::max<int64_t>(4096, (N + 7) / 8);
-}
 static ScoreLayout score_layout(const ScoreGeom& g) {
   ScoreLayout L{};
   const int rp = score_rows_pad(g.G * g.lq);
@@ -1019,9 +654,7 @@ static ScoreLayout score_layout(const ScoreGeom& g) {
   L.rowpart = o; o += align256((size_t)g.hkv * g.n_colblk * rp * sizeof(float2));
   L.rowoff = o; o += align256((size_t)g.hkv * rp * sizeof(float));
   L.obs = o; o += align256((size_t)g.hkv * g.lq * g.n_keys * sizeof(float));
-  L.hist = o; o += align256((size_t)3 * g.hkv * kRadixBins * sizeof(uint32_t));
-  L.cand = o; o += align256((size_t)g.hkv * cand_cap(g) * sizeof(uint32_t));
-  L.state = o; o += align256((size_t)g.hkv * sizeof(CvState));
+  L.cv = o; o += align256(cv_workspace_bytes(g.hkv, g.lq, g.n_keys));
   L.total = o;
   return L;
 }
@@ -1054,29 +687,7 @@ hipError_t launch_score(int dtype, const ScoreGeom& g, const void* q_rows, const
   e = launch_score_obs(dtype, g.G, g.causal, rp, grid, stream, a);
   if (e != hipSuccess) return e;
 
-  const int64_t N = (int64_t)g.lq * g.n_keys;
-  uint32_t* hist = reinterpret_cast<uint32_t*>(w + L.hist);
-  CvState* st = reinterpret_cast<CvState*>(w + L.state);
-  hipLaunchKernelGGL(cv_init_kernel, dim3(24), dim3(256), 0, stream, st, hist, N, g.k_pct, g.hkv);
-  const unsigned hb = (unsigned)std::min<int64_t>(512, (N + 1023) / 1024);
-  const unsigned pb = (unsigned)((g.hkv + 63) / 64);
-  uint32_t* cand = reinterpret_cast<uint32_t*>(w + L.cand);
-  const uint32_t cap = cand_cap(g);
-  for (int pass = 0; pass < 3; ++pass) {
-    uint32_t* hp = hist + (size_t)pass * g.hkv * kRadixBins;
-    hipLaunchKernelGGL(radix_hist_kernel, dim3(hb, g.hkv), dim3(256), 0, stream, a.obs, N, pass, st, hp, cand, cap);
-    hipLaunchKernelGGL(radix_pick_kernel, dim3(g.hkv), dim3(kPickThreads), 0, stream, hp, pass, st, g.hkv);
-  }
-  hipLaunchKernelGGL(radix_min_above_kernel, dim3(hb, g.hkv), dim3(256), 0, stream, a.obs, N, st, cand, cap, 1);
-  hipLaunchKernelGGL(radix_min_above_kernel, dim3(hb, g.hkv), dim3(256), 0, stream, a.obs, N, st, cand, cap, 0);
-  hipLaunchKernelGGL(cv_threshold_kernel, dim3(pb), dim3(64), 0, stream, st,
-                     hist + (size_t)2 * g.hkv * kRadixBins, N, g.k_pct, g.alpha, g.hkv);
-  // 64 columns per workgroup and step; few enough workgroups that the two
-  // per-head totals are not a hot spot of global atomics
-  const unsigned cb = (unsigned)std::min<int64_t>(256, (g.n_keys + 63) / 64);
-  hipLaunchKernelGGL(cv_count_kernel, dim3(cb, g.hkv), dim3(256), 0, stream, a.obs, g.lq, g.n_keys, st);
-  hipLaunchKernelGGL(cv_final_kernel, dim3(pb), dim3(64), 0, stream, st, g.n_keys, cv_out, g.hkv);
-  return hipGetLastError();
+  return launch_cv(a.obs, g.hkv, g.lq, g.n_keys, g.k_pct, g.alpha, w + L.cv, cv_out, stream);
 }
 
 }  // namespace catekv
