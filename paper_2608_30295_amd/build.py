@@ -18,7 +18,7 @@ LIB = os.path.join(HERE, "libcatekv.so")
 ARCH = "gfx950"
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 
-HIP_SOURCES = ["decode.hip", "prefill.hip", "retrieve.hip", "score_rowstats.hip", "score_colmass.hip", "score_obs.hip", "cv.hip"]
+HIP_SOURCES = ["decode.hip", "prefill.hip", "retrieve.hip", "score_rowstats.hip", "score_colmass.hip", "score_obs.hip", "score_obsb.hip", "cv.hip"]
 HOST_SOURCES = ["api.cpp"]
 
 # Packed fp32 ops are kept out of the device code: hipcc only emits them when

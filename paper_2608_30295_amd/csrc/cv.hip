@@ -16,48 +16,19 @@
 // Radix route: when the sample's range misses a rank, or the gathered
 // entries overflow their buffer (heavy ties), exact radix passes over A
 // take over for that head.
-#include <hip/hip_runtime.h>
+#include "score.h"
 
 #include <algorithm>
 #include <cmath>
 
-#include "internal.h"
-
 namespace catekv {
 namespace {
 
-constexpr int kBins = 2048;
-constexpr uint32_t kNone = 0xFFFFFFFFu;
-
-// Ordered integer key of a float: key order is float order (-0 < +0).
-__device__ __forceinline__ uint32_t ord_key(float f) {
-  const uint32_t u = __float_as_uint(f);
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-__device__ __forceinline__ float key_to_float(uint32_t key) {
-  return __uint_as_float((key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key);
-}
-
-struct CvState {                   // per KV head, in the workspace
-  int64_t rank;                    // lo = floor((N - 1) k), 0-based
-  uint32_t k_lo, k_hi;             // the bracket: ordered keys [k_lo, k_hi]
-  float t_lo, t_hi;                // Phi lies in [t_lo, t_hi)
-  int shift1;                      // (key - k_lo) >> shift1: first digit over the bracket
-  uint32_t phi_over;               // a workgroup's gathered pairs overflowed its buffer
-  unsigned long long n_cand;       // entries inside the bracket
-  unsigned long long below_br;     // entries below the bracket
-  unsigned long long sum_c, sum_c2;  // sums of C_j and C_j^2 (bracket route)
-  double phi;
-  uint32_t min2;                   // bracket route: smallest key offset above x_(lo)'s first-digit bin
-  uint32_t n_list;                 // bracket route: entries of x_(lo)'s first-digit bin
-  uint32_t arrive_r;               // bracket route: listing workgroups done
-  uint32_t arrive_f;               // radix route: workgroups done in the launch that ends the head
-  uint32_t fb_min;                 // radix route: smallest key above x_(lo)'s 22-bit bucket
-  uint32_t fb_prefix[2];           // radix route: key prefix after the first and second digit
-  int64_t fb_rem[2];               //   rank left inside that prefix
-  unsigned long long fb_lt[2];     //   entries below that prefix
-  unsigned long long fb_sum_c, fb_sum_c2;
-};
+constexpr int kBins = kCvBins;
+constexpr uint32_t kNone = kCvNone;
+__device__ __forceinline__ uint32_t ord_key(float f) { return cv_key(f); }
+__device__ __forceinline__ float key_to_float(uint32_t key) { return cv_key_float(key); }
+__device__ __forceinline__ bool bracket_route(const CvState& S, int64_t N) { return cv_bracket_route(S, N); }
 
 __device__ __forceinline__ uint32_t mbcnt(uint64_t m) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
@@ -172,7 +143,7 @@ __device__ __forceinline__ double phi_of(double xlo, double xhi, int64_t N, doub
 }
 
 // ---------------------------------------------------------------------------
-// 1. Sample: state, and the bracket from 8192 entries of A in runs of 8
+// 1. Sample: state, and the bracket from the sampled entries of A
 // ---------------------------------------------------------------------------
 
 // The sample's first two radix digits give the 22-bit key prefixes holding
@@ -181,10 +152,9 @@ __device__ __forceinline__ double phi_of(double xlo, double xhi, int64_t N, doub
 // range follows from the bracket's floats, widened by 2^-40 relative (far
 // beyond the rounding of the fp64 interpolation) and rounded outward to floats.
 constexpr int kSampleThreads = 1024;
-constexpr int kSamplePer = 8;
-constexpr int64_t kSampleSize = kSampleThreads * kSamplePer;
+constexpr int kSamplePer = kCvSamples / kSampleThreads;
 
-__global__ __launch_bounds__(kSampleThreads) void cv_sample_kernel(const float* __restrict__ A, int64_t N,
+__global__ __launch_bounds__(kSampleThreads) void cv_sample_kernel(const float* __restrict__ samples, int64_t N,
                                                                    double k_pct, double alpha, CvState* st,
                                                                    uint32_t* __restrict__ hist, int hkv) {
   __shared__ uint32_t s_h[kBins];
@@ -200,14 +170,13 @@ __global__ __launch_bounds__(kSampleThreads) void cv_sample_kernel(const float* 
   for (int i = t; i < 2 * kBins; i += kSampleThreads) s_h2[i / kBins][i % kBins] = 0;
   const int64_t rank = (int64_t)floor((double)(N - 1) * k_pct);
   __syncthreads();
-  const int64_t ns = N < kSampleSize ? N : kSampleSize;
-  const int64_t stride = N < kSampleSize ? kSamplePer : (N / kSampleThreads) & ~(int64_t)(kSamplePer - 1);
-  const float* Ah = A + (size_t)h * N;
+  const int64_t ns = cv_sample_count(N);
+  const float* sh = samples + (size_t)h * kCvSamples;
   float v[kSamplePer];
 #pragma unroll
-  for (int u = 0; u < kSamplePer; ++u) v[u] = Ah[std::min<int64_t>((int64_t)t * stride + u, N - 1)];
+  for (int u = 0; u < kSamplePer; ++u) v[u] = sh[std::min<int64_t>((int64_t)t * kSamplePer + u, ns - 1)];
 #pragma unroll
-  for (int u = 0; u < kSamplePer; ++u) hist_add(s_h, (int64_t)t * stride + u < N, ord_key(v[u]) >> 21);
+  for (int u = 0; u < kSamplePer; ++u) hist_add(s_h, (int64_t)t * kSamplePer + u < ns, ord_key(v[u]) >> 21);
   const double rs = (double)rank * (double)ns / (double)N;
   const double pq = (double)rank / (double)N;
   const double m = 8.0 * sqrt((double)ns * pq * (1.0 - pq)) + 32.0;
@@ -217,7 +186,7 @@ __global__ __launch_bounds__(kSampleThreads) void cv_sample_kernel(const float* 
   const int64_t rl = s_pos[0], rh = s_pos[1];
 #pragma unroll
   for (int u = 0; u < kSamplePer; ++u) {
-    const bool ok = (int64_t)t * stride + u < N;
+    const bool ok = (int64_t)t * kSamplePer + u < ns;
     const uint32_t key = ord_key(v[u]);
     if (ok && (key >> 21) == bl) atomicAdd(&s_h2[0][(key >> 10) & 0x7FF], 1u);
     if (ok && (key >> 21) == bh) atomicAdd(&s_h2[1][(key >> 10) & 0x7FF], 1u);
@@ -248,10 +217,13 @@ __global__ __launch_bounds__(kSampleThreads) void cv_sample_kernel(const float* 
     s.t_hi = th;
     s.shift1 = bits > 11 ? bits - 11 : 0;
     s.phi_over = 0;
+    s.c1 = 0;
+    s.c2 = 0;
     s.n_cand = 0;
-    s.below_br = 0;
-    s.sum_c = 0;
-    s.sum_c2 = 0;
+    s.ge_lo = 0;
+    s.ge_thi = 0;
+    s.e1 = 0;
+    s.e2 = 0;
     s.phi = 0.0;
     s.min2 = kNone;
     s.n_list = 0;
@@ -267,176 +239,21 @@ __global__ __launch_bounds__(kSampleThreads) void cv_sample_kernel(const float* 
 }
 
 // ---------------------------------------------------------------------------
-// 2. The bracketing pass over A, column by column
+// 2. The bracketing pass is the observation-matrix pass (score.h,
+//    kObsBracket): per column the entries at or above t_hi, the entries
+//    below the bracket, the bracket entries' first-digit histogram, and the
+//    entries of the union of bracket and Phi's range as (value, column) in
+//    one buffer per wave of each column block.
 // ---------------------------------------------------------------------------
 
-// Workgroup x owns column blocks x, x + cb, x + 2 cb, ... (64 columns each);
-// its waves take turns over them, and a wave walks all lq rows of its block
-// itself (one column per lane, each row read 256 contiguous bytes, 16 rows
-// loaded together per step), so a column's count stays in its lane.  Per
-// entry: below the bracket (counted), at or above t_hi (counted for the
-// column), inside the union of the bracket and Phi's range (staged in LDS as
-// (value, the column's index among the workgroup's columns)).  A wave writes
-// its stage out in one run to the workgroup's own share of the pair buffer
-// before a step that would overflow it; the entries written out that lie in
-// the bracket are counted and enter the workgroup's histogram of the first
-// digit then, 64 at a time.  Entries are probabilities (A >= +0), so the
-// floats compare like their keys.
-constexpr int kStepRows = 16;     // rows per lane loaded together
-constexpr int kCountRows = 16;    // the same for the radix route's column walk
-constexpr int kStage = 512;       // pairs a wave stages
+constexpr int kCountRows = 16;    // rows per lane loaded together by the radix route's column walk
 
-// Column walk: ~2048 workgroups over all heads, and enough that none owns
-// more than 8192 columns.
+// The radix route's column walk: ~2048 workgroups over all heads.
 int64_t col_blocks(int64_t n_keys, int hkv) {
   const int64_t blocks = (n_keys + 63) / 64;
   const int64_t want = std::max<int64_t>(256, 2048 / std::max(1, hkv));
-  return std::max<int64_t>(1, std::max(std::min(blocks, want), (blocks + 127) / 128));
+  return std::max<int64_t>(1, std::min(blocks, want));
 }
-
-__device__ __forceinline__ float bracket_top(uint32_t k_hi) {   // first float above the bracket's keys
-  const float f = k_hi == kNone ? INFINITY : key_to_float(k_hi + 1);
-  return f != f ? INFINITY : f;
-}
-
-__global__ __launch_bounds__(256) void cv_bracket_kernel(const float* __restrict__ A, int lq, int64_t n_keys,
-                                                         CvState* st, uint32_t* __restrict__ hist0,
-                                                         uint2* __restrict__ pairs, uint32_t* __restrict__ pfill,
-                                                         uint32_t capw, uint32_t* __restrict__ colcnt) {
-  __shared__ uint32_t s_h[kBins];
-  __shared__ uint2 s_pair[4][kStage];
-  __shared__ uint32_t s_fill;
-  __shared__ unsigned long long s_red[4];
-  const int h = blockIdx.y;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  CvState& S = st[h];
-  for (int i = threadIdx.x; i < kBins; i += 256) s_h[i] = 0;
-  if (threadIdx.x == 0) s_fill = 0;
-  const uint32_t k_lo = S.k_lo, span = S.k_hi - S.k_lo;
-  const float f_lo = key_to_float(k_lo), f_hi = bracket_top(S.k_hi);
-  const float t_lo = S.t_lo, t_hi = S.t_hi;
-  const float u_lo = fminf(f_lo, t_lo), u_hi = fmaxf(f_hi, t_hi);
-  const int sh1 = S.shift1;
-  __syncthreads();
-  const size_t wg = (size_t)h * gridDim.x + blockIdx.x;
-  uint2* ph = pairs + wg * capw;
-  uint32_t np = 0, nin = 0;        // wave-uniform: staged pairs, bracket entries written out
-  uint32_t below = 0;
-  unsigned long long a1 = 0, a2 = 0;
-  // reserve n slots of the workgroup's share (one LDS atomic per wave)
-  auto reserve = [&](uint32_t n) {
-    uint32_t base = 0;
-    if (lane == 0) base = atomicAdd(&s_fill, n);
-    return __shfl(base, 0);
-  };
-  auto flush = [&]() {
-    for (uint32_t i = lane; i < ((np + 63) & ~63u); i += 64) {
-      const uint32_t o = i < np ? (s_pair[wave][i].x | 0x80000000u) - k_lo : kNone;
-      const bool in = o <= span;
-      nin += (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(in));
-      hist_add(s_h, in, o >> sh1);
-    }
-    const uint32_t base = reserve(np);
-    for (uint32_t i = lane; i < np; i += 64)
-      if (base + i < capw) ph[base + i] = s_pair[wave][i];
-    np = 0;
-  };
-  const float* Ah = A + (size_t)h * lq * n_keys;
-  const int64_t blocks = (n_keys + 63) / 64;
-  const int kb = (int)((blocks - blockIdx.x + gridDim.x - 1) / gridDim.x);   // blocks of this workgroup
-  const int nch = (lq + kStepRows - 1) / kStepRows;                          // row steps per block
-  const int nq = (kb > wave ? (kb - wave + 3) / 4 : 0) * nch;                // this wave's steps
-  unsigned int c = 0;
-  for (int q = 0; q < nq; ++q) {
-    // step q: block k = wave + 4 (q / nch), rows [kStepRows (q % nch), +kStepRows)
-    const int k = wave + 4 * (q / nch), i0 = (q % nch) * kStepRows;
-    const int64_t j = ((int64_t)blockIdx.x + (int64_t)k * gridDim.x) * 64 + lane;
-    const bool jv = j < n_keys;
-    // every load issued (clamped to the last column and row), then used
-    const float* p = Ah + std::min<int64_t>(j, n_keys - 1);
-    float v[kStepRows];
-#pragma unroll
-    for (int u = 0; u < kStepRows; ++u) v[u] = p[(size_t)std::min(i0 + u, lq - 1) * n_keys];
-    // a lane past the last column meets thresholds no entry reaches
-    const float lo_u = jv ? u_lo : INFINITY, lo_b = jv ? f_lo : 0.f, hi_c = jv ? t_hi : INFINITY;
-    uint64_t bu[kStepRows];
-    uint32_t tu = 0;
-#pragma unroll
-    for (int u = 0; u < kStepRows; ++u) {
-      const bool row = i0 + u < lq;          // uniform
-      const float x = v[u];
-      c += row && x >= hi_c;
-      below += row && x < lo_b;
-      bu[u] = __builtin_amdgcn_ballot_w64(row && x >= lo_u && x < u_hi);
-      tu += (uint32_t)__builtin_popcountll(bu[u]);
-    }
-    if (tu) {
-      const uint32_t local = (uint32_t)k * 64 + lane;
-      if (np + tu > (uint32_t)kStage) flush();
-      if (tu <= (uint32_t)kStage) {
-#pragma unroll
-        for (int u = 0; u < kStepRows; ++u) {
-          if ((bu[u] >> lane) & 1) s_pair[wave][np + mbcnt(bu[u])] = make_uint2(__float_as_uint(v[u]), local);
-          np += (uint32_t)__builtin_popcountll(bu[u]);
-        }
-      } else {             // more than a stage in one step (heavy ties): straight out, then counted
-        uint32_t base = reserve(tu);
-#pragma unroll
-        for (int u = 0; u < kStepRows; ++u) {
-          const bool in_u = (bu[u] >> lane) & 1;
-          const uint32_t at = base + mbcnt(bu[u]);
-          if (in_u && at < capw) ph[at] = make_uint2(__float_as_uint(v[u]), local);
-          const uint32_t o = in_u ? (__float_as_uint(v[u]) | 0x80000000u) - k_lo : kNone;
-          nin += (uint32_t)__builtin_popcountll(__builtin_amdgcn_ballot_w64(o <= span));
-          hist_add(s_h, o <= span, o >> sh1);
-          base += (uint32_t)__builtin_popcountll(bu[u]);
-        }
-      }
-    }
-    if (q % nch == nch - 1) {      // the block's last rows: the column count is complete
-      if (jv) {
-        colcnt[(size_t)h * n_keys + j] = c;
-        a1 += c;
-        a2 += (unsigned long long)c * c;
-      }
-      c = 0;
-    }
-  }
-  if (np) flush();
-  const unsigned long long tb = block_sum256(below, s_red);
-  const unsigned long long t1 = block_sum256(a1, s_red);
-  const unsigned long long t2 = block_sum256(a2, s_red);
-  const unsigned long long tn = block_sum256(lane == 0 ? nin : 0u, s_red);
-  if (threadIdx.x == 0) {
-    if (tb) atomicAdd(&S.below_br, tb);
-    if (tn) atomicAdd(&S.n_cand, tn);
-    if (t1) {
-      atomicAdd(&S.sum_c, t1);
-      atomicAdd(&S.sum_c2, t2);
-    }
-    pfill[wg] = min(s_fill, capw);
-    if (s_fill > capw) atomicOr(&S.phi_over, 1u);
-  }
-  for (int i = threadIdx.x; i < kBins; i += 256)
-    if (s_h[i]) atomicAdd(&hist0[(size_t)h * kBins + i], s_h[i]);
-}
-
-// The head takes the bracket route when the bracket holds ranks lo and lo + 1
-// (lo only, when lo = N - 1) and every gathered pair fit its buffer.
-// Decided alike by every launch after the bracketing pass.
-__device__ __forceinline__ bool bracket_route(const CvState& S, int64_t N) {
-  const int64_t lo = S.rank;
-  const unsigned long long top = (unsigned long long)(lo + 1 <= N - 1 ? lo + 1 : lo);
-  return S.phi_over == 0 && S.below_br <= (unsigned long long)lo && top < S.below_br + S.n_cand;
-}
-
-// ---------------------------------------------------------------------------
-// 3. Bracket route: workgroup x takes the pairs of column-walk workgroups
-//    [kRegions x, kRegions (x + 1)) and lists the bracket entries in
-//    x_(lo)'s first-digit bin; it also keeps the smallest bracket entry above
-//    that bin.  The last workgroup of a head to finish takes x_(lo), x_(lo+1)
-//    and Phi.  Radix route: histogram of the top key digit over A.
-// ---------------------------------------------------------------------------
 
 __device__ __forceinline__ void hist_over_A(const float* __restrict__ Ah, int64_t N, uint32_t* s_h, uint32_t mask,
                                             uint32_t want, int shift, uint32_t dmask, uint32_t above, uint32_t* mn) {
@@ -462,8 +279,67 @@ __device__ __forceinline__ void flush_hist(const uint32_t* s_h, uint32_t* __rest
     if (s_h[i]) atomicAdd(&g[i], s_h[i]);
 }
 
-constexpr int kListCap = 65536;    // entries of x_(lo)'s first-digit bin listed, at most
-constexpr int kRegions = 2;        // pair buffers per listing workgroup
+// Pairs of column block b (its waves' buffers): the bracket entries are
+// counted and histogrammed by their first digit, and the pairs at or above
+// the bracket's bottom and at or above t_hi counted (the entries below the
+// bracket follow, cv_below).
+__global__ __launch_bounds__(256) void cv_pairs_kernel(CvState* st, uint32_t* __restrict__ hist0,
+                                                       const uint2* __restrict__ pairs,
+                                                       const uint32_t* __restrict__ pfill, uint32_t capw, int nsub,
+                                                       int n_colblk) {
+  __shared__ uint32_t s_h[kBins];
+  __shared__ unsigned long long s_red[4];
+  const int h = blockIdx.y, b = blockIdx.x;
+  const int t = threadIdx.x;
+  CvState& S = st[h];
+  for (int i = t; i < kBins; i += 256) s_h[i] = 0;
+  const uint32_t k_lo = S.k_lo, span = S.k_hi - S.k_lo;
+  const int sh1 = S.shift1;
+  const float f_lo = key_to_float(k_lo), t_hi = S.t_hi;
+  __syncthreads();
+  uint32_t n_in = 0, n_lo = 0, n_thi = 0;
+  for (int w = 0; w < nsub; ++w) {
+    const size_t wr = ((size_t)h * n_colblk + b) * nsub + w;
+    const uint2* ph = pairs + wr * capw;
+    const uint32_t fill = pfill[wr];
+    for (uint32_t i0 = 0; i0 < fill; i0 += 4 * 256) {   // the same trip count on every lane
+      uint32_t x[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) x[u] = ph[min(i0 + u * 256 + t, fill - 1)].x;   // every load issued, then used
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const bool ok = i0 + u * 256 + t < fill;
+        const float v = __uint_as_float(x[u]);
+        const uint32_t o = (x[u] | 0x80000000u) - k_lo;
+        const bool in = ok && o <= span;
+        n_in += in;
+        n_lo += ok && v >= f_lo;
+        n_thi += ok && v >= t_hi;
+        hist_add(s_h, in, o >> sh1);
+      }
+    }
+  }
+  const unsigned long long a_in = block_sum256(n_in, s_red);
+  const unsigned long long a_lo = block_sum256(n_lo, s_red);
+  const unsigned long long a_thi = block_sum256(n_thi, s_red);
+  if (t == 0) {
+    if (a_in) atomicAdd(&S.n_cand, a_in);
+    if (a_lo) atomicAdd(&S.ge_lo, a_lo);
+    if (a_thi) atomicAdd(&S.ge_thi, a_thi);
+  }
+  flush_hist(s_h, hist0 + (size_t)h * kBins);
+}
+
+// ---------------------------------------------------------------------------
+// 3. Bracket route: workgroup x takes the pairs of column-walk workgroups
+//    [kRegions x, kRegions (x + 1)) and lists the bracket entries in
+//    x_(lo)'s first-digit bin; it also keeps the smallest bracket entry above
+//    that bin.  The last workgroup of a head to finish takes x_(lo), x_(lo+1)
+//    and Phi.  Radix route: histogram of the top key digit over A.
+// ---------------------------------------------------------------------------
+
+constexpr int kListCap = kCvListCap;
+constexpr int kRegions = 8;        // pair buffers per listing workgroup
 constexpr int kShortList = 1024;   // lists resolved by counting ranks
 constexpr int kListStage = 2048;   // entries staged before a reservation (a round adds <= 1024)
 
@@ -628,7 +504,7 @@ __global__ __launch_bounds__(256) void cv_list_kernel(const float* __restrict__ 
   const int nwg = sh1 == 0 ? 1 : (cb + kRegions - 1) / kRegions;
   if ((int)blockIdx.x >= nwg) return;
   const uint32_t k_lo = S.k_lo, span = S.k_hi - S.k_lo;
-  const unsigned long long below = S.below_br;
+  const unsigned long long below = cv_below(S, N);
   const int64_t rem0 = S.rank - (int64_t)below;
   locate_ranks<256>(hist0 + (size_t)h * kBins, kBins, rem0, rem0, s_tot, s_bin, s_pos);
   const uint32_t b1 = s_bin[0], next1 = s_bin[2];
@@ -708,12 +584,15 @@ __global__ __launch_bounds__(256) void cv_list_kernel(const float* __restrict__ 
 //    sums of C_j and C_j^2.  Radix route: the second key digit over A.
 // ---------------------------------------------------------------------------
 
+constexpr int kColWin = 8192;      // columns counted in LDS at a time
+
 __global__ __launch_bounds__(256) void cv_columns_kernel(const float* __restrict__ A, int64_t N, CvState* st,
                                                          const uint32_t* __restrict__ hist1,
                                                          uint32_t* __restrict__ hist2, const uint2* __restrict__ pairs,
-                                                         const uint32_t* __restrict__ pfill, uint32_t capw, int cb,
+                                                         const uint32_t* __restrict__ pfill, uint32_t capw, int nsub,
+                                                         int n_colblk, int64_t cb_tokens,
                                                          const uint32_t* __restrict__ colcnt, int64_t n_keys) {
-  extern __shared__ uint32_t s_e[];   // max(columns owned, kBins) entries
+  __shared__ uint32_t s_e[kColWin];
   __shared__ int64_t s_tot[4];
   __shared__ uint32_t s_bin[3];
   __shared__ int64_t s_pos[2];
@@ -739,42 +618,51 @@ __global__ __launch_bounds__(256) void cv_columns_kernel(const float* __restrict
     flush_hist(s_h, hist2 + (size_t)h * kBins);
     return;
   }
+  // column block b's gathered values in [Phi, t_hi), counted per column in
+  // LDS, kColWin columns at a time
   const double phi = S.phi;
   const float t_hi = S.t_hi;
-  const int64_t blocks = (n_keys + 63) / 64;
-  const int nloc = (int)((blocks - blockIdx.x + cb - 1) / cb) * 64;   // this workgroup's columns
-  for (int i = t; i < nloc; i += 256) s_e[i] = 0;
-  __syncthreads();
-  const size_t wg = (size_t)h * cb + blockIdx.x;
-  const uint2* ph = pairs + wg * capw;
-  const uint32_t fill = pfill[wg];
-  for (uint32_t i0 = 0; i0 < fill; i0 += 4 * 256) {
-    uint2 e[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) e[u] = ph[min(i0 + u * 256 + t, fill - 1)];   // every load issued, then used
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const float x = __uint_as_float(e[u].x);
-      if (i0 + u * 256 + t < fill && x < t_hi && (double)x >= phi)   // entries >= t_hi are in C already
-        atomicAdd(&s_e[e[u].y], 1u);
-    }
-  }
-  __syncthreads();
+  const int b = blockIdx.x;
+  const int64_t c0 = (int64_t)b * cb_tokens, c1 = std::min(c0 + cb_tokens, n_keys);
   const uint32_t* cc = colcnt + (size_t)h * n_keys;
   unsigned long long a1 = 0, a2 = 0;
-  for (int l = t; l < nloc; l += 256) {
-    const unsigned long long e = s_e[l];
-    if (e) {
-      const unsigned long long c = cc[((int64_t)blockIdx.x + (int64_t)(l >> 6) * cb) * 64 + (l & 63)];
-      a1 += e;
-      a2 += 2 * c * e + e * e;         // (c + e)^2 - c^2
+  for (int64_t w0 = c0; w0 < c1; w0 += kColWin) {
+    const int nw = (int)std::min<int64_t>(kColWin, c1 - w0);
+    __syncthreads();
+    for (int i = t; i < nw; i += 256) s_e[i] = 0;
+    __syncthreads();
+    for (int w = 0; w < nsub; ++w) {
+      const size_t wr = ((size_t)h * n_colblk + b) * nsub + w;
+      const uint2* ph = pairs + wr * capw;
+      const uint32_t fill = pfill[wr];
+      for (uint32_t i0 = 0; i0 < fill; i0 += 4 * 256) {
+        uint2 e[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) e[u] = ph[min(i0 + u * 256 + t, fill - 1)];   // every load issued, then used
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float x = __uint_as_float(e[u].x);
+          const int64_t rel = (int64_t)e[u].y - w0;
+          if (i0 + u * 256 + t < fill && rel >= 0 && rel < nw && x < t_hi && (double)x >= phi)
+            atomicAdd(&s_e[rel], 1u);   // entries >= t_hi are in C already
+        }
+      }
+    }
+    __syncthreads();
+    for (int l = t; l < nw; l += 256) {
+      const unsigned long long e = s_e[l];
+      if (e) {
+        const unsigned long long c = cc[w0 + l];
+        a1 += e;
+        a2 += 2 * c * e + e * e;       // (c + e)^2 - c^2
+      }
     }
   }
   const unsigned long long t1 = block_sum256(a1, s_red);
   const unsigned long long t2 = block_sum256(a2, s_red);
   if (t == 0 && t1) {
-    atomicAdd(&S.sum_c, t1);
-    atomicAdd(&S.sum_c2, t2);
+    atomicAdd(&S.e1, t1);
+    atomicAdd(&S.e2, t2);
   }
 }
 
@@ -796,7 +684,7 @@ __global__ __launch_bounds__(256) void cv_digit2_kernel(const float* __restrict_
   const int h = blockIdx.y;
   CvState& S = st[h];
   if (bracket_route(S, N)) {  // the bracket route's score, from the previous launch's sums
-    if (blockIdx.x == 0 && threadIdx.x == 0) cv_out[h] = cv_value(S.sum_c, S.sum_c2, n_keys);
+    if (blockIdx.x == 0 && threadIdx.x == 0) cv_out[h] = cv_value(S.c1 + S.e1, S.c2 + S.e2, n_keys);
     return;
   }
   const int64_t rem0 = S.fb_rem[0];
@@ -882,28 +770,29 @@ __global__ __launch_bounds__(256) void cv_count_kernel(const float* __restrict__
   }
 }
 
-// Gathered pairs: a sixteenth of A per head, split evenly over the
-// workgroups of the column walk (the union of bracket and Phi's range holds
-// about 1-2% of A at the sample's margins; a workgroup's overflow sends the
-// head the radix route).
-uint32_t pair_cap(int64_t N, int64_t cb) {
-  const int64_t c = std::max<int64_t>(256, ((N + 15) / 16 + cb - 1) / cb);
+// Gathered pairs: a sixteenth of A per head, split evenly over the waves of
+// the column blocks (the union of bracket and Phi's range holds about 1-2%
+// of A at the sample's margins; a wave's overflow sends the head the radix
+// route).
+uint32_t pair_cap(int64_t N, int64_t nbuf) {
+  const int64_t c = std::max<int64_t>(64, ((N + 15) / 16 + nbuf - 1) / nbuf);
   return (uint32_t)((c + 3) & ~(int64_t)3);
 }
 
 struct CvLayout {
-  size_t hist, list, pairs, pfill, colcnt, state, total;
+  size_t hist, list, samples, pairs, pfill, colcnt, state, total;
 };
 size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
-CvLayout cv_layout(int hkv, int lq, int64_t n_keys) {
+CvLayout cv_layout(int hkv, int lq, int64_t n_keys, int n_colblk) {
   const int64_t N = (int64_t)lq * n_keys;
-  const int64_t cb = col_blocks(n_keys, hkv);
+  const int64_t nbuf = (int64_t)n_colblk * kCvMaxSub;
   CvLayout L{};
   size_t o = 0;
   L.hist = o; o += al256((size_t)4 * hkv * kBins * sizeof(uint32_t));
   L.list = o; o += al256((size_t)hkv * kListCap * sizeof(uint32_t));
-  L.pairs = o; o += al256((size_t)hkv * cb * pair_cap(N, cb) * sizeof(uint2));
-  L.pfill = o; o += al256((size_t)hkv * cb * sizeof(uint32_t));
+  L.samples = o; o += al256((size_t)hkv * kCvSamples * sizeof(float));
+  L.pairs = o; o += al256((size_t)hkv * nbuf * pair_cap(N, nbuf) * sizeof(uint2));
+  L.pfill = o; o += al256((size_t)hkv * nbuf * sizeof(uint32_t));
   L.colcnt = o; o += al256((size_t)hkv * n_keys * sizeof(uint32_t));
   L.state = o; o += al256((size_t)hkv * sizeof(CvState));
   L.total = o;
@@ -912,37 +801,59 @@ CvLayout cv_layout(int hkv, int lq, int64_t n_keys) {
 
 }  // namespace
 
-size_t cv_workspace_bytes(int hkv, int lq, int64_t n_keys) { return cv_layout(hkv, lq, n_keys).total; }
+size_t cv_workspace_bytes(int hkv, int lq, int64_t n_keys, int n_colblk) {
+  return cv_layout(hkv, lq, n_keys, n_colblk).total;
+}
 
-hipError_t launch_cv(const float* A, int hkv, int lq, int64_t n_keys, double k_pct, double alpha, void* ws,
-                     float* cv_out, hipStream_t stream) {
-  const CvLayout L = cv_layout(hkv, lq, n_keys);
+CvLink cv_link(void* ws, int hkv, int lq, int64_t n_keys, int n_colblk, int nsub) {
+  const CvLayout L = cv_layout(hkv, lq, n_keys, n_colblk);
   char* w = reinterpret_cast<char*>(ws);
-  const int64_t N = (int64_t)lq * n_keys;
-  const int64_t cb = col_blocks(n_keys, hkv);
-  const uint32_t capw = pair_cap(N, cb);
-  uint32_t* hist = reinterpret_cast<uint32_t*>(w + L.hist);
+  CvLink c{};
+  c.st = reinterpret_cast<CvState*>(w + L.state);
+  c.samples = reinterpret_cast<float*>(w + L.samples);
+  c.hist = reinterpret_cast<uint32_t*>(w + L.hist);
+  c.hist0 = c.hist;
+  c.list = reinterpret_cast<uint32_t*>(w + L.list);
+  c.pairs = reinterpret_cast<uint2*>(w + L.pairs);
+  c.pfill = reinterpret_cast<uint32_t*>(w + L.pfill);
+  c.capw = pair_cap((int64_t)lq * n_keys, (int64_t)n_colblk * kCvMaxSub);
+  c.nsub = nsub;
+  c.colcnt = reinterpret_cast<uint32_t*>(w + L.colcnt);
+  return c;
+}
+
+hipError_t launch_cv_sample(const ScoreArgs& a, double k_pct, double alpha, hipStream_t stream) {
+  const int64_t N = (int64_t)a.lq * a.n_keys;
+  hipLaunchKernelGGL(cv_sample_kernel, dim3(a.hkv), dim3(kSampleThreads), 0, stream, a.cv.samples, N, k_pct, alpha,
+                     a.cv.st, a.cv.hist, a.hkv);
+  return hipGetLastError();
+}
+
+hipError_t launch_cv_pairs(const ScoreArgs& a, hipStream_t stream) {
+  hipLaunchKernelGGL(cv_pairs_kernel, dim3((unsigned)a.n_colblk, a.hkv), dim3(256), 0, stream, a.cv.st, a.cv.hist,
+                     a.cv.pairs, a.cv.pfill, a.cv.capw, a.cv.nsub, a.n_colblk);
+  return hipGetLastError();
+}
+
+hipError_t launch_cv_finish(const ScoreArgs& a, double k_pct, double alpha, float* cv_out, hipStream_t stream) {
+  const int hkv = a.hkv, lq = a.lq;
+  const int64_t n_keys = a.n_keys, N = (int64_t)lq * n_keys;
+  const CvLink& c = a.cv;
   const size_t hs = (size_t)hkv * kBins;
-  uint32_t* list = reinterpret_cast<uint32_t*>(w + L.list);
-  uint2* pairs = reinterpret_cast<uint2*>(w + L.pairs);
-  uint32_t* pfill = reinterpret_cast<uint32_t*>(w + L.pfill);
-  uint32_t* colcnt = reinterpret_cast<uint32_t*>(w + L.colcnt);
-  CvState* st = reinterpret_cast<CvState*>(w + L.state);
+  uint32_t* hist = c.hist;
+  const float* A = a.obs;
+  const int nbuf = a.n_colblk * c.nsub;
   // radix-route passes over A in entry order: enough workgroups per head to fill the device
   const unsigned hb = (unsigned)std::max<int64_t>(1, std::min<int64_t>(512, (N + 1023) / 1024));
-  const int64_t blocks = (n_keys + 63) / 64;
-  const size_t col_lds = (size_t)std::max<int64_t>(kBins, (blocks + cb - 1) / cb * 64) * sizeof(uint32_t);
-  const unsigned lw = (unsigned)std::max<int64_t>(hb, (cb + kRegions - 1) / kRegions);
-  const dim3 walk((unsigned)cb, hkv), flat(hb, hkv);
-  hipLaunchKernelGGL(cv_sample_kernel, dim3(hkv), dim3(kSampleThreads), 0, stream, A, N, k_pct, alpha, st, hist, hkv);
-  hipLaunchKernelGGL(cv_bracket_kernel, walk, dim3(256), 0, stream, A, lq, n_keys, st, hist, pairs, pfill, capw, colcnt);
-  hipLaunchKernelGGL(cv_list_kernel, dim3(lw, hkv), dim3(256), 0, stream, A, N, st, hist, hist + hs, pairs, pfill, capw,
-                     (int)cb, list, k_pct, alpha);
-  hipLaunchKernelGGL(cv_columns_kernel, walk, dim3(256), col_lds, stream, A, N, st, hist + hs, hist + 2 * hs, pairs,
-                     pfill, capw, (int)cb, colcnt, n_keys);
-  hipLaunchKernelGGL(cv_digit2_kernel, flat, dim3(256), 0, stream, A, N, st, hist + 2 * hs, hist + 3 * hs, n_keys,
+  const unsigned lw = (unsigned)std::max<int64_t>(hb, (nbuf + kRegions - 1) / kRegions);
+  const dim3 walk((unsigned)col_blocks(n_keys, hkv), hkv), flat(hb, hkv);
+  hipLaunchKernelGGL(cv_list_kernel, dim3(lw, hkv), dim3(256), 0, stream, A, N, c.st, hist, hist + hs, c.pairs,
+                     c.pfill, c.capw, nbuf, c.list, k_pct, alpha);
+  hipLaunchKernelGGL(cv_columns_kernel, dim3((unsigned)a.n_colblk, hkv), dim3(256), 0, stream, A, N, c.st, hist + hs,
+                     hist + 2 * hs, c.pairs, c.pfill, c.capw, c.nsub, a.n_colblk, a.cb_tokens, c.colcnt, n_keys);
+  hipLaunchKernelGGL(cv_digit2_kernel, flat, dim3(256), 0, stream, A, N, c.st, hist + 2 * hs, hist + 3 * hs, n_keys,
                      cv_out);
-  hipLaunchKernelGGL(cv_count_kernel, walk, dim3(256), 0, stream, A, lq, n_keys, st, hist + 3 * hs, k_pct, alpha,
+  hipLaunchKernelGGL(cv_count_kernel, walk, dim3(256), 0, stream, A, lq, n_keys, c.st, hist + 3 * hs, k_pct, alpha,
                      cv_out);
   return hipGetLastError();
 }

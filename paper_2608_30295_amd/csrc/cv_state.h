@@ -1,0 +1,100 @@
+// Per-head state of the CV score (Section 3.2, Eq. 2-4) shared by the
+// kernels of csrc/cv.hip and the observation-matrix passes of score.h, and
+// the workspace regions they exchange.  Device code only.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace catekv {
+
+constexpr int kCvBins = 2048;                 // radix and first-digit histograms
+constexpr uint32_t kCvNone = 0xFFFFFFFFu;
+constexpr int kCvListCap = 65536;             // entries of x_(lo)'s first-digit bin listed, at most
+constexpr int kCvMaxSub = 16;                 // waves per score workgroup, at most
+
+// The sample of A that brackets the quantile: 1024 runs of 8 consecutive
+// entries spread evenly over the N entries (all of them when N <= 8192).
+// Sample s = 8 t + u is entry t * stride + u in row-major order.
+constexpr int kCvSampleRuns = 1024, kCvSampleRun = 8, kCvSamples = kCvSampleRuns * kCvSampleRun;
+__host__ __device__ inline int64_t cv_sample_count(int64_t N) { return N < kCvSamples ? N : kCvSamples; }
+__host__ __device__ inline int64_t cv_sample_stride(int64_t N) {
+  return N < kCvSamples ? kCvSampleRun : (N / kCvSampleRuns) & ~(int64_t)(kCvSampleRun - 1);
+}
+
+// Ordered integer key of a float: key order is float order (-0 < +0).
+__device__ __forceinline__ uint32_t cv_key(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float cv_key_float(uint32_t key) {
+  return __uint_as_float((key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key);
+}
+
+struct CvState {                   // per KV head, in the workspace
+  int64_t rank;                    // lo = floor((N - 1) k), 0-based
+  uint32_t k_lo, k_hi;             // the bracket: ordered keys [k_lo, k_hi]
+  float t_lo, t_hi;                // Phi lies in [t_lo, t_hi)
+  int shift1;                      // (key - k_lo) >> shift1: first digit over the bracket
+  uint32_t phi_over;               // a wave's gathered pairs overflowed its buffer
+  unsigned long long c1, c2;       // sums of c_j and c_j^2, c_j = #{i : A[i][j] >= t_hi}
+  unsigned long long n_cand;       // entries inside the bracket (from the pairs)
+  unsigned long long ge_lo;        // pairs at or above the bracket's bottom
+  unsigned long long ge_thi;       // pairs at or above t_hi
+  unsigned long long e1, e2;       // bracket route: changes of sum C and sum C^2 by the pairs in [Phi, t_hi)
+  double phi;
+  uint32_t min2;                   // bracket route: smallest key offset above x_(lo)'s first-digit bin
+  uint32_t n_list;                 // bracket route: entries of x_(lo)'s first-digit bin
+  uint32_t arrive_r;               // bracket route: listing workgroups done
+  uint32_t arrive_f;               // radix route: workgroups done in the launch that ends the head
+  uint32_t fb_min;                 // radix route: smallest key above x_(lo)'s 22-bit bucket
+  uint32_t fb_prefix[2];           // radix route: key prefix after the first and second digit
+  int64_t fb_rem[2];               //   rank left inside that prefix
+  unsigned long long fb_lt[2];     //   entries below that prefix
+  unsigned long long fb_sum_c, fb_sum_c2;
+};
+
+// The first float above the bracket's keys.
+__device__ __forceinline__ float cv_bracket_top(uint32_t k_hi) {
+  const float f = k_hi == kCvNone ? INFINITY : cv_key_float(k_hi + 1);
+  return f != f ? INFINITY : f;
+}
+
+// Entries below the bracket: N less those at or above its bottom, which are
+// the pairs there plus the entries at or above the union's top (the entries
+// at or above t_hi less the pairs there).  Valid for a head whose pairs all
+// fit their buffers.
+__device__ __forceinline__ unsigned long long cv_below(const CvState& S, int64_t N) {
+  return (unsigned long long)N - S.ge_lo - S.c1 + S.ge_thi;
+}
+
+// The head takes the bracket route when every gathered pair fit its buffer
+// and the bracket holds ranks lo and lo + 1 (lo only, when lo = N - 1).
+// Decided alike by every launch after the pair count.
+__device__ __forceinline__ bool cv_bracket_route(const CvState& S, int64_t N) {
+  if (S.phi_over) return false;
+  const int64_t lo = S.rank;
+  const unsigned long long top = (unsigned long long)(lo + 1 <= N - 1 ? lo + 1 : lo);
+  const unsigned long long below = cv_below(S, N);
+  return below <= (unsigned long long)lo && top < below + S.n_cand;
+}
+
+// What the observation-matrix pass exchanges with the CV kernels.  Pairs
+// (value bits, key column) of the entries inside the union of the bracket
+// and Phi's range go to wave w of column block b's own buffer,
+// pairs + ((h * n_colblk + b) * nsub + w) * capw, its fill to
+// pfill[(h * n_colblk + b) * nsub + w].
+struct CvLink {
+  CvState* st;                     // [hkv]
+  float* samples;                  // [hkv][kCvSamples] sampled entries of A (from the row-statistics merge)
+  uint32_t* hist0;                 // [hkv][kCvBins] first digit of key - k_lo of the bracket entries
+  uint2* pairs;
+  uint32_t* pfill;
+  uint32_t capw;                   // pairs per wave buffer
+  int nsub;                        // waves per column block (buffers per block)
+  uint32_t* colcnt;                // [hkv][n_keys] entries >= t_hi per column
+  uint32_t* hist;                  // [4][hkv][kCvBins]: hist0, then the radix route's three digits
+  uint32_t* list;                  // [hkv][kCvListCap] bracket entries of x_(lo)'s first-digit bin
+};
+
+}  // namespace catekv

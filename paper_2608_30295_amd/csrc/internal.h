@@ -137,11 +137,7 @@ struct ScoreGeom {
 };
 
 size_t score_workspace_bytes(const ScoreGeom& g);
-// CV score (Eq. 2-4) of every KV head from its observation matrix A
-// ([hkv][lq][n_keys] fp32) into cv_out[hkv]; ws holds cv_workspace_bytes.
-size_t cv_workspace_bytes(int hkv, int lq, int64_t n_keys);
-hipError_t launch_cv(const float* A, int hkv, int lq, int64_t n_keys, double k_pct, double alpha, void* ws,
-                     float* cv_out, hipStream_t stream);
+
 hipError_t launch_score(int dtype, const ScoreGeom& g, const void* q_rows, const void* k,
                         float* cv_out, void* ws, hipStream_t stream);
 

@@ -42,13 +42,104 @@ __device__ float2 rowstats_exact(const ScoreArgs& a, int sel, int row, int b, in
   return make_float2(m, sum16(l));
 }
 
+constexpr int kMergeRows = 16;    // rows per 256-thread workgroup of the merge
+
+// CV (observation matrix): the sampled entries of A whose query rows are
+// the workgroup's kMergeRows rows (G divides kMergeRows, so a query's G rows
+// are all here), A = (1/G) sum_g exp2(s c - offset) in plain fp32 dot
+// products, one entry per thread at a time with the rows' Q in LDS; the
+// sample only has to place the quantile, the bracketing pass classifies A's
+// values as the observation pass computes them.
+template <typename T, int G>
+__device__ void cv_sample_rows(const ScoreArgs& a, int sel, int row0, float my_off) {
+  __shared__ float s_q[kMergeRows][kD + 1];   // +1: rows start in different banks
+  __shared__ float s_o[kMergeRows];
+  const int h = a.heads[sel];
+  const int t = threadIdx.x;
+  const uint32_t n_keys = (uint32_t)a.n_keys;
+  const int64_t N = (int64_t)a.lq * a.n_keys;     // below 2^32 (the entry points check)
+  for (int e = t; e < kMergeRows * kD; e += 256) {
+    const int rr = e / kD, d = e % kD, r = row0 + rr;
+    const int i = r / G, g = r - (r / G) * G;
+    const T* q = reinterpret_cast<const T*>(a.q) + ((size_t)(h * G + g) * a.lq + (r < a.R ? i : 0)) * kD;
+    float x;
+    if constexpr (sizeof(T) == 2) x = __uint_as_float((uint32_t)q[d] << 16);
+    else x = q[d];
+    s_q[rr][d] = r < a.R ? x : 0.f;
+  }
+  if ((t & 15) == 0) s_o[t >> 4] = my_off;
+  __syncthreads();
+  const int q0 = row0 / G, q1 = min(a.lq, (row0 + kMergeRows) / G);   // this workgroup's queries
+  if (q0 >= q1) return;
+  const int64_t ns = cv_sample_count(N), stride = cv_sample_stride(N);
+  const bool all = N < kCvSamples;                                   // sample s is entry s
+  const int64_t e0 = (int64_t)q0 * n_keys, e1 = (int64_t)q1 * n_keys;
+  // (plain selects: std::min / std::max return references, which the
+  // compiler would keep in scratch memory here)
+  const int64_t t0 = (e0 - (kCvSampleRun - 1) + stride - 1) / stride;
+  const int64_t s0 = all ? e0 : (t0 > 0 ? t0 : 0) * kCvSampleRun;
+  const int64_t s1r = all ? e1 : ((e1 - 1) / stride + 1) * kCvSampleRun;
+  const int64_t s1 = s1r < ns ? s1r : ns;
+  const T* kh = reinterpret_cast<const T*>(a.k) + (size_t)h * a.n * kD;
+  const float invG = 1.0f / (float)G;
+  for (int64_t s = s0 + t; s < s1; s += 256) {
+    const uint32_t ent = (uint32_t)(all ? s : (s / kCvSampleRun) * stride + (s % kCvSampleRun));
+    const uint32_t i = ent / n_keys, j = ent - (ent / n_keys) * n_keys;
+    if ((int)i < q0 || (int)i >= q1) continue;
+    const float* qr = s_q[(i - q0) * G];
+    const T* kr = kh + (size_t)(a.key_off + j) * kD;
+    float dot[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) dot[g] = 0.f;
+#pragma unroll 1
+    for (int c0 = 0; c0 < kD; c0 += 16) {       // 16 dims: their K values loaded together
+      float kv[16];
+      if constexpr (sizeof(T) == 2) {
+        uint4 w[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) w[u] = *reinterpret_cast<const uint4*>(kr + c0 + 8 * u);
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const uint32_t x[4] = {w[u].x, w[u].y, w[u].z, w[u].w};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            kv[8 * u + 2 * e] = bf16_lo(x[e]);
+            kv[8 * u + 2 * e + 1] = bf16_hi(x[e]);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float4 f = *reinterpret_cast<const float4*>(kr + c0 + 4 * u);
+          kv[4 * u] = f.x;
+          kv[4 * u + 1] = f.y;
+          kv[4 * u + 2] = f.z;
+          kv[4 * u + 3] = f.w;
+        }
+      }
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const float* qg = qr + g * (kD + 1) + c0;
+#pragma unroll
+        for (int d = 0; d < 16; ++d) dot[g] = __builtin_fmaf(qg[d], kv[d], dot[g]);
+      }
+    }
+    const bool vis = !a.causal || a.key_off + (int64_t)j <= a.q_pos0 + (int64_t)i;
+    float acc = 0.f;
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+      if (vis) acc += fast_exp2(__builtin_fmaf(dot[g], a.c, -s_o[(i - q0) * G + g]));
+    a.cv.samples[(size_t)sel * kCvSamples + s] = acc * invG;
+  }
+}
+
 // Merge the per-column-block row statistics: offset = m c + log2(l), +inf
 // for rows with no visible key and for padding rows.  16 lanes share a row
 // and walk its column blocks with independent loads, then reduce over DPP.
 // A block whose sum overflowed is recomputed exactly first.
-constexpr int kMergeRows = 16;    // rows per 256-thread workgroup
 template <typename T>
-__global__ __launch_bounds__(256) void rowstats_merge_kernel(ScoreArgs a, int rpad, float* __restrict__ off) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 4))) void rowstats_merge_kernel(ScoreArgs a, int rpad,
+                                                                                               float* __restrict__ off) {
   const int sel = blockIdx.y;
   const int n_colblk = a.n_colblk, R = a.R;
   const int row = blockIdx.x * kMergeRows + (threadIdx.x >> 4);
@@ -93,7 +184,15 @@ __global__ __launch_bounds__(256) void rowstats_merge_kernel(ScoreArgs a, int rp
   }
   const float M16 = max16(M);
   L = sum16(L * fast_exp2(M - M16));
-  if (ln == 0 && row < rpad) off[(size_t)sel * rpad + row] = (ok && L > 0.f) ? M16 + __log2f(L) : INFINITY;
+  const float o = (ok && L > 0.f) ? M16 + __log2f(L) : INFINITY;
+  if (ln == 0 && row < rpad) off[(size_t)sel * rpad + row] = o;
+  if (a.cv.samples) {
+    const int r0 = blockIdx.x * kMergeRows;
+    if (a.G == 1) cv_sample_rows<T, 1>(a, sel, r0, o);
+    else if (a.G == 2) cv_sample_rows<T, 2>(a, sel, r0, o);
+    else if (a.G == 4) cv_sample_rows<T, 4>(a, sel, r0, o);
+    else cv_sample_rows<T, 8>(a, sel, r0, o);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -654,7 +753,7 @@ static ScoreLayout score_layout(const ScoreGeom& g) {
   L.rowpart = o; o += align256((size_t)g.hkv * g.n_colblk * rp * sizeof(float2));
   L.rowoff = o; o += align256((size_t)g.hkv * rp * sizeof(float));
   L.obs = o; o += align256((size_t)g.hkv * g.lq * g.n_keys * sizeof(float));
-  L.cv = o; o += align256(cv_workspace_bytes(g.hkv, g.lq, g.n_keys));
+  L.cv = o; o += align256(cv_workspace_bytes(g.hkv, g.lq, g.n_keys, g.n_colblk));
   L.total = o;
   return L;
 }
@@ -675,6 +774,7 @@ hipError_t launch_score(int dtype, const ScoreGeom& g, const void* q_rows, const
   a.rowpart = reinterpret_cast<float2*>(w + L.rowpart);
   a.rowoff = reinterpret_cast<const float*>(w + L.rowoff);
   a.obs = reinterpret_cast<float*>(w + L.obs);
+  a.cv = cv_link(w + L.cv, g.hkv, g.lq, g.n_keys, g.n_colblk, kCvMaxSub);
   const dim3 grid(g.n_colblk, g.hkv);
   hipError_t e = launch_score_rowstats(dtype, g.G, g.causal, rp, grid, stream, a);
   if (e != hipSuccess) return e;
@@ -684,10 +784,18 @@ hipError_t launch_score(int dtype, const ScoreGeom& g, const void* q_rows, const
   else
     hipLaunchKernelGGL(rowstats_merge_kernel<float>, dim3((rp + kMergeRows - 1) / kMergeRows, g.hkv), dim3(256), 0,
                        stream, a, rp, reinterpret_cast<float*>(w + L.rowoff));
+  // the merge also took the sampled entries of A; the bracket from them,
+  // the bracketing pass, A itself only for the heads the bracket missed
+  e = launch_cv_sample(a, g.k_pct, g.alpha, stream);
+  if (e != hipSuccess) return e;
+  e = launch_score_obs_bracket(dtype, g.G, g.causal, rp, grid, stream, a);
+  if (e != hipSuccess) return e;
+  e = launch_cv_pairs(a, stream);
+  if (e != hipSuccess) return e;
+  a.cv_gate = 1;
   e = launch_score_obs(dtype, g.G, g.causal, rp, grid, stream, a);
   if (e != hipSuccess) return e;
-
-  return launch_cv(a.obs, g.hkv, g.lq, g.n_keys, g.k_pct, g.alpha, w + L.cv, cv_out, stream);
+  return launch_cv_finish(a, g.k_pct, g.alpha, cv_out, stream);
 }
 
 }  // namespace catekv

@@ -13,6 +13,7 @@
 #pragma once
 
 #include "common.h"
+#include "cv_state.h"
 #include "internal.h"
 
 #include <type_traits>
@@ -80,7 +81,7 @@ template <typename T> struct Shape {
   __device__ static __forceinline__ float row_sum(float x) { return sum16(x); }
   __device__ static __forceinline__ float col_sum(float x) { return add_xor32(add_xor16(x)); }
 };
-enum ScoreMode { kRowStats = 0, kColMass = 1, kObsMatrix = 2 };
+enum ScoreMode { kRowStats = 0, kColMass = 1, kObsMatrix = 2, kObsBracket = 3 };
 enum RowStatsVar { kRsSum = 0, kRsMax = 1 };
 
 struct ScoreArgs {
@@ -103,6 +104,12 @@ struct ScoreArgs {
   int cs_fused;           // chunk size when it divides the 64-column tile, else 0
   int64_t n_chunks;
   float* obs;             // kObsMatrix out: [n_sel][lq][n_keys]
+  // kObsBracket: A's values classified against the CV bracket instead of
+  // stored (below it, inside the union of bracket and Phi's range, at or
+  // above t_hi per column); kObsMatrix with cv_gate set skips the heads
+  // whose bracket took them (only the radix route reads A)
+  CvLink cv;
+  int cv_gate;
 };
 
 template <typename T, int W, int MT, int MODE, int G, bool CAUSAL>
@@ -114,7 +121,8 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
   // G = 0: the group size is taken at run time (a.G); only the passes whose
   // arithmetic never splits a group's rows (row statistics without a causal
   // mask, column mass) are built that way
-  static_assert(G > 0 || (!CAUSAL && MODE != kObsMatrix), "G must be fixed for masks and the group mean");
+  constexpr bool OBSB = MODE == kObsBracket;
+  static_assert(G > 0 || (!CAUSAL && MODE != kObsMatrix && !OBSB), "G must be fixed for masks and the group mean");
   const int GR = G > 0 ? G : a.G;
   constexpr int RPAD = W * MT * TR;
   constexpr int NSTAGE = kTileTok * SEG / (W * 64);   // 16-byte loads per thread per tile
@@ -122,7 +130,7 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
   // s_waitcnt immediate: vmcnt <= NSTAGE * (NRING - 2), expcnt not waited on;
   // lgkmcnt(0) in column-mass mode, whose column partials in LDS the barrier publishes
   constexpr int VM = NSTAGE * (NRING - 2);
-  constexpr int LGKM = MODE == kColMass ? 0 : 0xF;
+  constexpr int LGKM = MODE == kColMass || OBSB ? 0 : 0xF;
   constexpr int kWaitRing = (VM & 0xF) | ((VM >> 4) << 14) | (0x7 << 4) | (LGKM << 8);
   // one LDS array per ring stage: stages chosen at compile time do not alias,
   // so the compiler adds no waits of its own between the loads and the reads
@@ -137,6 +145,7 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
   const int64_t col0 = (int64_t)cb * a.cb_tokens;                   // first key column
   const int64_t col_end = min(col0 + a.cb_tokens, a.n_keys);
   const int n_tiles = (int)((col_end - col0 + kTileTok - 1) / kTileTok);
+  if (MODE == kObsMatrix && a.cv_gate && cv_bracket_route(a.cv.st[sel], (int64_t)a.lq * a.n_keys)) return;
   const T* kh = reinterpret_cast<const T*>(a.k) + (size_t)h * a.n * kD;
   const T* qb = reinterpret_cast<const T*>(a.q);
 
@@ -168,6 +177,33 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
       off[mt][r] = 0.f;
       if (MODE != kRowStats) off[mt][r] = a.rowoff[(size_t)sel * RPAD + row_of(mt, r)];
     }
+
+  // kObsBracket: t_hi and the union of the bracket and Phi's range; this
+  // wave's pair buffer (fill: wave-uniform)
+  uint32_t wfill = 0;
+  float bt_hi = 0.f, bu_lo = 0.f, bu_hi = 0.f;
+  unsigned long long ca1 = 0, ca2 = 0;
+  uint2* wpairs = nullptr;
+  if (OBSB) {
+    const CvState& B = a.cv.st[sel];
+    bt_hi = B.t_hi;
+    bu_lo = fminf(cv_key_float(B.k_lo), B.t_lo);
+    bu_hi = fmaxf(cv_bracket_top(B.k_hi), bt_hi);
+    wpairs = a.cv.pairs + (((size_t)sel * a.n_colblk + cb) * a.cv.nsub + wave) * a.cv.capw;
+  }
+  // one A value of this lane (key column col; ok: a real entry): counted for
+  // its column at or above t_hi, written out inside the union
+  auto classify = [&](float v, bool ok, int64_t col, int t, float (&cnt)[kTileTok / TC]) {
+    cnt[t] += (ok && v >= bt_hi) ? 1.f : 0.f;
+    const bool in_u = ok && v >= bu_lo && v < bu_hi;
+    const uint64_t bal = __builtin_amdgcn_ballot_w64(in_u);
+    if (bal) {
+      const uint32_t at = wfill + (uint32_t)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                                                      __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+      if (in_u && at < a.cv.capw) wpairs[at] = make_uint2(__float_as_uint(v), (uint32_t)col);
+      wfill += (uint32_t)__builtin_popcountll(bal);
+    }
+  };
 
   // K tiles arrive through a ring of NRING LDS stages filled by direct
   // global-to-LDS loads (no staging registers).  Thread x's load i lands in
@@ -210,8 +246,17 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
     float v = 0.f;
 #pragma unroll
     for (int w = 0; w < W; ++w) v += s_col[p][w][lane];
-    v *= 1.0f / (float)GR;
     const int64_t col = col0 + (int64_t)t * kTileTok + lane;
+    if (OBSB) {                    // entries >= t_hi of the column (exact small integers in fp32)
+      if (col < col_end) {
+        const uint32_t c = (uint32_t)v;
+        a.cv.colcnt[(size_t)sel * a.n_keys + col] = c;
+        ca1 += c;
+        ca2 += (unsigned long long)c * c;
+      }
+      return;
+    }
+    v *= 1.0f / (float)GR;
     if (a.cs_fused > 0) {
       const float mx = max_in_group(col < col_end ? v : -INFINITY, a.cs_fused);
       if ((lane & (a.cs_fused - 1)) == 0 && col < col_end)
@@ -300,7 +345,7 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
 #pragma unroll
             for (int r = 0; r < NR; ++r)
               cmass[hh * NCT + ct] += fast_exp2(__builtin_fmaf(acc[ct][mt][r], a.c, -off[mt][r]));
-      } else {  // kObsMatrix: group mean over the G rows of each query i
+      } else {  // kObsMatrix / kObsBracket: group mean over the G rows of each query i
         const float invG = 1.0f / (float)G;
 #pragma unroll
         for (int ct = 0; ct < NCT; ++ct) {
@@ -315,13 +360,15 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
               // the lane's NR registers hold NR consecutive rows from a multiple of 4:
               // queries i0 .. i0 + NR / G - 1, one store base for all of them
               const int i0 = row_of(mt, 0) / G;
-              float* ob = a.obs + ((size_t)sel * a.lq + i0) * a.n_keys + col;
+              float* ob = OBSB ? nullptr : a.obs + ((size_t)sel * a.lq + i0) * a.n_keys + col;
 #pragma unroll
               for (int r0 = 0; r0 < NR; r0 += G) {
                 float v = p[r0];
 #pragma unroll
                 for (int r = 1; r < G; ++r) v += p[r0 + r];
-                if (i0 + r0 / G < a.lq && colok) ob[(size_t)(r0 / G) * a.n_keys] = v * invG;
+                const bool ok = i0 + r0 / G < a.lq && colok;
+                if (OBSB) classify(v * invG, ok, col, hh * NCT + ct, cmass);
+                else if (ok) ob[(size_t)(r0 / G) * a.n_keys] = v * invG;
               }
             } else {  // G == 8: lanes l and l ^ kPair8 hold the two halves of each group of 8 rows
 #pragma unroll
@@ -329,8 +376,9 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
                 const float q4 = p[b4] + p[b4 + 1] + p[b4 + 2] + p[b4 + 3];
                 const float v = S::kPair8 == 16 ? add_xor16(q4) : add_xor32(q4);
                 const int i = row_of(mt, b4) / 8;
-                if ((lane & S::kPair8) == 0 && i < a.lq && colok)
-                  a.obs[((size_t)sel * a.lq + i) * a.n_keys + col] = v * invG;
+                const bool ok = (lane & S::kPair8) == 0 && i < a.lq && colok;
+                if (OBSB) classify(v * invG, ok, col, hh * NCT + ct, cmass);
+                else if (ok) a.obs[((size_t)sel * a.lq + i) * a.n_keys + col] = v * invG;
               }
             }
           }
@@ -347,7 +395,7 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
     mfma_half(1, acc1);
     valu_half(1, acc1, mask_tag);
 
-    if (MODE == kColMass) {
+    if (MODE == kColMass || OBSB) {
       // sum over the lanes holding each column; each wave leaves its partial in LDS
 #pragma unroll
       for (int t = 0; t < kTileTok / TC; ++t) {
@@ -369,7 +417,7 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
     __builtin_amdgcn_s_barrier();
     compiler_fence();
     issue(ring((S + NRING - 1) % NRING), tile + NRING - 1);
-    if (MODE == kColMass && tile > 0 && wave == ((tile - 1) & (W - 1))) finish_cols(tile - 1);
+    if ((MODE == kColMass || OBSB) && tile > 0 && wave == ((tile - 1) & (W - 1))) finish_cols(tile - 1);
     body(ring(S), tile);
   };
   auto prime = [&]() {
@@ -434,7 +482,7 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
     run(std::integral_constant<int, 0>{}, RsSum{});
   }
 
-  if (MODE == kColMass) {
+  if (MODE == kColMass || OBSB) {
     barrier_lds_only();
     if (n_tiles > 0 && wave == ((n_tiles - 1) & (W - 1))) finish_cols(n_tiles - 1);
   }
@@ -442,6 +490,30 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
   // the ring's trailing loads must land before the workgroup's LDS is released
   __builtin_amdgcn_s_waitcnt(0);
   compiler_fence();
+
+  if (OBSB) {
+    // the workgroup's column-count sums and pair fills to the head's state
+    __shared__ unsigned long long s_sum[2][16];
+    unsigned long long x0 = ca1, x1 = ca2;
+    for (int o = 32; o > 0; o >>= 1) {
+      x0 += __shfl_xor(x0, o);
+      x1 += __shfl_xor(x1, o);
+    }
+    if (lane == 0) {
+      s_sum[0][wave] = x0;
+      s_sum[1][wave] = x1;
+      a.cv.pfill[((size_t)sel * a.n_colblk + cb) * a.cv.nsub + wave] = min(wfill, a.cv.capw);
+      if (wfill > a.cv.capw) atomicOr(&a.cv.st[sel].phi_over, 1u);
+    }
+    if (threadIdx.x >= W && threadIdx.x < a.cv.nsub)   // buffers of waves this shape does not have
+      a.cv.pfill[((size_t)sel * a.n_colblk + cb) * a.cv.nsub + threadIdx.x] = 0;
+    barrier_lds_only();
+    if (threadIdx.x < 2) {
+      unsigned long long v = 0;
+      for (int w = 0; w < W; ++w) v += s_sum[threadIdx.x][w];
+      if (v) atomicAdd(threadIdx.x == 0 ? &a.cv.st[sel].c1 : &a.cv.st[sel].c2, v);
+    }
+  }
 
   if (MODE == kRowStats) {
     // merge the lanes that share each row (maxima in log2 units)
@@ -478,7 +550,7 @@ inline hipError_t launch_score_mt(int rows_pad, dim3 grid, hipStream_t s, const 
   constexpr bool F32 = std::is_same<T, float>::value;
   // one query per row (G = 1) stores every row of the observation matrix on
   // its own: those passes keep two waves per SIMD
-  constexpr bool NARROW = MODE == kObsMatrix && G == 1;
+  constexpr bool NARROW = (MODE == kObsMatrix || MODE == kObsBracket) && G == 1;
 #define CATEKV_SK(WW, MM, PP) \
   hipLaunchKernelGGL((score_kernel<T, WW, MM, MODE, G, CAUSAL, PP>), grid, dim3((WW) * 64), 0, s, a)
   if constexpr (F32) {
@@ -511,5 +583,16 @@ hipError_t launch_score_rowstats(int dtype, int G, bool causal, int rows_pad, di
 hipError_t launch_score_colmass(int dtype, int rows_pad, dim3 grid, hipStream_t s, const ScoreArgs& a);
 hipError_t launch_score_obs(int dtype, int G, bool causal, int rows_pad, dim3 grid, hipStream_t s,
                             const ScoreArgs& a);
+hipError_t launch_score_obs_bracket(int dtype, int G, bool causal, int rows_pad, dim3 grid, hipStream_t s,
+                                    const ScoreArgs& a);
+
+// The CV score's own kernels (cv.hip) around the observation-matrix passes:
+// the workspace they share, the bracket from the merge's samples, and after
+// the bracketing pass the order statistic, the column counts and the score.
+size_t cv_workspace_bytes(int hkv, int lq, int64_t n_keys, int n_colblk);
+CvLink cv_link(void* ws, int hkv, int lq, int64_t n_keys, int n_colblk, int nsub);
+hipError_t launch_cv_sample(const ScoreArgs& a, double k_pct, double alpha, hipStream_t s);
+hipError_t launch_cv_pairs(const ScoreArgs& a, hipStream_t s);
+hipError_t launch_cv_finish(const ScoreArgs& a, double k_pct, double alpha, float* cv_out, hipStream_t s);
 
 }  // namespace catekv
