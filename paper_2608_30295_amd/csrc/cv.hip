@@ -282,11 +282,12 @@ __device__ __forceinline__ void flush_hist(const uint32_t* s_h, uint32_t* __rest
 // Pairs of column block b (its waves' buffers): the bracket entries are
 // counted and histogrammed by their first digit, and the pairs at or above
 // the bracket's bottom and at or above t_hi counted (the entries below the
-// bracket follow, cv_below).
+// bracket follow, cv_below); sum c and sum c^2 over the block's columns.
 __global__ __launch_bounds__(256) void cv_pairs_kernel(CvState* st, uint32_t* __restrict__ hist0,
                                                        const uint2* __restrict__ pairs,
                                                        const uint32_t* __restrict__ pfill, uint32_t capw, int nsub,
-                                                       int n_colblk) {
+                                                       int n_colblk, const uint32_t* __restrict__ colcnt,
+                                                       int64_t n_keys, int64_t cb_tokens) {
   __shared__ uint32_t s_h[kBins];
   __shared__ unsigned long long s_red[4];
   const int h = blockIdx.y, b = blockIdx.x;
@@ -319,13 +320,27 @@ __global__ __launch_bounds__(256) void cv_pairs_kernel(CvState* st, uint32_t* __
       }
     }
   }
+  // sum c and sum c^2 over the block's columns
+  unsigned long long c1 = 0, c2 = 0;
+  const int64_t j0 = (int64_t)b * cb_tokens, j1 = j0 + cb_tokens < n_keys ? j0 + cb_tokens : n_keys;
+  for (int64_t j = j0 + t; j < j1; j += 256) {
+    const unsigned long long c = colcnt[(size_t)h * n_keys + j];
+    c1 += c;
+    c2 += c * c;
+  }
   const unsigned long long a_in = block_sum256(n_in, s_red);
   const unsigned long long a_lo = block_sum256(n_lo, s_red);
   const unsigned long long a_thi = block_sum256(n_thi, s_red);
+  const unsigned long long a_c1 = block_sum256(c1, s_red);
+  const unsigned long long a_c2 = block_sum256(c2, s_red);
   if (t == 0) {
     if (a_in) atomicAdd(&S.n_cand, a_in);
     if (a_lo) atomicAdd(&S.ge_lo, a_lo);
     if (a_thi) atomicAdd(&S.ge_thi, a_thi);
+    if (a_c1) {
+      atomicAdd(&S.c1, a_c1);
+      atomicAdd(&S.c2, a_c2);
+    }
   }
   flush_hist(s_h, hist0 + (size_t)h * kBins);
 }
@@ -831,7 +846,7 @@ hipError_t launch_cv_sample(const ScoreArgs& a, double k_pct, double alpha, hipS
 
 hipError_t launch_cv_pairs(const ScoreArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL(cv_pairs_kernel, dim3((unsigned)a.n_colblk, a.hkv), dim3(256), 0, stream, a.cv.st, a.cv.hist,
-                     a.cv.pairs, a.cv.pfill, a.cv.capw, a.cv.nsub, a.n_colblk);
+                     a.cv.pairs, a.cv.pfill, a.cv.capw, a.cv.nsub, a.n_colblk, a.cv.colcnt, a.n_keys, a.cb_tokens);
   return hipGetLastError();
 }
 

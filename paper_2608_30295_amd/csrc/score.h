@@ -105,9 +105,9 @@ struct ScoreArgs {
   int64_t n_chunks;
   float* obs;             // kObsMatrix out: [n_sel][lq][n_keys]
   // kObsBracket: A's values classified against the CV bracket instead of
-  // stored (below it, inside the union of bracket and Phi's range, at or
-  // above t_hi per column); kObsMatrix with cv_gate set skips the heads
-  // whose bracket took them (only the radix route reads A)
+  // stored (inside the union of bracket and Phi's range, at or above t_hi
+  // per column); kObsMatrix with cv_gate set skips the heads whose bracket
+  // took them (only the radix route reads A)
   CvLink cv;
   int cv_gate;
 };
@@ -182,7 +182,6 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
   // wave's pair buffer (fill: wave-uniform)
   uint32_t wfill = 0;
   float bt_hi = 0.f, bu_lo = 0.f, bu_hi = 0.f;
-  unsigned long long ca1 = 0, ca2 = 0;
   uint2* wpairs = nullptr;
   if (OBSB) {
     const CvState& B = a.cv.st[sel];
@@ -193,14 +192,14 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
   }
   // one A value of this lane (key column col; ok: a real entry): counted for
   // its column at or above t_hi, written out inside the union
-  auto classify = [&](float v, bool ok, int64_t col, int t, float (&cnt)[kTileTok / TC]) {
-    cnt[t] += (ok && v >= bt_hi) ? 1.f : 0.f;
+  auto classify = [&](float v, bool ok, uint32_t col, int t, uint32_t& cnt) {
+    cnt += (ok && v >= bt_hi) ? 1u << (8 * t) : 0u;   // four 8-bit counters (a lane adds at most MT NR per tile)
     const bool in_u = ok && v >= bu_lo && v < bu_hi;
     const uint64_t bal = __builtin_amdgcn_ballot_w64(in_u);
     if (bal) {
       const uint32_t at = wfill + (uint32_t)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
                                                                       __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
-      if (in_u && at < a.cv.capw) wpairs[at] = make_uint2(__float_as_uint(v), (uint32_t)col);
+      if (in_u && at < a.cv.capw) wpairs[at] = make_uint2(__float_as_uint(v), col);
       wfill += (uint32_t)__builtin_popcountll(bal);
     }
   };
@@ -243,19 +242,17 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
   // dividing 64 a chunk never straddles a tile and BlockMax is taken here.
   auto finish_cols = [&](int t) {
     const int p = t & 1;
+    const int64_t col = col0 + (int64_t)t * kTileTok + lane;
+    if (OBSB) {                    // entries >= t_hi of the column (exact small integers in fp32)
+      float c = 0.f;
+#pragma unroll 1
+      for (int w = 0; w < W; ++w) c += s_col[p][w][lane];
+      if (col < col_end) a.cv.colcnt[(size_t)sel * a.n_keys + col] = (uint32_t)c;
+      return;
+    }
     float v = 0.f;
 #pragma unroll
     for (int w = 0; w < W; ++w) v += s_col[p][w][lane];
-    const int64_t col = col0 + (int64_t)t * kTileTok + lane;
-    if (OBSB) {                    // entries >= t_hi of the column (exact small integers in fp32)
-      if (col < col_end) {
-        const uint32_t c = (uint32_t)v;
-        a.cv.colcnt[(size_t)sel * a.n_keys + col] = c;
-        ca1 += c;
-        ca2 += (unsigned long long)c * c;
-      }
-      return;
-    }
     v *= 1.0f / (float)GR;
     if (a.cs_fused > 0) {
       const float mx = max_in_group(col < col_end ? v : -INFINITY, a.cs_fused);
@@ -292,6 +289,7 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
     float cmass[kTileTok / TC];
 #pragma unroll
     for (int t = 0; t < kTileTok / TC; ++t) cmass[t] = -0.f;   // -0 + x folds to x
+    uint32_t ccount = 0;                                          // kObsBracket: per column position t, bits 8t..8t+7
     // the MFMA work of one half tile (32 columns: NCT column tiles); k-step
     // outer, row tile inner: a B fragment is live for MT MFMAs, and the MT
     // accumulator chains interleave
@@ -350,6 +348,7 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
 #pragma unroll
         for (int ct = 0; ct < NCT; ++ct) {
           const int64_t col = tcol0 + hh * 32 + ct * TC + S::col(lane);
+          const uint32_t col32 = (uint32_t)tcol0 + (uint32_t)(hh * 32 + ct * TC + S::col(lane));   // key columns < 2^32
           const bool colok = !MASK || col < col_end;
 #pragma unroll
           for (int mt = 0; mt < MT; ++mt) {
@@ -367,7 +366,7 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
 #pragma unroll
                 for (int r = 1; r < G; ++r) v += p[r0 + r];
                 const bool ok = i0 + r0 / G < a.lq && colok;
-                if (OBSB) classify(v * invG, ok, col, hh * NCT + ct, cmass);
+                if (OBSB) classify(v * invG, ok, col32, hh * NCT + ct, ccount);
                 else if (ok) ob[(size_t)(r0 / G) * a.n_keys] = v * invG;
               }
             } else {  // G == 8: lanes l and l ^ kPair8 hold the two halves of each group of 8 rows
@@ -377,7 +376,7 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
                 const float v = S::kPair8 == 16 ? add_xor16(q4) : add_xor32(q4);
                 const int i = row_of(mt, b4) / 8;
                 const bool ok = (lane & S::kPair8) == 0 && i < a.lq && colok;
-                if (OBSB) classify(v * invG, ok, col, hh * NCT + ct, cmass);
+                if (OBSB) classify(v * invG, ok, col32, hh * NCT + ct, ccount);
                 else if (ok) a.obs[((size_t)sel * a.lq + i) * a.n_keys + col] = v * invG;
               }
             }
@@ -399,7 +398,7 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
       // sum over the lanes holding each column; each wave leaves its partial in LDS
 #pragma unroll
       for (int t = 0; t < kTileTok / TC; ++t) {
-        const float v = S::col_sum(cmass[t]);
+        const float v = S::col_sum(OBSB ? (float)((ccount >> (8 * t)) & 0xFFu) : cmass[t]);
         if (lane < TC) s_col[tile & 1][wave][t * TC + lane] = v;
       }
     }
@@ -491,28 +490,13 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
   __builtin_amdgcn_s_waitcnt(0);
   compiler_fence();
 
-  if (OBSB) {
-    // the workgroup's column-count sums and pair fills to the head's state
-    __shared__ unsigned long long s_sum[2][16];
-    unsigned long long x0 = ca1, x1 = ca2;
-    for (int o = 32; o > 0; o >>= 1) {
-      x0 += __shfl_xor(x0, o);
-      x1 += __shfl_xor(x1, o);
-    }
+  if (OBSB) {                      // the waves' pair fills
     if (lane == 0) {
-      s_sum[0][wave] = x0;
-      s_sum[1][wave] = x1;
       a.cv.pfill[((size_t)sel * a.n_colblk + cb) * a.cv.nsub + wave] = min(wfill, a.cv.capw);
       if (wfill > a.cv.capw) atomicOr(&a.cv.st[sel].phi_over, 1u);
     }
     if (threadIdx.x >= W && threadIdx.x < a.cv.nsub)   // buffers of waves this shape does not have
       a.cv.pfill[((size_t)sel * a.n_colblk + cb) * a.cv.nsub + threadIdx.x] = 0;
-    barrier_lds_only();
-    if (threadIdx.x < 2) {
-      unsigned long long v = 0;
-      for (int w = 0; w < W; ++w) v += s_sum[threadIdx.x][w];
-      if (v) atomicAdd(threadIdx.x == 0 ? &a.cv.st[sel].c1 : &a.cv.st[sel].c2, v);
-    }
   }
 
   if (MODE == kRowStats) {

@@ -401,6 +401,51 @@ def test_score_heads_crowded_and_spread_quantile_bins():
     np.testing.assert_allclose(cv, ref, rtol=1e-4, atol=1e-6)
 
 
+@pytest.mark.parametrize("k_pct,alpha", [(0.984, 0.8), (0.99, 1.0), (0.996, 0.8)])
+def test_score_heads_paper_percentiles(k_pct, alpha):
+    """The percentile thresholds and scaling factors of the paper's settings
+    (Section 5): Phi = alpha * Quantile_k below the quantile itself when
+    alpha < 1, so Phi's range and the bracket are apart."""
+    wl = _small("ctx32k_bf16", n=6000)
+    seq = synth.make_sequence(wl)
+    say(f"score_heads k={k_pct} alpha={alpha}")
+    cv = ck.score_heads(to_dev(seq.q_cv), to_dev(seq.k), q_pos0=seq.q_cv_pos0, l_init=wl.l_init,
+                        l_rec=wl.l_rec, k_pct=k_pct, alpha=alpha)
+    torch.cuda.synchronize()
+    cv = cv.cpu().numpy().astype(np.float64)
+    ref = O.score_heads(f64(seq.q_cv), seq.q_cv_pos0, f64(seq.k), wl.l_init, wl.l_rec, k_pct, alpha)
+    say("  gpu", np.round(cv, 6), "\n  ref", np.round(ref, 6))
+    np.testing.assert_allclose(cv, ref, rtol=1e-4, atol=1e-6)
+
+
+@pytest.mark.parametrize("n,m,k_pct", [(20000, 40, 0.999), (60000, 1040, 0.99)])
+def test_score_heads_tied_top_columns(n, m, k_pct):
+    """Closed form with a tie at the quantile: identical query rows, m key
+    columns (spread evenly) with one equal, larger score and the others
+    small and spread out.  Rank lo lands among the lq * m tied entries, so Phi is their
+    value, C is lq on the m columns and 0 elsewhere, cv = sqrt((n - m) / m).
+    The tied bin holds 2560 entries (a list resolved digit by digit) or
+    66560 (more than the list takes: resolved over every gathered entry)."""
+    lq, G = 64, 4
+    rng = np.random.default_rng(7)
+    k = np.zeros((1, n, 128), dtype=np.float32)
+    k[0, :, 1:] = 0.1 * rng.standard_normal((n, 127), dtype=np.float32)
+    cols = np.linspace(0, n - 1, m).astype(np.int64)
+    k[0, cols, :] = 0.0
+    k[0, cols, 0] = 8.0                      # exact in bf16: score 8 / sqrt(128) against q = e_0
+    q = np.zeros((G, lq, 128), dtype=np.float32)
+    q[:, :, 0] = 1.0
+    q[:, :, 1:] = 0.5 * rng.standard_normal(127, dtype=np.float32)   # the other columns' scores spread out
+    kb, qb = synth.f32_to_bf16_bits(k), synth.f32_to_bf16_bits(q)
+    say(f"tied top columns n={n} m={m} k={k_pct} (tie of {lq * m} entries)")
+    cv = ck.score_heads(to_dev(qb), to_dev(kb), q_pos0=n, l_init=0, l_rec=0, k_pct=k_pct, alpha=1.0, causal=False)
+    torch.cuda.synchronize()
+    want = math.sqrt((n - m) / m)
+    got = float(cv.cpu()[0])
+    say(f"  gpu {got:.6f} closed form {want:.6f}")
+    assert abs(got - want) <= 1e-5 * want
+
+
 def test_score_heads_toy_through_abi():
     # the hand-worked 2 x 4 toy (cv = sqrt(3)) driven through the GPU path
     A = np.array([[0.7, 0.1, 0.1, 0.1], [0.6, 0.2, 0.1, 0.1]])
