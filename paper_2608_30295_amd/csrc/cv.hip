@@ -6,13 +6,11 @@
 // population standard deviation of C over its mean.
 //
 // Bracket route: a sample of A gives a key range [k_lo, k_hi] expected to
-// hold ranks lo and lo + 1, and with it a range [t_lo, t_hi) that then holds
-// Phi.  One walk over A, column by column, counts the entries below the key
-// range, counts per column the entries at or above t_hi (at or above Phi
-// whatever its exact value) and gathers the few entries inside either range
-// with their columns.  x_(lo), x_(lo+1) and Phi are resolved over the
-// gathered entries, and the gathered values at or above Phi join their
-// columns' counts.
+// hold ranks lo and lo + 1, and with it a bound t_lo <= Phi.  The
+// observation pass writes out the few entries at or above the lower of the
+// two bounds with their columns (every entry at or above Phi is among
+// them); x_(lo), x_(lo+1) and Phi are resolved over those inside the key
+// range, and C_j is the count of column j's gathered values at or above Phi.
 // Radix route: when the sample's range misses a rank, or the gathered
 // entries overflow their buffer (heavy ties), exact radix passes over A
 // take over for that head.
@@ -61,17 +59,17 @@ __device__ void locate_ranks(const uint32_t* hh, int nb, int64_t r0, int64_t r1,
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   __syncthreads();                 // earlier readers of s_bin / s_pos are done
   uint32_t c[BPT];
-  int64_t mine = 0;
+  uint32_t mine = 0;               // a head's counts stay below 2^32 (N < 2^32)
 #pragma unroll
   for (int i = 0; i < BPT; ++i) {
     const int b = t * BPT + i;
     c[i] = b < nb ? hh[b] : 0u;
     mine += c[i];
   }
-  int64_t x = mine;
+  uint32_t x = mine;
 #pragma unroll
   for (int off = 1; off < 64; off <<= 1) {
-    const int64_t y = __shfl_up(x, off);
+    const uint32_t y = __shfl_up(x, off);
     if (lane >= off) x += y;
   }
   if (lane == 63) s_tot[wave] = x;
@@ -81,7 +79,7 @@ __device__ void locate_ranks(const uint32_t* hh, int nb, int64_t r0, int64_t r1,
     s_pos[0] = s_pos[1] = 0;
   }
   __syncthreads();
-  int64_t before = x - mine;
+  int64_t before = (int64_t)(x - mine);
   for (int w = 0; w < wave; ++w) before += s_tot[w];
 #pragma unroll
   for (int i = 0; i < BPT; ++i) {
@@ -108,6 +106,21 @@ __device__ __forceinline__ unsigned long long block_sum256(unsigned long long v,
   if ((threadIdx.x & 63) == 0) s[threadIdx.x >> 6] = v;
   __syncthreads();
   return s[0] + s[1] + s[2] + s[3];
+}
+
+// K sums over a workgroup of 256 threads at once (one exchange).
+template <int K>
+__device__ __forceinline__ void block_sums256(unsigned long long (&v)[K], unsigned long long (*s)[4]) {
+#pragma unroll
+  for (int k = 0; k < K; ++k)
+    for (int off = 32; off > 0; off >>= 1) v[k] += __shfl_xor(v[k], off);
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0)
+#pragma unroll
+    for (int k = 0; k < K; ++k) s[k][threadIdx.x >> 6] = v[k];
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < K; ++k) v[k] = s[k][0] + s[k][1] + s[k][2] + s[k][3];
 }
 
 // Eq. 4 from exact integer sums: sqrt(E[C^2] - E[C]^2) / E[C].
@@ -148,9 +161,10 @@ __device__ __forceinline__ double phi_of(double xlo, double xhi, int64_t N, doub
 
 // The sample's first two radix digits give the 22-bit key prefixes holding
 // sample ranks lo s / N -+ (8 sigma + 32), sigma the binomial spread of a
-// sample rank; the bracket is every key with a prefix in that range.  Phi's
-// range follows from the bracket's floats, widened by 2^-40 relative (far
-// beyond the rounding of the fp64 interpolation) and rounded outward to floats.
+// sample rank; the bracket is every key with a prefix in that range.  As
+// x_(lo) >= the bracket's bottom f_lo, Phi >= alpha f_lo: t_lo is that bound
+// less 2^-40 relative (far beyond the rounding of the fp64 interpolation),
+// rounded down to a float.
 constexpr int kSampleThreads = 1024;
 constexpr int kSamplePer = kCvSamples / kSampleThreads;
 
@@ -201,29 +215,21 @@ __global__ __launch_bounds__(kSampleThreads) void cv_sample_kernel(const float* 
     const uint32_t k_lo = p_lo << 10;
     const uint32_t k_hi = p_hi == 0x3FFFFFu ? 0xFFFFFFFFu : ((p_hi + 1) << 10) - 1;
     const float f_lo = key_to_float(k_lo);
-    float f_hi = k_hi == 0xFFFFFFFFu ? INFINITY : key_to_float(k_hi + 1);
-    if (f_hi != f_hi) f_hi = INFINITY;     // the bracket reaches the top of the finite floats
     const double dl = alpha * (double)f_lo - fabs(alpha * (double)f_lo) * 0x1p-40;
-    const double dh = alpha * (double)f_hi + fabs(alpha * (double)f_hi) * 0x1p-40;
-    float tl = (float)dl, th = (float)dh;
+    float tl = (float)dl;
     if ((double)tl > dl) tl = nextafterf(tl, -INFINITY);
-    if ((double)th < dh) th = nextafterf(th, INFINITY);
     const uint32_t span = k_hi - k_lo;
     const int bits = span ? 32 - __clz((int)span) : 0;
     s.rank = rank;
     s.k_lo = k_lo;
     s.k_hi = k_hi;
     s.t_lo = tl;
-    s.t_hi = th;
     s.shift1 = bits > 11 ? bits - 11 : 0;
     s.phi_over = 0;
-    s.c1 = 0;
-    s.c2 = 0;
     s.n_cand = 0;
     s.ge_lo = 0;
-    s.ge_thi = 0;
-    s.e1 = 0;
-    s.e2 = 0;
+    s.sum_c = 0;
+    s.sum_c2 = 0;
     s.phi = 0.0;
     s.min2 = kNone;
     s.n_list = 0;
@@ -240,18 +246,16 @@ __global__ __launch_bounds__(kSampleThreads) void cv_sample_kernel(const float* 
 
 // ---------------------------------------------------------------------------
 // 2. The bracketing pass is the observation-matrix pass (score.h,
-//    kObsBracket): per column the entries at or above t_hi, the entries
-//    below the bracket, the bracket entries' first-digit histogram, and the
-//    entries of the union of bracket and Phi's range as (value, column) in
-//    one buffer per wave of each column block.
+//    kObsBracket): the entries at or above min(bracket bottom, t_lo) as
+//    (value, column), in one buffer per wave of each column block.
 // ---------------------------------------------------------------------------
 
 constexpr int kCountRows = 16;    // rows per lane loaded together by the radix route's column walk
 
-// The radix route's column walk: ~2048 workgroups over all heads.
+// The radix route's column walk: ~1024 workgroups over all heads.
 int64_t col_blocks(int64_t n_keys, int hkv) {
   const int64_t blocks = (n_keys + 63) / 64;
-  const int64_t want = std::max<int64_t>(256, 2048 / std::max(1, hkv));
+  const int64_t want = std::max<int64_t>(128, 1024 / std::max(1, hkv));
   return std::max<int64_t>(1, std::min(blocks, want));
 }
 
@@ -279,68 +283,75 @@ __device__ __forceinline__ void flush_hist(const uint32_t* s_h, uint32_t* __rest
     if (s_h[i]) atomicAdd(&g[i], s_h[i]);
 }
 
+// nb (<= 64) consecutive pair buffers starting at buffer `first`, seen as
+// one index space: s_pre[w] = pairs before buffer w (filled by the first
+// wave, all fills loaded at once); returns the total.  Item k lies in the
+// last buffer w with s_pre[w] <= k.
+__device__ uint32_t buffer_prefix(const uint32_t* __restrict__ pfill, size_t first, int nb, uint32_t* s_pre) {
+  const int t = threadIdx.x;
+  if (t < 64) {
+    const uint32_t f = t < nb ? pfill[first + t] : 0u;
+    uint32_t x = f;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const uint32_t y = __shfl_up(x, off);
+      if (t >= off) x += y;
+    }
+    if (t < nb) s_pre[t] = x - f;
+    if (t == nb - 1) s_pre[nb] = x;
+  }
+  __syncthreads();
+  return s_pre[nb];
+}
+__device__ __forceinline__ const uint2* buffer_item(const uint2* __restrict__ pairs, size_t first, int nb,
+                                                    uint32_t capw, const uint32_t* s_pre, uint32_t k) {
+  int w = 0;
+  while (w + 1 < nb && s_pre[w + 1] <= k) ++w;
+  return pairs + (first + w) * capw + (k - s_pre[w]);
+}
+
 // Pairs of column block b (its waves' buffers): the bracket entries are
 // counted and histogrammed by their first digit, and the pairs at or above
-// the bracket's bottom and at or above t_hi counted (the entries below the
-// bracket follow, cv_below); sum c and sum c^2 over the block's columns.
+// the bracket's bottom counted (the entries below the bracket follow,
+// cv_below).
 __global__ __launch_bounds__(256) void cv_pairs_kernel(CvState* st, uint32_t* __restrict__ hist0,
                                                        const uint2* __restrict__ pairs,
                                                        const uint32_t* __restrict__ pfill, uint32_t capw, int nsub,
-                                                       int n_colblk, const uint32_t* __restrict__ colcnt,
-                                                       int64_t n_keys, int64_t cb_tokens) {
+                                                       int n_colblk) {
   __shared__ uint32_t s_h[kBins];
-  __shared__ unsigned long long s_red[4];
+  __shared__ unsigned long long s_red5[2][4];
+  __shared__ uint32_t s_pre[kCvMaxSub + 1];
   const int h = blockIdx.y, b = blockIdx.x;
   const int t = threadIdx.x;
   CvState& S = st[h];
   for (int i = t; i < kBins; i += 256) s_h[i] = 0;
   const uint32_t k_lo = S.k_lo, span = S.k_hi - S.k_lo;
   const int sh1 = S.shift1;
-  const float f_lo = key_to_float(k_lo), t_hi = S.t_hi;
+  const float f_lo = key_to_float(k_lo);
   __syncthreads();
-  uint32_t n_in = 0, n_lo = 0, n_thi = 0;
-  for (int w = 0; w < nsub; ++w) {
-    const size_t wr = ((size_t)h * n_colblk + b) * nsub + w;
-    const uint2* ph = pairs + wr * capw;
-    const uint32_t fill = pfill[wr];
-    for (uint32_t i0 = 0; i0 < fill; i0 += 4 * 256) {   // the same trip count on every lane
-      uint32_t x[4];
+  uint32_t n_in = 0, n_lo = 0;
+  const size_t first = ((size_t)h * n_colblk + b) * nsub;
+  const uint32_t total = buffer_prefix(pfill, first, nsub, s_pre);
+  for (uint32_t i0 = 0; i0 < total; i0 += 4 * 256) {   // the same trip count on every lane
+    uint32_t x[4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) x[u] = ph[min(i0 + u * 256 + t, fill - 1)].x;   // every load issued, then used
+    for (int u = 0; u < 4; ++u)   // every load issued (clamped), then used
+      x[u] = buffer_item(pairs, first, nsub, capw, s_pre, min(i0 + u * 256 + t, total - 1))->x;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const bool ok = i0 + u * 256 + t < fill;
-        const float v = __uint_as_float(x[u]);
-        const uint32_t o = (x[u] | 0x80000000u) - k_lo;
-        const bool in = ok && o <= span;
-        n_in += in;
-        n_lo += ok && v >= f_lo;
-        n_thi += ok && v >= t_hi;
-        hist_add(s_h, in, o >> sh1);
-      }
+    for (int u = 0; u < 4; ++u) {
+      const bool ok = i0 + u * 256 + t < total;
+      const uint32_t o = (x[u] | 0x80000000u) - k_lo;
+      const bool in = ok && o <= span;
+      n_in += in;
+      n_lo += ok && __uint_as_float(x[u]) >= f_lo;
+      hist_add(s_h, in, o >> sh1);
     }
   }
-  // sum c and sum c^2 over the block's columns
-  unsigned long long c1 = 0, c2 = 0;
-  const int64_t j0 = (int64_t)b * cb_tokens, j1 = j0 + cb_tokens < n_keys ? j0 + cb_tokens : n_keys;
-  for (int64_t j = j0 + t; j < j1; j += 256) {
-    const unsigned long long c = colcnt[(size_t)h * n_keys + j];
-    c1 += c;
-    c2 += c * c;
-  }
-  const unsigned long long a_in = block_sum256(n_in, s_red);
-  const unsigned long long a_lo = block_sum256(n_lo, s_red);
-  const unsigned long long a_thi = block_sum256(n_thi, s_red);
-  const unsigned long long a_c1 = block_sum256(c1, s_red);
-  const unsigned long long a_c2 = block_sum256(c2, s_red);
+  unsigned long long v[2] = {n_in, n_lo};
+  block_sums256(v, s_red5);
   if (t == 0) {
-    if (a_in) atomicAdd(&S.n_cand, a_in);
-    if (a_lo) atomicAdd(&S.ge_lo, a_lo);
-    if (a_thi) atomicAdd(&S.ge_thi, a_thi);
-    if (a_c1) {
-      atomicAdd(&S.c1, a_c1);
-      atomicAdd(&S.c2, a_c2);
-    }
+    if (v[0]) atomicAdd(&S.n_cand, v[0]);
+    if (v[1]) atomicAdd(&S.ge_lo, v[1]);
   }
   flush_hist(s_h, hist0 + (size_t)h * kBins);
 }
@@ -503,6 +514,7 @@ __global__ __launch_bounds__(256) void cv_list_kernel(const float* __restrict__ 
   __shared__ uint32_t s_nl, s_lbase;
   __shared__ uint32_t s_x[4];
   __shared__ int s_last;
+  __shared__ uint32_t s_pre[kRegions + 1];
   const int h = blockIdx.y;
   const int t = threadIdx.x, lane = t & 63;
   CvState& S = st[h];
@@ -545,35 +557,32 @@ __global__ __launch_bounds__(256) void cv_list_kernel(const float* __restrict__ 
       if (t == 0) s_nl = 0;
       __syncthreads();
     };
-    const int r0 = blockIdx.x * kRegions, r1 = min(cb, r0 + kRegions);
-    for (int r = r0; r < r1; ++r) {
-      const size_t wr = (size_t)h * cb + r;
-      const uint2* ph = pairs + wr * capw;
-      const uint32_t fill = pfill[wr];
-      for (uint32_t i0 = 0; i0 < fill; i0 += 4 * 256) {   // the same trip count on every lane
-        uint32_t o[4];
+    const int r0 = blockIdx.x * kRegions, nb = min(cb, r0 + kRegions) - r0;
+    const size_t first = (size_t)h * cb + r0;
+    const uint32_t total = buffer_prefix(pfill, first, nb, s_pre);
+    for (uint32_t i0 = 0; i0 < total; i0 += 4 * 256) {   // the same trip count on every lane
+      uint32_t o[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {   // every load issued (clamped), then used
-          const uint32_t i = i0 + u * 256 + t;
-          const uint32_t x = ph[min(i, fill - 1)].x;
-          o[u] = i < fill ? (x | 0x80000000u) - k_lo : kNone;
-        }
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const bool ok = o[u] <= span;
-          const bool in = ok && (o[u] >> sh1) == b1;
-          if (ok && (o[u] >> sh1) > b1) mn = min(mn, o[u]);
-          const uint64_t bal = __builtin_amdgcn_ballot_w64(in);
-          if (bal) {
-            uint32_t base = 0;
-            if (lane == 0) base = atomicAdd(&s_nl, (uint32_t)__builtin_popcountll(bal));
-            base = __shfl(base, 0) + mbcnt(bal);
-            if (in) s_stage[base] = o[u];
-          }
-        }
-        __syncthreads();
-        if (s_nl > (uint32_t)(kListStage - 4 * 256)) out();   // room for the next round
+      for (int u = 0; u < 4; ++u) {   // every load issued (clamped), then used
+        const uint32_t i = i0 + u * 256 + t;
+        const uint32_t x = buffer_item(pairs, first, nb, capw, s_pre, min(i, total - 1))->x;
+        o[u] = i < total ? (x | 0x80000000u) - k_lo : kNone;
       }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const bool ok = o[u] <= span;
+        const bool in = ok && (o[u] >> sh1) == b1;
+        if (ok && (o[u] >> sh1) > b1) mn = min(mn, o[u]);
+        const uint64_t bal = __builtin_amdgcn_ballot_w64(in);
+        if (bal) {
+          uint32_t base = 0;
+          if (lane == 0) base = atomicAdd(&s_nl, (uint32_t)__builtin_popcountll(bal));
+          base = __shfl(base, 0) + mbcnt(bal);
+          if (in) s_stage[base] = o[u];
+        }
+      }
+      __syncthreads();
+      if (s_nl > (uint32_t)(kListStage - 4 * 256)) out();   // room for the next round
     }
     out();
     for (int off = 32; off > 0; off >>= 1) mn = min(mn, (uint32_t)__shfl_xor((int)mn, off));
@@ -594,9 +603,9 @@ __global__ __launch_bounds__(256) void cv_list_kernel(const float* __restrict__ 
 }
 
 // ---------------------------------------------------------------------------
-// 4. Bracket route: each workgroup of the column walk adds its own gathered
-//    values in [Phi, t_hi) to its columns (LDS counts) and the change to the
-//    sums of C_j and C_j^2.  Radix route: the second key digit over A.
+// 4. Bracket route: each column block counts its gathered values at or
+//    above Phi per column (LDS counters): C_j, and the sums of C_j and
+//    C_j^2.  Radix route: the second key digit over A.
 // ---------------------------------------------------------------------------
 
 constexpr int kColWin = 8192;      // columns counted in LDS at a time
@@ -606,8 +615,9 @@ __global__ __launch_bounds__(256) void cv_columns_kernel(const float* __restrict
                                                          uint32_t* __restrict__ hist2, const uint2* __restrict__ pairs,
                                                          const uint32_t* __restrict__ pfill, uint32_t capw, int nsub,
                                                          int n_colblk, int64_t cb_tokens,
-                                                         const uint32_t* __restrict__ colcnt, int64_t n_keys) {
+                                                         int64_t n_keys) {
   __shared__ uint32_t s_e[kColWin];
+  __shared__ uint32_t s_pre[kCvMaxSub + 1];
   __shared__ int64_t s_tot[4];
   __shared__ uint32_t s_bin[3];
   __shared__ int64_t s_pos[2];
@@ -633,51 +643,44 @@ __global__ __launch_bounds__(256) void cv_columns_kernel(const float* __restrict
     flush_hist(s_h, hist2 + (size_t)h * kBins);
     return;
   }
-  // column block b's gathered values in [Phi, t_hi), counted per column in
-  // LDS, kColWin columns at a time
+  // C_j of column block b's columns: its gathered values at or above Phi
+  // (every entry there is one), counted per column in LDS, kColWin columns
+  // at a time
   const double phi = S.phi;
-  const float t_hi = S.t_hi;
   const int b = blockIdx.x;
-  const int64_t c0 = (int64_t)b * cb_tokens, c1 = std::min(c0 + cb_tokens, n_keys);
-  const uint32_t* cc = colcnt + (size_t)h * n_keys;
+  const int64_t c0 = (int64_t)b * cb_tokens, c1 = c0 + cb_tokens < n_keys ? c0 + cb_tokens : n_keys;
+  const size_t first = ((size_t)h * n_colblk + b) * nsub;
+  const uint32_t total = buffer_prefix(pfill, first, nsub, s_pre);
   unsigned long long a1 = 0, a2 = 0;
   for (int64_t w0 = c0; w0 < c1; w0 += kColWin) {
     const int nw = (int)std::min<int64_t>(kColWin, c1 - w0);
     __syncthreads();
     for (int i = t; i < nw; i += 256) s_e[i] = 0;
     __syncthreads();
-    for (int w = 0; w < nsub; ++w) {
-      const size_t wr = ((size_t)h * n_colblk + b) * nsub + w;
-      const uint2* ph = pairs + wr * capw;
-      const uint32_t fill = pfill[wr];
-      for (uint32_t i0 = 0; i0 < fill; i0 += 4 * 256) {
-        uint2 e[4];
+    for (uint32_t i0 = 0; i0 < total; i0 += 4 * 256) {
+      uint2 e[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) e[u] = ph[min(i0 + u * 256 + t, fill - 1)];   // every load issued, then used
+      for (int u = 0; u < 4; ++u)   // every load issued (clamped), then used
+        e[u] = *buffer_item(pairs, first, nsub, capw, s_pre, min(i0 + u * 256 + t, total - 1));
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const float x = __uint_as_float(e[u].x);
-          const int64_t rel = (int64_t)e[u].y - w0;
-          if (i0 + u * 256 + t < fill && rel >= 0 && rel < nw && x < t_hi && (double)x >= phi)
-            atomicAdd(&s_e[rel], 1u);   // entries >= t_hi are in C already
-        }
+      for (int u = 0; u < 4; ++u) {
+        const float x = __uint_as_float(e[u].x);
+        const int64_t rel = (int64_t)e[u].y - w0;
+        if (i0 + u * 256 + t < total && rel >= 0 && rel < nw && (double)x >= phi) atomicAdd(&s_e[rel], 1u);
       }
     }
     __syncthreads();
     for (int l = t; l < nw; l += 256) {
-      const unsigned long long e = s_e[l];
-      if (e) {
-        const unsigned long long c = cc[w0 + l];
-        a1 += e;
-        a2 += 2 * c * e + e * e;       // (c + e)^2 - c^2
-      }
+      const unsigned long long c = s_e[l];
+      a1 += c;
+      a2 += c * c;
     }
   }
   const unsigned long long t1 = block_sum256(a1, s_red);
   const unsigned long long t2 = block_sum256(a2, s_red);
   if (t == 0 && t1) {
-    atomicAdd(&S.e1, t1);
-    atomicAdd(&S.e2, t2);
+    atomicAdd(&S.sum_c, t1);
+    atomicAdd(&S.sum_c2, t2);
   }
 }
 
@@ -699,7 +702,7 @@ __global__ __launch_bounds__(256) void cv_digit2_kernel(const float* __restrict_
   const int h = blockIdx.y;
   CvState& S = st[h];
   if (bracket_route(S, N)) {  // the bracket route's score, from the previous launch's sums
-    if (blockIdx.x == 0 && threadIdx.x == 0) cv_out[h] = cv_value(S.c1 + S.e1, S.c2 + S.e2, n_keys);
+    if (blockIdx.x == 0 && threadIdx.x == 0) cv_out[h] = cv_value(S.sum_c, S.sum_c2, n_keys);
     return;
   }
   const int64_t rem0 = S.fb_rem[0];
@@ -795,7 +798,7 @@ uint32_t pair_cap(int64_t N, int64_t nbuf) {
 }
 
 struct CvLayout {
-  size_t hist, list, samples, pairs, pfill, colcnt, state, total;
+  size_t hist, list, samples, pairs, pfill, state, total;
 };
 size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
 CvLayout cv_layout(int hkv, int lq, int64_t n_keys, int n_colblk) {
@@ -808,7 +811,6 @@ CvLayout cv_layout(int hkv, int lq, int64_t n_keys, int n_colblk) {
   L.samples = o; o += al256((size_t)hkv * kCvSamples * sizeof(float));
   L.pairs = o; o += al256((size_t)hkv * nbuf * pair_cap(N, nbuf) * sizeof(uint2));
   L.pfill = o; o += al256((size_t)hkv * nbuf * sizeof(uint32_t));
-  L.colcnt = o; o += al256((size_t)hkv * n_keys * sizeof(uint32_t));
   L.state = o; o += al256((size_t)hkv * sizeof(CvState));
   L.total = o;
   return L;
@@ -833,7 +835,6 @@ CvLink cv_link(void* ws, int hkv, int lq, int64_t n_keys, int n_colblk, int nsub
   c.pfill = reinterpret_cast<uint32_t*>(w + L.pfill);
   c.capw = pair_cap((int64_t)lq * n_keys, (int64_t)n_colblk * kCvMaxSub);
   c.nsub = nsub;
-  c.colcnt = reinterpret_cast<uint32_t*>(w + L.colcnt);
   return c;
 }
 
@@ -846,7 +847,7 @@ hipError_t launch_cv_sample(const ScoreArgs& a, double k_pct, double alpha, hipS
 
 hipError_t launch_cv_pairs(const ScoreArgs& a, hipStream_t stream) {
   hipLaunchKernelGGL(cv_pairs_kernel, dim3((unsigned)a.n_colblk, a.hkv), dim3(256), 0, stream, a.cv.st, a.cv.hist,
-                     a.cv.pairs, a.cv.pfill, a.cv.capw, a.cv.nsub, a.n_colblk, a.cv.colcnt, a.n_keys, a.cb_tokens);
+                     a.cv.pairs, a.cv.pfill, a.cv.capw, a.cv.nsub, a.n_colblk);
   return hipGetLastError();
 }
 
@@ -858,14 +859,15 @@ hipError_t launch_cv_finish(const ScoreArgs& a, double k_pct, double alpha, floa
   uint32_t* hist = c.hist;
   const float* A = a.obs;
   const int nbuf = a.n_colblk * c.nsub;
-  // radix-route passes over A in entry order: enough workgroups per head to fill the device
-  const unsigned hb = (unsigned)std::max<int64_t>(1, std::min<int64_t>(512, (N + 1023) / 1024));
+  // radix-route passes over A: 128 workgroups per head (launches that only
+  // return on the bracket route stay short)
+  const unsigned hb = (unsigned)std::max<int64_t>(1, std::min<int64_t>(128, (N + 1023) / 1024));
   const unsigned lw = (unsigned)std::max<int64_t>(hb, (nbuf + kRegions - 1) / kRegions);
   const dim3 walk((unsigned)col_blocks(n_keys, hkv), hkv), flat(hb, hkv);
   hipLaunchKernelGGL(cv_list_kernel, dim3(lw, hkv), dim3(256), 0, stream, A, N, c.st, hist, hist + hs, c.pairs,
                      c.pfill, c.capw, nbuf, c.list, k_pct, alpha);
   hipLaunchKernelGGL(cv_columns_kernel, dim3((unsigned)a.n_colblk, hkv), dim3(256), 0, stream, A, N, c.st, hist + hs,
-                     hist + 2 * hs, c.pairs, c.pfill, c.capw, c.nsub, a.n_colblk, a.cb_tokens, c.colcnt, n_keys);
+                     hist + 2 * hs, c.pairs, c.pfill, c.capw, c.nsub, a.n_colblk, a.cb_tokens, n_keys);
   hipLaunchKernelGGL(cv_digit2_kernel, flat, dim3(256), 0, stream, A, N, c.st, hist + 2 * hs, hist + 3 * hs, n_keys,
                      cv_out);
   hipLaunchKernelGGL(cv_count_kernel, walk, dim3(256), 0, stream, A, lq, n_keys, c.st, hist + 3 * hs, k_pct, alpha,

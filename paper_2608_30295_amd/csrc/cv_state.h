@@ -34,14 +34,12 @@ __device__ __forceinline__ float cv_key_float(uint32_t key) {
 struct CvState {                   // per KV head, in the workspace
   int64_t rank;                    // lo = floor((N - 1) k), 0-based
   uint32_t k_lo, k_hi;             // the bracket: ordered keys [k_lo, k_hi]
-  float t_lo, t_hi;                // Phi lies in [t_lo, t_hi)
+  float t_lo;                      // Phi >= t_lo (a float)
   int shift1;                      // (key - k_lo) >> shift1: first digit over the bracket
   uint32_t phi_over;               // a wave's gathered pairs overflowed its buffer
-  unsigned long long c1, c2;       // sums of c_j and c_j^2, c_j = #{i : A[i][j] >= t_hi}
   unsigned long long n_cand;       // entries inside the bracket (from the pairs)
-  unsigned long long ge_lo;        // pairs at or above the bracket's bottom
-  unsigned long long ge_thi;       // pairs at or above t_hi
-  unsigned long long e1, e2;       // bracket route: changes of sum C and sum C^2 by the pairs in [Phi, t_hi)
+  unsigned long long ge_lo;        // entries at or above the bracket's bottom (all are pairs)
+  unsigned long long sum_c, sum_c2;  // bracket route: sums of C_j and C_j^2 (from the pairs)
   double phi;
   uint32_t min2;                   // bracket route: smallest key offset above x_(lo)'s first-digit bin
   uint32_t n_list;                 // bracket route: entries of x_(lo)'s first-digit bin
@@ -61,11 +59,9 @@ __device__ __forceinline__ float cv_bracket_top(uint32_t k_hi) {
 }
 
 // Entries below the bracket: N less those at or above its bottom, which are
-// the pairs there plus the entries at or above the union's top (the entries
-// at or above t_hi less the pairs there).  Valid for a head whose pairs all
-// fit their buffers.
+// all among the pairs (valid for a head whose pairs all fit their buffers).
 __device__ __forceinline__ unsigned long long cv_below(const CvState& S, int64_t N) {
-  return (unsigned long long)N - S.ge_lo - S.c1 + S.ge_thi;
+  return (unsigned long long)N - S.ge_lo;
 }
 
 // The head takes the bracket route when every gathered pair fit its buffer
@@ -80,8 +76,8 @@ __device__ __forceinline__ bool cv_bracket_route(const CvState& S, int64_t N) {
 }
 
 // What the observation-matrix pass exchanges with the CV kernels.  Pairs
-// (value bits, key column) of the entries inside the union of the bracket
-// and Phi's range go to wave w of column block b's own buffer,
+// (value bits, key column) of the entries at or above the lower of the
+// bracket's bottom and t_lo go to wave w of column block b's own buffer,
 // pairs + ((h * n_colblk + b) * nsub + w) * capw, its fill to
 // pfill[(h * n_colblk + b) * nsub + w].
 struct CvLink {
@@ -92,7 +88,6 @@ struct CvLink {
   uint32_t* pfill;
   uint32_t capw;                   // pairs per wave buffer
   int nsub;                        // waves per column block (buffers per block)
-  uint32_t* colcnt;                // [hkv][n_keys] entries >= t_hi per column
   uint32_t* hist;                  // [4][hkv][kCvBins]: hist0, then the radix route's three digits
   uint32_t* list;                  // [hkv][kCvListCap] bracket entries of x_(lo)'s first-digit bin
 };

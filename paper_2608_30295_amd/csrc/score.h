@@ -104,10 +104,10 @@ struct ScoreArgs {
   int cs_fused;           // chunk size when it divides the 64-column tile, else 0
   int64_t n_chunks;
   float* obs;             // kObsMatrix out: [n_sel][lq][n_keys]
-  // kObsBracket: A's values classified against the CV bracket instead of
-  // stored (inside the union of bracket and Phi's range, at or above t_hi
-  // per column); kObsMatrix with cv_gate set skips the heads whose bracket
-  // took them (only the radix route reads A)
+  // kObsBracket: A's values at or above the CV bracket's lower end written
+  // out with their columns instead of every value stored; kObsMatrix with
+  // cv_gate set skips the heads whose bracket took them (only the radix
+  // route reads A)
   CvLink cv;
   int cv_gate;
 };
@@ -130,7 +130,7 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
   // s_waitcnt immediate: vmcnt <= NSTAGE * (NRING - 2), expcnt not waited on;
   // lgkmcnt(0) in column-mass mode, whose column partials in LDS the barrier publishes
   constexpr int VM = NSTAGE * (NRING - 2);
-  constexpr int LGKM = MODE == kColMass || OBSB ? 0 : 0xF;
+  constexpr int LGKM = MODE == kColMass ? 0 : 0xF;
   constexpr int kWaitRing = (VM & 0xF) | ((VM >> 4) << 14) | (0x7 << 4) | (LGKM << 8);
   // one LDS array per ring stage: stages chosen at compile time do not alias,
   // so the compiler adds no waits of its own between the loads and the reads
@@ -178,23 +178,20 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
       if (MODE != kRowStats) off[mt][r] = a.rowoff[(size_t)sel * RPAD + row_of(mt, r)];
     }
 
-  // kObsBracket: t_hi and the union of the bracket and Phi's range; this
-  // wave's pair buffer (fill: wave-uniform)
+  // kObsBracket: the entries at or above u_lo (the lower of the bracket's
+  // bottom and Phi's range's) go to this wave's pair buffer (fill:
+  // wave-uniform); they are all the entries at or above Phi
   uint32_t wfill = 0;
-  float bt_hi = 0.f, bu_lo = 0.f, bu_hi = 0.f;
+  float bu_lo = 0.f;
   uint2* wpairs = nullptr;
   if (OBSB) {
     const CvState& B = a.cv.st[sel];
-    bt_hi = B.t_hi;
     bu_lo = fminf(cv_key_float(B.k_lo), B.t_lo);
-    bu_hi = fmaxf(cv_bracket_top(B.k_hi), bt_hi);
     wpairs = a.cv.pairs + (((size_t)sel * a.n_colblk + cb) * a.cv.nsub + wave) * a.cv.capw;
   }
-  // one A value of this lane (key column col; ok: a real entry): counted for
-  // its column at or above t_hi, written out inside the union
-  auto classify = [&](float v, bool ok, uint32_t col, int t, uint32_t& cnt) {
-    cnt += (ok && v >= bt_hi) ? 1u << (8 * t) : 0u;   // four 8-bit counters (a lane adds at most MT NR per tile)
-    const bool in_u = ok && v >= bu_lo && v < bu_hi;
+  // one A value of this lane (key column col; ok: a real entry)
+  auto classify = [&](float v, bool ok, uint32_t col) {
+    const bool in_u = ok && v >= bu_lo;
     const uint64_t bal = __builtin_amdgcn_ballot_w64(in_u);
     if (bal) {
       const uint32_t at = wfill + (uint32_t)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
@@ -243,13 +240,6 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
   auto finish_cols = [&](int t) {
     const int p = t & 1;
     const int64_t col = col0 + (int64_t)t * kTileTok + lane;
-    if (OBSB) {                    // entries >= t_hi of the column (exact small integers in fp32)
-      float c = 0.f;
-#pragma unroll 1
-      for (int w = 0; w < W; ++w) c += s_col[p][w][lane];
-      if (col < col_end) a.cv.colcnt[(size_t)sel * a.n_keys + col] = (uint32_t)c;
-      return;
-    }
     float v = 0.f;
 #pragma unroll
     for (int w = 0; w < W; ++w) v += s_col[p][w][lane];
@@ -289,7 +279,6 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
     float cmass[kTileTok / TC];
 #pragma unroll
     for (int t = 0; t < kTileTok / TC; ++t) cmass[t] = -0.f;   // -0 + x folds to x
-    uint32_t ccount = 0;                                          // kObsBracket: per column position t, bits 8t..8t+7
     // the MFMA work of one half tile (32 columns: NCT column tiles); k-step
     // outer, row tile inner: a B fragment is live for MT MFMAs, and the MT
     // accumulator chains interleave
@@ -366,7 +355,7 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
 #pragma unroll
                 for (int r = 1; r < G; ++r) v += p[r0 + r];
                 const bool ok = i0 + r0 / G < a.lq && colok;
-                if (OBSB) classify(v * invG, ok, col32, hh * NCT + ct, ccount);
+                if (OBSB) classify(v * invG, ok, col32);
                 else if (ok) ob[(size_t)(r0 / G) * a.n_keys] = v * invG;
               }
             } else {  // G == 8: lanes l and l ^ kPair8 hold the two halves of each group of 8 rows
@@ -376,7 +365,7 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
                 const float v = S::kPair8 == 16 ? add_xor16(q4) : add_xor32(q4);
                 const int i = row_of(mt, b4) / 8;
                 const bool ok = (lane & S::kPair8) == 0 && i < a.lq && colok;
-                if (OBSB) classify(v * invG, ok, col32, hh * NCT + ct, ccount);
+                if (OBSB) classify(v * invG, ok, col32);
                 else if (ok) a.obs[((size_t)sel * a.lq + i) * a.n_keys + col] = v * invG;
               }
             }
@@ -394,11 +383,11 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
     mfma_half(1, acc1);
     valu_half(1, acc1, mask_tag);
 
-    if (MODE == kColMass || OBSB) {
+    if (MODE == kColMass) {
       // sum over the lanes holding each column; each wave leaves its partial in LDS
 #pragma unroll
       for (int t = 0; t < kTileTok / TC; ++t) {
-        const float v = S::col_sum(OBSB ? (float)((ccount >> (8 * t)) & 0xFFu) : cmass[t]);
+        const float v = S::col_sum(cmass[t]);
         if (lane < TC) s_col[tile & 1][wave][t * TC + lane] = v;
       }
     }
@@ -416,7 +405,7 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
     __builtin_amdgcn_s_barrier();
     compiler_fence();
     issue(ring((S + NRING - 1) % NRING), tile + NRING - 1);
-    if ((MODE == kColMass || OBSB) && tile > 0 && wave == ((tile - 1) & (W - 1))) finish_cols(tile - 1);
+    if (MODE == kColMass && tile > 0 && wave == ((tile - 1) & (W - 1))) finish_cols(tile - 1);
     body(ring(S), tile);
   };
   auto prime = [&]() {
@@ -481,7 +470,7 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
     run(std::integral_constant<int, 0>{}, RsSum{});
   }
 
-  if (MODE == kColMass || OBSB) {
+  if (MODE == kColMass) {
     barrier_lds_only();
     if (n_tiles > 0 && wave == ((n_tiles - 1) & (W - 1))) finish_cols(n_tiles - 1);
   }
