@@ -86,6 +86,11 @@ struct PlanLayout {
 
 size_t a256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// The worker-major segment table sits right after the segment list.
+size_t v2_items_off(size_t segs_off, int n_segments) {
+  return segs_off + a256((size_t)n_segments * sizeof(catekv::DecodeItem));
+}
+
 int device_cus() {
   int dev = 0, n_cu = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
@@ -148,6 +153,7 @@ PlanLayout plan_layout(const int64_t* max_len, int n_views, int G, int split, in
   const size_t sf = catekv::decode_slot_floats(G) * sizeof(float);
   size_t o = 0;
   P.segs_off = o; o += a256((size_t)P.n_segments * sizeof(catekv::DecodeItem));
+  o += a256((size_t)P.n_workers * catekv::kDecodeV2MaxSeg * sizeof(catekv::V2Item));   // v2_items_off()
   P.workers_off = o; o += a256((size_t)(P.n_workers + 1) * sizeof(int32_t));
   P.views_off = o; o += a256((size_t)n_views * sizeof(catekv::ViewInfo));
   P.slots_off = o; o += a256((size_t)std::max(P.n_slots, 1) * sf);
@@ -164,7 +170,8 @@ PlanLayout choose_plan(const int64_t* max_len, int n_views, int G, int split, in
   std::vector<int> per_worker(P.n_workers, 0);
   int most = 0;
   for (const Segment& sg : P.segs) most = std::max(most, ++per_worker[sg.worker]);
-  if (most <= catekv::kDecodeV2MaxSeg) {
+  const int least = *std::min_element(per_worker.begin(), per_worker.end());   // the stream kernel assumes >= 1
+  if (most <= catekv::kDecodeV2MaxSeg && least >= 1 && n_views < (1 << 24)) {   // view ids fit 24 bits
     *variant = catekv::kDecodeStreamV2;
     return P;
   }
@@ -428,11 +435,28 @@ int catekv_decode_plan(const int64_t* max_len_host, int batch, int hq, int hkv, 
     wseg[s.worker + 1] = i + 1;
   }
   for (int w = 1; w <= P.n_workers; ++w) wseg[w] = std::max(wseg[w], wseg[w - 1]);
+  std::vector<catekv::V2Item> v2((size_t)P.n_workers * catekv::kDecodeV2MaxSeg, catekv::V2Item{0, 0, 0, -1});
+  if (variant == catekv::kDecodeStreamV2) {
+    // every entry of a worker, padding included, carries the worker's segment count
+    for (int w = 0; w < P.n_workers; ++w) {
+      const int ns = wseg[w + 1] - wseg[w];   // in [1, kDecodeV2MaxSeg] for this variant
+      for (int j = 0; j < catekv::kDecodeV2MaxSeg; ++j) {
+        catekv::V2Item& e = v2[(size_t)w * catekv::kDecodeV2MaxSeg + j];
+        if (j < ns) {
+          const catekv::DecodeItem& it = segs[wseg[w] + j];
+          const catekv::ViewInfo& vi = views[it.bh];
+          e = catekv::V2Item{it.bh, it.t0, it.t1, vi.n_parts > 1 ? vi.first_slot + it.part : -1};
+        }
+        e.bh_n |= ns << 24;
+      }
+    }
+  }
 
   std::vector<unsigned char> host(P.slots_off, 0);
   std::memcpy(host.data() + P.segs_off, segs.data(), segs.size() * sizeof(catekv::DecodeItem));
   std::memcpy(host.data() + P.workers_off, wseg.data(), wseg.size() * sizeof(int32_t));
   std::memcpy(host.data() + P.views_off, views.data(), views.size() * sizeof(catekv::ViewInfo));
+  std::memcpy(host.data() + v2_items_off(P.segs_off, P.n_segments), v2.data(), v2.size() * sizeof(catekv::V2Item));
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   hipError_t e = hipMemcpyAsync(ws, host.data(), host.size(), hipMemcpyHostToDevice, s);
   if (e != hipSuccess) return hip_fail(e, "decode_plan upload");
@@ -481,6 +505,7 @@ int catekv_decode_attn(int dtype, const catekv_decode_plan_t* plan, const void* 
   a.lens = lens;
   a.items = reinterpret_cast<const catekv::DecodeItem*>(w + plan->segs_off);
   a.worker_seg = reinterpret_cast<const int32_t*>(w + plan->workers_off);
+  a.v2items = reinterpret_cast<const catekv::V2Item*>(w + v2_items_off(plan->segs_off, plan->n_segments));
   a.views = reinterpret_cast<const catekv::ViewInfo*>(w + plan->views_off);
   a.slots = reinterpret_cast<float*>(w + plan->slots_off);
   a.n_workers = plan->n_workers;

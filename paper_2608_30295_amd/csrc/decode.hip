@@ -543,8 +543,13 @@ constexpr int kV2MaxSeg = kDecodeV2MaxSeg;   // segments per worker held in the 
 struct V2Seg {
   const char* k;
   const char* v;
-  int32_t t0, t_end, n_units, row0, slot, n_parts;
+  int32_t t0, t_end, n_units, row0, slot;
 };
+
+// Views whose K/V pointers and lengths every workgroup reads into LDS at the
+// start, side by side with its own segment list (larger batches read them
+// per segment, one load later).
+constexpr int kV2PreViews = 256;
 
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
@@ -575,18 +580,35 @@ void decode_stream_v2_kernel(DecodeArgs a) {
   __shared__ uint4 s_q[kV2MaxSeg][G][16];       // per segment: G query rows of 16 x 16 bytes
   __shared__ float s_o[2][WAVES][G][kD];
   __shared__ float s_ml[2][WAVES][2][G];
+  __shared__ catekv_kv_ptrs s_kv[kV2PreViews];
+  __shared__ int64_t s_len[kV2PreViews];
 
-  const int seg_lo = a.worker_seg[blockIdx.x];
-  const int nseg = a.worker_seg[blockIdx.x + 1] - seg_lo;   // the plan keeps it <= kV2MaxSeg
-
+  // Start-up: the segment list with the worker's segment count and (small
+  // batches) every view's pointers and length are independent loads, all
+  // issued before the first wait; the query rows follow one load later.
+  const int nv = a.n_views;
+  const bool pre = nv <= kV2PreViews;
+  const V2Item it = a.v2items[(size_t)blockIdx.x * kV2MaxSeg +
+                              ((int)threadIdx.x < kV2MaxSeg ? (int)threadIdx.x : kV2MaxSeg - 1)];
+  if (pre) {
+    const int tv = (int)threadIdx.x < nv ? (int)threadIdx.x : nv - 1;
+    const catekv_kv_ptrs pv = a.kv[tv];
+    const int64_t pl = a.lens[tv];
+    if ((int)threadIdx.x < nv) {
+      s_kv[threadIdx.x] = pv;
+      s_len[threadIdx.x] = pl;
+    }
+  }
+  __syncthreads();
+  // every entry carries the segment count, which the plan keeps in [1, kV2MaxSeg]
+  const int nseg = __builtin_amdgcn_readfirstlane((uint32_t)it.bh_n >> 24);
   if ((int)threadIdx.x < nseg) {
-    const DecodeItem it = a.items[seg_lo + threadIdx.x];
-    const catekv_kv_ptrs view = a.kv[it.bh];
-    int64_t len = a.lens[it.bh];
-    const ViewInfo vi = a.views[it.bh];
+    const int bh = it.bh_n & 0xFFFFFF;
+    const catekv_kv_ptrs view = pre ? s_kv[bh] : a.kv[bh];
+    int64_t len = pre ? s_len[bh] : a.lens[bh];
     len = len < 0 ? 0 : len;
     const int t_end = (int)((int64_t)it.t1 < len ? (int64_t)it.t1 : len);
-    const int b = it.bh / hkv, h = it.bh - b * hkv;
+    const int b = bh / hkv, h = bh - b * hkv;
     V2Seg sg;
     sg.k = reinterpret_cast<const char*>(view.k);
     sg.v = reinterpret_cast<const char*>(view.v);
@@ -594,17 +616,8 @@ void decode_stream_v2_kernel(DecodeArgs a) {
     sg.t_end = t_end;
     sg.n_units = t_end > it.t0 ? (t_end - it.t0 + 15) / 16 : 0;
     sg.row0 = b * hq + h * G;
-    sg.slot = vi.first_slot + it.part;
-    sg.n_parts = vi.n_parts;
+    sg.slot = it.slot;
     s_seg[threadIdx.x] = sg;
-  }
-  for (int t = threadIdx.x; t < nseg * G * 16; t += NT) {
-    const int sgi = t / (G * 16), r = t - sgi * (G * 16);
-    const int g = r >> 4, piece = r & 15;
-    const int bh = a.items[seg_lo + sgi].bh;
-    const int b = bh / hkv, h = bh - b * hkv;
-    s_q[sgi][g][piece] = ldg16(reinterpret_cast<const char*>(a.q) +
-                               ((size_t)b * hq + (size_t)h * G + g) * (kD * 2) + piece * 16);
   }
   __syncthreads();
 
@@ -703,7 +716,7 @@ void decode_stream_v2_kernel(DecodeArgs a) {
         Ov += s_o[buf][w][g][e] * cw;
       }
       const float Mn = M * scale;                 // natural-log units of the scaled score
-      if (sg.n_parts == 1) emit(a.out, a.lse, (size_t)sg.row0 + g, e, Mn, L, Ov);
+      if (sg.slot < 0) emit(a.out, a.lse, (size_t)sg.row0 + g, e, Mn, L, Ov);
       else put_slot<G>(a.slots + (size_t)sg.slot * SF, g, e, Mn, L, Ov);
     }
   };
@@ -775,6 +788,30 @@ void decode_stream_v2_kernel(DecodeArgs a) {
       O[2 * i + 1] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(A_lo, Bo, O[2 * i + 1], 0, 0, 0);
     }
   };
+
+  // the query rows of every segment to LDS (clamped: every thread loads and
+  // stores; a clamped thread writes the last piece again, the same value)
+  constexpr int QP = (kV2MaxSeg * G * 16 + NT - 1) / NT;
+  const int nq = nseg * G * 16;                  // > 0: a worker has at least one segment
+  {
+    uint4 qv[QP];
+#pragma unroll
+    for (int p = 0; p < QP; ++p) {
+      int t = threadIdx.x + p * NT;
+      t = t < nq ? t : nq - 1;
+      const int sgi = t / (G * 16), r = t - sgi * (G * 16);
+      qv[p] = ldg16(reinterpret_cast<const char*>(a.q) + ((size_t)s_seg[sgi].row0 + (r >> 4)) * (kD * 2) +
+                    (r & 15) * 16);
+    }
+#pragma unroll
+    for (int p = 0; p < QP; ++p) {
+      int t = threadIdx.x + p * NT;
+      t = t < nq ? t : nq - 1;
+      const int sgi = t / (G * 16), r = t - sgi * (G * 16);
+      s_q[sgi][r >> 4][r & 15] = qv[p];
+    }
+  }
+  __syncthreads();
 
   if (is < nseg) {
     issue(0);

@@ -32,6 +32,16 @@ constexpr int kDecodeStreamV2 = 2;   // one 8-wave workgroup per compute unit (b
                                      // segments per workgroup
 constexpr int kDecodeV2MaxSeg = 16;
 
+// A segment of a one-workgroup-per-CU plan (kDecodeStreamV2) as the stream
+// kernel reads it: the plan also writes them worker-major, kDecodeV2MaxSeg
+// entries per worker, so that a workgroup finds its segments with one load.
+struct V2Item {
+  int32_t bh_n;           // view bh (low 24 bits) and the worker's segment count (high 8 bits)
+  int32_t t0;
+  int32_t t1;
+  int32_t slot;           // partial slot, or -1 when the segment covers its whole view
+};
+
 // Per view: where its partial slots live and how many segments cover it.
 struct ViewInfo {
   int32_t first_slot;     // slot of part 0
@@ -48,6 +58,7 @@ struct DecodeArgs {
   const int64_t* lens;
   const DecodeItem* items;      // segments, grouped by worker
   const int32_t* worker_seg;    // [n_workers + 1] first segment of each worker
+  const V2Item* v2items;        // kDecodeStreamV2: [n_workers][kDecodeV2MaxSeg]
   const ViewInfo* views;
   float* slots;                 // partial slots
   int n_workers, n_views, n_multi, hkv;
