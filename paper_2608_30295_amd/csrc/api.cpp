@@ -559,8 +559,10 @@ int catekv_retrieve_pages(int dtype, const void* q, const void* kmin, const void
   if (rc) return rc;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   float* scores = reinterpret_cast<float*>(ws);
-  hipError_t e = catekv::launch_page_scores(dtype, hq / hkv, q, kmin, kmax, n_pages, heads_host, n_sel, scores, s);
   char* topk_ws = reinterpret_cast<char*>(ws) + a256((size_t)n_sel * (size_t)n_pages * sizeof(float));
+  // the page-score launch clears the top-k's arrival counters (its first n_sel words)
+  hipError_t e = catekv::launch_page_scores(dtype, hq / hkv, q, kmin, kmax, n_pages, heads_host, n_sel, scores,
+                                            reinterpret_cast<uint32_t*>(topk_ws), n_sel, s);
   if (e == hipSuccess) e = catekv::launch_topk(scores, n_sel, n_pages, n_keep, idx_out, topk_ws, s);
   if (e != hipSuccess) return hip_fail(e, "retrieve_pages launch");
   return ok();

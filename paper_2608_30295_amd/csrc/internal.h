@@ -124,7 +124,9 @@ hipError_t launch_compact(int dtype, const void* k, const void* v, int hkv, int6
 
 // Indices of the min(b, n) largest of each row of S [n_rows][n] (ties to the
 // lower index), ascending, -1 padded to b.  ws: topk_workspace_bytes() bytes
-// (rows longer than 32768 scores are reduced slice by slice through it).
+// (rows longer than 4096 scores are reduced slice by slice through it); its
+// first n_rows 32-bit words must be zero on entry (an earlier launch of the
+// same call clears them) and are left zero.
 size_t topk_workspace_bytes(int n_rows, int64_t n);
 hipError_t launch_topk(const float* S, int n_rows, int64_t n, int b, int32_t* idx_out, void* ws,
                        hipStream_t stream);
@@ -134,7 +136,7 @@ hipError_t launch_page_bounds(int dtype, const void* k, int64_t n, int cs, const
                               void* kmin, void* kmax, hipStream_t stream);
 hipError_t launch_page_scores(int dtype, int G, const void* q, const void* kmin, const void* kmax,
                               int64_t n_pages, const int32_t* heads, int n_sel, float* scores,
-                              hipStream_t stream);
+                              uint32_t* zero_u32, int n_zero, hipStream_t stream);
 
 // ---- CV head scoring -----------------------------------------------------
 struct ScoreGeom {

@@ -142,6 +142,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 4))) voi
                                                                                                float* __restrict__ off) {
   const int sel = blockIdx.y;
   const int n_colblk = a.n_colblk, R = a.R;
+  if (blockIdx.x == 0 && blockIdx.y == 0)
+    for (int i = threadIdx.x; i < a.n_zero; i += blockDim.x) a.zero_u32[i] = 0;
   const int row = blockIdx.x * kMergeRows + (threadIdx.x >> 4);
   const int ln = threadIdx.x & 15;
   const bool ok = row < R;
@@ -329,8 +331,8 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(const float* __restr
 //
 // Three uses (MODE): a whole row of scores; one slice of a row (rows are cut
 // into PER * kTopkThreads-score slices whose own k best, in ascending order,
-// go to a candidate list); a row's candidate list (scores looked up through
-// the list, -1 entries never chosen, output mapped back through it).  The k
+// go to a candidate list with their keys); a row's candidate list (keys read
+// from the list, -1 entries never chosen, the candidates' indices out).  The k
 // best of a row are always among its slices' k best (an entry outranked by k
 // entries of its own slice is outranked by k entries of the row; ties go to
 // the lower index in both), and the candidate list is ascending, so the two
@@ -339,17 +341,25 @@ enum TopkMode { kTopkRow = 0, kTopkSliceMode = 1, kTopkList = 2 };
 constexpr int64_t kTopkSlice = 16 * kTopkThreads;   // scores per slice of long rows
 constexpr int64_t kTopkSmallSlice = 4 * kTopkThreads;   // scores per slice of short rows
 
+// A candidate: the score's ordered key (low word) and its index (high word,
+// -1 for none).  The two stages run in one launch (topk_fused_kernel): a
+// slice writes its candidates with device-scope atomics and the list stage
+// reads them with device-scope atomic loads, so a workgroup on another XCD
+// sees them, and the list stage needs no second look at the scores.
+typedef unsigned long long TopkCand;
+
 struct TopkArgs {
   const float* S;          // scores [rows][n]
   int64_t n;
-  const int32_t* list;     // kTopkList: candidate indices [rows][list_len], -1 = none
+  const TopkCand* list;    // kTopkList: candidates [rows][list_len]
   int64_t list_len;
   int k, b;                // select k; kTopkRow / kTopkList write b entries per row (-1 padded)
-  int32_t* out;            // kTopkSliceMode: [rows][n_slices][k]; otherwise [rows][b]
+  int32_t* out;            // kTopkRow / kTopkList: [rows][b]
+  TopkCand* cand;          // kTopkSliceMode: [rows][n_slices][k]
 };
 
 template <int PER, int MODE>
-__global__ __launch_bounds__(kTopkThreads) void topk_wave_kernel(TopkArgs a) {
+__device__ __forceinline__ void topk_body(const TopkArgs& a, int row, int slice, int n_slices) {
   constexpr int NW = kTopkThreads / 64;
   constexpr int NCOPY = 16;
   constexpr int RS = 260;                  // words per copy: 256 bins, rows 16-byte aligned
@@ -360,33 +370,41 @@ __global__ __launch_bounds__(kTopkThreads) void topk_wave_kernel(TopkArgs a) {
   __shared__ uint32_t s_prefix;
   __shared__ int s_remaining;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int row = MODE == kTopkSliceMode ? blockIdx.y : blockIdx.x;
   const float* Ss = a.S + (size_t)row * a.n;
   int64_t start = 0, len = a.n;
   int k = a.k, b = a.b;
   int32_t* out = a.out + (size_t)row * a.b;
-  const int32_t* lst = nullptr;
+  TopkCand* cout = nullptr;
+  const TopkCand* lst = nullptr;
   if (MODE == kTopkSliceMode) {
     constexpr int64_t SL = (int64_t)PER * kTopkThreads;
-    start = (int64_t)blockIdx.x * SL;
+    start = (int64_t)slice * SL;
     len = min(SL, a.n - start);
     k = (int)min((int64_t)a.k, len);
     b = a.k;
-    out = a.out + ((size_t)row * gridDim.x + blockIdx.x) * a.k;
+    cout = a.cand + ((size_t)row * n_slices + slice) * a.k;
   } else if (MODE == kTopkList) {
     len = a.list_len;
     lst = a.list + (size_t)row * a.list_len;
   }
   const int64_t base = (int64_t)wave * PER * 64 + lane;       // entry of row 0; row i adds 64 i
+  // kTopkList keeps the candidates' indices in registers up to 8 per lane
+  // and reads longer lists' indices again when writing (registers: at most
+  // 128 per lane at 1024 threads)
+  constexpr bool KEEP = PER <= 8;
   uint32_t key[PER];
+  int32_t idx[KEEP ? PER : 1];
   uint32_t vmask = 0;                                          // bit i: row i holds an entry
   const int64_t rem = len - base;
   const int nv = rem <= 0 ? 0 : (int)min<int64_t>(PER, (rem + 63) / 64);
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
     if (MODE == kTopkList) {
-      const int32_t j = i < nv ? lst[base + 64 * i] : -1;
-      key[i] = j >= 0 ? ord_key(Ss[j]) : 0u;
+      TopkCand c = 0xFFFFFFFF00000000ull;
+      if (i < nv) c = __hip_atomic_load(&lst[base + 64 * i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const int32_t j = (int32_t)(c >> 32);
+      if (KEEP) idx[KEEP ? i : 0] = j;
+      key[i] = j >= 0 ? (uint32_t)c : 0u;
       vmask |= (j >= 0 ? 1u : 0u) << i;
     } else {
       key[i] = i < nv ? ord_key(Ss[start + base + 64 * i]) : 0u;
@@ -495,12 +513,45 @@ __global__ __launch_bounds__(kTopkThreads) void topk_wave_kernel(TopkArgs a) {
     const int p = pos + __popcll(mt & below);
     if (take && p < k) {
       const int64_t e = base + 64 * i;
-      out[p] = MODE == kTopkList ? lst[e] : (int32_t)(start + e);
+      if (MODE == kTopkList)
+        out[p] = KEEP ? idx[KEEP ? i : 0]
+                      : (int32_t)(__hip_atomic_load(&lst[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >> 32);
+      else if (MODE == kTopkSliceMode)
+        atomicExch(&cout[p], ((TopkCand)(uint32_t)(start + e) << 32) | key[i]);
+      else out[p] = (int32_t)(start + e);
     }
     pos += __popcll(mt);
     eqr += __popcll(meq);
   }
-  for (int i = k + t; i < b; i += kTopkThreads) out[i] = -1;
+  for (int i = k + t; i < b; i += kTopkThreads) {
+    if (MODE == kTopkSliceMode) atomicExch(&cout[i], 0xFFFFFFFF00000000ull);
+    else out[i] = -1;
+  }
+}
+
+// one row per workgroup
+template <int PER>
+__global__ __launch_bounds__(kTopkThreads) void topk_wave_kernel(TopkArgs a) {
+  topk_body<PER, kTopkRow>(a, blockIdx.x, 0, 1);
+}
+
+// Both stages in one launch, grid (slices, rows): every workgroup selects its
+// slice's k best; the last of a row to finish (arrive[row] counts them, zero
+// on entry and reset on exit) selects the row's k best among the candidates.
+// A workgroup arrives once its candidate stores have completed (device-scope
+// atomics, waited for), so no cache write-back is needed.
+template <int PER1, int PER2>
+__global__ __launch_bounds__(kTopkThreads) void topk_fused_kernel(TopkArgs s1, TopkArgs s2, uint32_t* arrive) {
+  __shared__ int s_last;
+  const int row = blockIdx.y;
+  topk_body<PER1, kTopkSliceMode>(s1, row, blockIdx.x, gridDim.x);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0) s_last = atomicAdd(&arrive[row], 1u) == gridDim.x - 1;
+  __syncthreads();
+  if (!s_last) return;
+  topk_body<PER2, kTopkList>(s2, row, 0, 1);
+  if (threadIdx.x == 0) arrive[row] = 0;
 }
 
 struct CompactArgs {
@@ -634,6 +685,8 @@ hipError_t launch_select(int dtype, const SelectGeom& g, const void* q_obs, cons
   a.rowpart = reinterpret_cast<float2*>(w + L.rowpart);
   a.rowoff = reinterpret_cast<const float*>(w + L.rowoff);
   a.colmass = reinterpret_cast<float*>(w + L.colmass);
+  a.zero_u32 = reinterpret_cast<uint32_t*>(w + L.topk);   // the top-k's arrival counters
+  a.n_zero = g.n_sel;
   const dim3 grid(g.n_colblk, g.n_sel);
   hipError_t e = launch_score_rowstats(dtype, g.G, false, rp, grid, stream, a);
   if (e != hipSuccess) return e;
@@ -655,25 +708,25 @@ hipError_t launch_select(int dtype, const SelectGeom& g, const void* q_obs, cons
   return launch_topk(S, g.n_sel, g.n_chunks, g.b, idx_out, w + L.topk, stream);
 }
 
+// ws: n_rows arrival counters (zero on entry: the caller's previous kernel
+// clears them; left zero), then the candidate lists of two-stage rows.
+size_t topk_counter_bytes(int n_rows) { return align256((size_t)n_rows * sizeof(uint32_t)); }
 size_t topk_workspace_bytes(int n_rows, int64_t n) {
-  return n > kTopkSmallSlice ? (size_t)n_rows * 2 * kTopkSlice * sizeof(int32_t) : 0;
+  return topk_counter_bytes(n_rows) + (n > kTopkSmallSlice ? (size_t)n_rows * 2 * kTopkSlice * sizeof(TopkCand) : 0);
 }
 
-// k best of each row's candidate list (ascending indices into the row)
-static void launch_topk_list(const TopkArgs& a, int n_rows, hipStream_t stream) {
-  const int64_t m = a.list_len;
-  if (m <= 1 * kTopkThreads)
-    hipLaunchKernelGGL((topk_wave_kernel<1, kTopkList>), dim3(n_rows), dim3(kTopkThreads), 0, stream, a);
-  else if (m <= 2 * kTopkThreads)
-    hipLaunchKernelGGL((topk_wave_kernel<2, kTopkList>), dim3(n_rows), dim3(kTopkThreads), 0, stream, a);
-  else if (m <= 4 * kTopkThreads)
-    hipLaunchKernelGGL((topk_wave_kernel<4, kTopkList>), dim3(n_rows), dim3(kTopkThreads), 0, stream, a);
-  else if (m <= 8 * kTopkThreads)
-    hipLaunchKernelGGL((topk_wave_kernel<8, kTopkList>), dim3(n_rows), dim3(kTopkThreads), 0, stream, a);
-  else if (m <= 16 * kTopkThreads)
-    hipLaunchKernelGGL((topk_wave_kernel<16, kTopkList>), dim3(n_rows), dim3(kTopkThreads), 0, stream, a);
-  else
-    hipLaunchKernelGGL((topk_wave_kernel<32, kTopkList>), dim3(n_rows), dim3(kTopkThreads), 0, stream, a);
+// both stages in one launch; PER2 from the candidate list's length
+template <int PER1>
+static void launch_topk_fused(const TopkArgs& s1, const TopkArgs& s2, unsigned n_slices, int n_rows,
+                              uint32_t* arrive, hipStream_t stream) {
+  const int64_t m = s2.list_len;
+  const dim3 grid(n_slices, n_rows), block(kTopkThreads);
+  if (m <= 1 * kTopkThreads) hipLaunchKernelGGL((topk_fused_kernel<PER1, 1>), grid, block, 0, stream, s1, s2, arrive);
+  else if (m <= 2 * kTopkThreads) hipLaunchKernelGGL((topk_fused_kernel<PER1, 2>), grid, block, 0, stream, s1, s2, arrive);
+  else if (m <= 4 * kTopkThreads) hipLaunchKernelGGL((topk_fused_kernel<PER1, 4>), grid, block, 0, stream, s1, s2, arrive);
+  else if (m <= 8 * kTopkThreads) hipLaunchKernelGGL((topk_fused_kernel<PER1, 8>), grid, block, 0, stream, s1, s2, arrive);
+  else if (m <= 16 * kTopkThreads) hipLaunchKernelGGL((topk_fused_kernel<PER1, 16>), grid, block, 0, stream, s1, s2, arrive);
+  else hipLaunchKernelGGL((topk_fused_kernel<PER1, 32>), grid, block, 0, stream, s1, s2, arrive);
 }
 
 hipError_t launch_topk(const float* S, int n_rows, int64_t n, int b, int32_t* idx_out, void* ws,
@@ -690,30 +743,27 @@ hipError_t launch_topk(const float* S, int n_rows, int64_t n, int b, int32_t* id
   // most an eighth of a slice.
   const bool few_short_rows = ws && n > kTopkSmallSlice && n <= 2 * kTopkSlice &&
                               8 * k_eff <= kTopkSmallSlice && (int64_t)n_rows * n_small <= 2048;
+  uint32_t* arrive = reinterpret_cast<uint32_t*>(ws);
+  TopkCand* cand = ws ? reinterpret_cast<TopkCand*>(reinterpret_cast<char*>(ws) + topk_counter_bytes(n_rows)) : nullptr;
   if (few_short_rows) {
     TopkArgs s1 = a;
-    s1.out = reinterpret_cast<int32_t*>(ws);
-    hipLaunchKernelGGL((topk_wave_kernel<4, kTopkSliceMode>), dim3((unsigned)n_small, n_rows),
-                       dim3(kTopkThreads), 0, stream, s1);
+    s1.cand = cand;
     TopkArgs s2 = a;
-    s2.list = s1.out;
+    s2.list = cand;
     s2.list_len = n_small * k_eff;
-    launch_topk_list(s2, n_rows, stream);
+    launch_topk_fused<4>(s1, s2, (unsigned)n_small, n_rows, arrive, stream);
   } else if (n <= kTopkSlice) {
-    hipLaunchKernelGGL((topk_wave_kernel<16, kTopkRow>), dim3(n_rows), dim3(kTopkThreads), 0, stream, a);
+    hipLaunchKernelGGL((topk_wave_kernel<16>), dim3(n_rows), dim3(kTopkThreads), 0, stream, a);
   } else if (n <= 2 * kTopkSlice) {
-    hipLaunchKernelGGL((topk_wave_kernel<32, kTopkRow>), dim3(n_rows), dim3(kTopkThreads), 0, stream, a);
+    hipLaunchKernelGGL((topk_wave_kernel<32>), dim3(n_rows), dim3(kTopkThreads), 0, stream, a);
   } else if (ws && n_slices * k_eff <= 2 * kTopkSlice) {
     // the k best of every slice, then the k best of those candidates
-    int32_t* cand = reinterpret_cast<int32_t*>(ws);
     TopkArgs s1 = a;
-    s1.out = cand;
-    hipLaunchKernelGGL((topk_wave_kernel<16, kTopkSliceMode>), dim3((unsigned)n_slices, n_rows),
-                       dim3(kTopkThreads), 0, stream, s1);
+    s1.cand = cand;
     TopkArgs s2 = a;
     s2.list = cand;
     s2.list_len = n_slices * k_eff;
-    launch_topk_list(s2, n_rows, stream);
+    launch_topk_fused<16>(s1, s2, (unsigned)n_slices, n_rows, arrive, stream);
   } else {
     hipLaunchKernelGGL(topk_kernel, dim3(n_rows), dim3(kTopkThreads), 0, stream, S, n, k_eff, b, idx_out);
   }

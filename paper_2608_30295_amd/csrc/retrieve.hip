@@ -37,6 +37,8 @@ struct PageScoreArgs {
   int64_t n_pages;
   int32_t heads[128];
   float* scores;          // [n_sel][n_pages]
+  uint32_t* zero_u32;     // cleared here for the top-k launch that follows, n_zero words
+  int n_zero;
 };
 
 // 16 bytes as fp32 values (8 bf16 or 4 fp32) and back; bf16 <-> fp32 is exact
@@ -108,6 +110,8 @@ __global__ __launch_bounds__(256) void page_score_kernel(PageScoreArgs a) {
   const int h = a.heads[sel];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int seg = lane % SEG, sub = lane / SEG;
+  if (blockIdx.x == 0 && blockIdx.y == 0)
+    for (int i = threadIdx.x; i < a.n_zero; i += blockDim.x) a.zero_u32[i] = 0;
   float qv[G][S::E];
 #pragma unroll
   for (int g = 0; g < G; ++g)
@@ -153,9 +157,10 @@ hipError_t launch_page_bounds(int dtype, const void* k, int64_t n, int cs, const
 
 hipError_t launch_page_scores(int dtype, int G, const void* q, const void* kmin, const void* kmax,
                               int64_t n_pages, const int32_t* heads, int n_sel, float* scores,
-                              hipStream_t stream) {
+                              uint32_t* zero_u32, int n_zero, hipStream_t stream) {
   PageScoreArgs a{};
   a.q = q; a.kmin = kmin; a.kmax = kmax; a.n_pages = n_pages; a.scores = scores;
+  a.zero_u32 = zero_u32; a.n_zero = n_zero;
   for (int i = 0; i < n_sel; ++i) a.heads[i] = heads[i];
   const int ppb = 4 * (dtype == CATEKV_BF16 ? 4 : 2);      // pages per workgroup per iteration
   const unsigned nblk = (unsigned)std::min<int64_t>((n_pages + ppb - 1) / ppb, 1024);

@@ -110,6 +110,8 @@ struct ScoreArgs {
   // route reads A)
   CvLink cv;
   int cv_gate;
+  uint32_t* zero_u32;     // cleared by the row-statistics merge (a later launch's counters), n_zero words
+  int n_zero;
 };
 
 template <typename T, int W, int MT, int MODE, int G, bool CAUSAL>

@@ -247,6 +247,27 @@ def test_retrieve_exact_ties_lowest_pages_first(n_pages, n_keep):
     assert idx.tolist() == want.tolist()
 
 
+@pytest.mark.parametrize("n_pages,n_keep", [(70000, 3000), (100000, 3000)])
+def test_retrieve_exact_ties_long_candidate_lists(n_pages, n_keep):
+    """Slices then candidates with 15000 and 21000 candidates per row (the
+    list stage reads the candidates' indices again when writing); the pages
+    repeat 37 patterns, so the oracle scores the patterns and tiles them."""
+    rng = np.random.default_rng(90 + n_pages + n_keep)
+    cs, G = 8, 4
+    pat = synth.f32_to_bf16_bits(rng.standard_normal((37, cs, 128), dtype=np.float32))
+    kk = pat[np.arange(n_pages) % 37].reshape(1, n_pages * cs, 128)
+    q_st = synth.f32_to_bf16_bits(rng.standard_normal((G, 128), dtype=np.float32))
+    say(f"retrieve long lists: pages={n_pages} keep={n_keep}")
+    kmin, kmax = ck.page_bounds(to_dev(kk), [0], cs)
+    idx = ck.retrieve_pages(to_dev(q_st), kmin, kmax, [0], 1, n_keep).cpu().numpy()[0]
+    mn, mx = O.page_bounds(f64(pat.reshape(37 * cs, 128)), cs)
+    sc = O.page_scores(f64(q_st), mn, mx)[np.arange(n_pages) % 37]
+    want = O.argtopk_ascending(sc, n_keep)
+    kth = np.sort(sc)[::-1][n_keep - 1]
+    assert (sc == kth).sum() > 1 and (sc > kth).sum() < n_keep
+    assert idx.tolist() == want.tolist()
+
+
 # ---------------------------------------------------- attention recall
 
 def test_recall_of_gpu_selection_and_retrieval_matches_oracle():
