@@ -69,6 +69,27 @@ def test_decode_ragged_views(dtype):
         np.testing.assert_allclose(lse[b], l_ref, atol=1e-4, rtol=0)
 
 
+def test_decode_more_views_than_preloaded():
+    """320 views (40 sequences x 8 KV heads) on the one-workgroup-per-CU
+    layout: beyond 256 views the stream kernel reads each segment's view
+    pointers and length itself instead of from the table every workgroup
+    preloads."""
+    rng = np.random.default_rng(17)
+    B, hq, hkv = 40, 16, 8
+    lens = rng.integers(300, 700, size=B * hkv).tolist()
+    views = _views(rng, lens, "bf16")
+    q_st = synth.f32_to_bf16_bits(rng.standard_normal((B, hq, 128), dtype=np.float32))
+    say(f"decode {B * hkv} views")
+    out, lse, _, plan = run_decode(views, B, hq, hkv, "bf16", q_st)
+    assert plan.plan.variant == 2 and plan.plan.n_multi > 0
+    qq = f64(q_st)
+    for b in range(B):
+        vv = [(f64(views[b * hkv + h][0]), f64(views[b * hkv + h][1])) for h in range(hkv)]
+        o_ref, l_ref = O.decode_gqa(qq[b], vv)
+        assert_rows_close(out[b], o_ref, "bf16", f"b={b}")
+        np.testing.assert_allclose(lse[b], l_ref, atol=1e-4, rtol=0)
+
+
 def test_decode_empty_and_single_token_views():
     rng = np.random.default_rng(12)
     B, hq, hkv = 1, 4, 4
