@@ -32,20 +32,6 @@ __device__ __forceinline__ uint32_t mbcnt(uint64_t m) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
 }
 
-// LDS histogram update by a wave: the lanes that share the leading active
-// lane's bin add with one atomic, the rest one by one.  act = ballot(valid).
-__device__ __forceinline__ void hist_add_act(uint32_t* s_h, uint64_t act, bool valid, uint32_t bin) {
-  const int lead = __builtin_ctzll(act);
-  const uint32_t lb = (uint32_t)__builtin_amdgcn_readlane((int)bin, lead);
-  const uint64_t same = __builtin_amdgcn_ballot_w64(valid && bin == lb);
-  const int lane = threadIdx.x & 63;
-  if (lane == lead) atomicAdd(&s_h[lb], (uint32_t)__builtin_popcountll(same));
-  else if (valid && bin != lb) atomicAdd(&s_h[bin], 1u);
-}
-__device__ __forceinline__ void hist_add(uint32_t* s_h, bool valid, uint32_t bin) {
-  const uint64_t act = __builtin_amdgcn_ballot_w64(valid);
-  if (act) hist_add_act(s_h, act, valid, bin);
-}
 
 // For a histogram hh[0, nb) (LDS or global) and 0-based ranks r0, r1 below
 // its total: the bins holding them (s_bin[0], s_bin[1]), their positions
@@ -106,21 +92,6 @@ __device__ __forceinline__ unsigned long long block_sum256(unsigned long long v,
   if ((threadIdx.x & 63) == 0) s[threadIdx.x >> 6] = v;
   __syncthreads();
   return s[0] + s[1] + s[2] + s[3];
-}
-
-// K sums over a workgroup of 256 threads at once (one exchange).
-template <int K>
-__device__ __forceinline__ void block_sums256(unsigned long long (&v)[K], unsigned long long (*s)[4]) {
-#pragma unroll
-  for (int k = 0; k < K; ++k)
-    for (int off = 32; off > 0; off >>= 1) v[k] += __shfl_xor(v[k], off);
-  __syncthreads();
-  if ((threadIdx.x & 63) == 0)
-#pragma unroll
-    for (int k = 0; k < K; ++k) s[k][threadIdx.x >> 6] = v[k];
-  __syncthreads();
-#pragma unroll
-  for (int k = 0; k < K; ++k) v[k] = s[k][0] + s[k][1] + s[k][2] + s[k][3];
 }
 
 // Eq. 4 from exact integer sums: sqrt(E[C^2] - E[C]^2) / E[C].
@@ -247,7 +218,9 @@ __global__ __launch_bounds__(kSampleThreads) void cv_sample_kernel(const float* 
 // ---------------------------------------------------------------------------
 // 2. The bracketing pass is the observation-matrix pass (score.h,
 //    kObsBracket): the entries at or above min(bracket bottom, t_lo) as
-//    (value, column), in one buffer per wave of each column block.
+//    (value, column), in one buffer per wave of each column block; at its
+//    end each workgroup counts its pairs into the head's totals (bracket
+//    entries by first digit, entries at or above the bracket's bottom).
 // ---------------------------------------------------------------------------
 
 constexpr int kCountRows = 16;    // rows per lane loaded together by the radix route's column walk
@@ -308,52 +281,6 @@ __device__ __forceinline__ const uint2* buffer_item(const uint2* __restrict__ pa
   int w = 0;
   while (w + 1 < nb && s_pre[w + 1] <= k) ++w;
   return pairs + (first + w) * capw + (k - s_pre[w]);
-}
-
-// Pairs of column block b (its waves' buffers): the bracket entries are
-// counted and histogrammed by their first digit, and the pairs at or above
-// the bracket's bottom counted (the entries below the bracket follow,
-// cv_below).
-__global__ __launch_bounds__(256) void cv_pairs_kernel(CvState* st, uint32_t* __restrict__ hist0,
-                                                       const uint2* __restrict__ pairs,
-                                                       const uint32_t* __restrict__ pfill, uint32_t capw, int nsub,
-                                                       int n_colblk) {
-  __shared__ uint32_t s_h[kBins];
-  __shared__ unsigned long long s_red5[2][4];
-  __shared__ uint32_t s_pre[kCvMaxSub + 1];
-  const int h = blockIdx.y, b = blockIdx.x;
-  const int t = threadIdx.x;
-  CvState& S = st[h];
-  for (int i = t; i < kBins; i += 256) s_h[i] = 0;
-  const uint32_t k_lo = S.k_lo, span = S.k_hi - S.k_lo;
-  const int sh1 = S.shift1;
-  const float f_lo = key_to_float(k_lo);
-  __syncthreads();
-  uint32_t n_in = 0, n_lo = 0;
-  const size_t first = ((size_t)h * n_colblk + b) * nsub;
-  const uint32_t total = buffer_prefix(pfill, first, nsub, s_pre);
-  for (uint32_t i0 = 0; i0 < total; i0 += 4 * 256) {   // the same trip count on every lane
-    uint32_t x[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u)   // every load issued (clamped), then used
-      x[u] = buffer_item(pairs, first, nsub, capw, s_pre, min(i0 + u * 256 + t, total - 1))->x;
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const bool ok = i0 + u * 256 + t < total;
-      const uint32_t o = (x[u] | 0x80000000u) - k_lo;
-      const bool in = ok && o <= span;
-      n_in += in;
-      n_lo += ok && __uint_as_float(x[u]) >= f_lo;
-      hist_add(s_h, in, o >> sh1);
-    }
-  }
-  unsigned long long v[2] = {n_in, n_lo};
-  block_sums256(v, s_red5);
-  if (t == 0) {
-    if (v[0]) atomicAdd(&S.n_cand, v[0]);
-    if (v[1]) atomicAdd(&S.ge_lo, v[1]);
-  }
-  flush_hist(s_h, hist0 + (size_t)h * kBins);
 }
 
 // ---------------------------------------------------------------------------
@@ -842,12 +769,6 @@ hipError_t launch_cv_sample(const ScoreArgs& a, double k_pct, double alpha, hipS
   const int64_t N = (int64_t)a.lq * a.n_keys;
   hipLaunchKernelGGL(cv_sample_kernel, dim3(a.hkv), dim3(kSampleThreads), 0, stream, a.cv.samples, N, k_pct, alpha,
                      a.cv.st, a.cv.hist, a.hkv);
-  return hipGetLastError();
-}
-
-hipError_t launch_cv_pairs(const ScoreArgs& a, hipStream_t stream) {
-  hipLaunchKernelGGL(cv_pairs_kernel, dim3((unsigned)a.n_colblk, a.hkv), dim3(256), 0, stream, a.cv.st, a.cv.hist,
-                     a.cv.pairs, a.cv.pfill, a.cv.capw, a.cv.nsub, a.n_colblk);
   return hipGetLastError();
 }
 

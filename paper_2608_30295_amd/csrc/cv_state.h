@@ -31,6 +31,21 @@ __device__ __forceinline__ float cv_key_float(uint32_t key) {
   return __uint_as_float((key & 0x80000000u) ? (key & 0x7FFFFFFFu) : ~key);
 }
 
+// LDS histogram update by a wave: the lanes that share the leading active
+// lane's bin add with one atomic, the rest one by one.  act = ballot(valid).
+__device__ __forceinline__ void hist_add_act(uint32_t* s_h, uint64_t act, bool valid, uint32_t bin) {
+  const int lead = __builtin_ctzll(act);
+  const uint32_t lb = (uint32_t)__builtin_amdgcn_readlane((int)bin, lead);
+  const uint64_t same = __builtin_amdgcn_ballot_w64(valid && bin == lb);
+  const int lane = threadIdx.x & 63;
+  if (lane == lead) atomicAdd(&s_h[lb], (uint32_t)__builtin_popcountll(same));
+  else if (valid && bin != lb) atomicAdd(&s_h[bin], 1u);
+}
+__device__ __forceinline__ void hist_add(uint32_t* s_h, bool valid, uint32_t bin) {
+  const uint64_t act = __builtin_amdgcn_ballot_w64(valid);
+  if (act) hist_add_act(s_h, act, valid, bin);
+}
+
 struct CvState {                   // per KV head, in the workspace
   int64_t rank;                    // lo = floor((N - 1) k), 0-based
   uint32_t k_lo, k_hi;             // the bracket: ordered keys [k_lo, k_hi]

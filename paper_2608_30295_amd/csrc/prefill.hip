@@ -840,8 +840,6 @@ hipError_t launch_score(int dtype, const ScoreGeom& g, const void* q_rows, const
   if (e != hipSuccess) return e;
   e = launch_score_obs_bracket(dtype, g.G, g.causal, rp, grid, stream, a);
   if (e != hipSuccess) return e;
-  e = launch_cv_pairs(a, stream);
-  if (e != hipSuccess) return e;
   a.cv_gate = 1;
   e = launch_score_obs(dtype, g.G, g.causal, rp, grid, stream, a);
   if (e != hipSuccess) return e;

@@ -488,6 +488,60 @@ __device__ __forceinline__ void score_body(const ScoreArgs& a) {
     }
     if (threadIdx.x >= W && threadIdx.x < a.cv.nsub)   // buffers of waves this shape does not have
       a.cv.pfill[((size_t)sel * a.n_colblk + cb) * a.cv.nsub + threadIdx.x] = 0;
+    // Each wave reads its own pairs back (its stores have completed: the
+    // wait above): the bracket entries are counted and histogrammed by
+    // their first digit (key - k_lo) >> shift1, and the pairs at or above
+    // the bracket's bottom counted; the block's counts and histogram go to
+    // the head's totals with one atomic each.
+    __shared__ uint32_t s_ph[OBSB ? kCvBins : 1];
+    __shared__ uint32_t s_pc[OBSB ? 2 * W : 1];
+    for (int i = threadIdx.x; i < kCvBins; i += W * 64) s_ph[i] = 0;
+    __syncthreads();
+    const CvState& B = a.cv.st[sel];
+    const uint32_t k_lo = B.k_lo, span = B.k_hi - B.k_lo;
+    const int sh1 = B.shift1;
+    const float f_lo = cv_key_float(k_lo);
+    const uint32_t fill = min(wfill, a.cv.capw);
+    uint32_t n_in = 0, n_lo = 0;
+    for (uint32_t i0 = 0; i0 < fill; i0 += 4 * 64) {   // the same trip count on every lane
+      uint32_t x[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {     // every load issued (clamped), then used
+        const uint32_t i = i0 + u * 64 + lane;
+        x[u] = wpairs[i < fill ? i : fill - 1].x;
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const bool ok = i0 + u * 64 + lane < fill;
+        const uint32_t o = (x[u] | 0x80000000u) - k_lo;
+        const bool in = ok && o <= span;
+        n_in += in;
+        n_lo += ok && __uint_as_float(x[u]) >= f_lo;
+        hist_add(s_ph, in, o >> sh1);
+      }
+    }
+    for (int off = 32; off > 0; off >>= 1) {
+      n_in += __shfl_xor(n_in, off);
+      n_lo += __shfl_xor(n_lo, off);
+    }
+    if (lane == 0) {
+      s_pc[wave] = n_in;
+      s_pc[W + wave] = n_lo;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      unsigned long long c_in = 0, c_lo = 0;
+#pragma unroll
+      for (int w = 0; w < W; ++w) {
+        c_in += s_pc[w];
+        c_lo += s_pc[W + w];
+      }
+      if (c_in) atomicAdd(&a.cv.st[sel].n_cand, c_in);
+      if (c_lo) atomicAdd(&a.cv.st[sel].ge_lo, c_lo);
+    }
+    uint32_t* h0 = a.cv.hist0 + (size_t)sel * kCvBins;
+    for (int i = threadIdx.x; i < kCvBins; i += W * 64)
+      if (s_ph[i]) atomicAdd(&h0[i], s_ph[i]);
   }
 
   if (MODE == kRowStats) {
@@ -567,7 +621,6 @@ hipError_t launch_score_obs_bracket(int dtype, int G, bool causal, int rows_pad,
 size_t cv_workspace_bytes(int hkv, int lq, int64_t n_keys, int n_colblk);
 CvLink cv_link(void* ws, int hkv, int lq, int64_t n_keys, int n_colblk, int nsub);
 hipError_t launch_cv_sample(const ScoreArgs& a, double k_pct, double alpha, hipStream_t s);
-hipError_t launch_cv_pairs(const ScoreArgs& a, hipStream_t s);
 hipError_t launch_cv_finish(const ScoreArgs& a, double k_pct, double alpha, float* cv_out, hipStream_t s);
 
 }  // namespace catekv
