@@ -365,6 +365,8 @@ CV_CASES = [
     ("ctx32k_bf16", dict(n=6000), True),
     ("ctx1m_bf16", dict(n=7000), True),          # decode-time calibration rows (mask is a no-op)
     ("ctx32k_bf16", dict(n=3000, hq=16, hkv=2), False),
+    ("ctx32k_bf16", dict(n=5000, hq=4, hkv=4), True),      # one query head per KV head
+    ("ctx32k_bf16", dict(n=4000, hq=8, hkv=4), False),     # two
 ]
 
 
