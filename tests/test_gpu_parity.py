@@ -253,6 +253,8 @@ SEL_CASES = [
     ("ctx32k_bf16", dict(n=16 + 8 * 40000 + 5, hq=4, hkv=2, l_obs=16)),   # over 32768: slices, then candidates
     ("ctx32k_bf16", dict(n=64 + 8 * 4097, hq=8, hkv=2, budget=4096)),    # 4096-score slices, one-score last slice, k = 512
     ("ctx32k_bf16", dict(n=64 + 8 * 9000 + 5, hq=8, hkv=2, budget=8)),   # 4096-score slices, k = 1
+    ("ctx32k_bf16", dict(n=6000 + 11, hq=4, hkv=4)),          # one query head per KV head (64 rows)
+    ("ctx32k_bf16", dict(n=6000 + 29, hq=8, hkv=4, l_obs=32)), # G = 2 at 32 window rows (64 rows)
 ]
 
 
