@@ -634,9 +634,10 @@ void decode_stream_v2_kernel(DecodeArgs a) {
   uint4 kb[2][4], vb[2][4];
   int meta_seg[2], meta_tile[2];                 // segment and first token of the tile in each buffer
   int lseg = 0, ltile = 0;                       // the last tile issued for real
-  // Loads of one tile; past the end of the stream the last real tile is read
-  // again (cached) and the buffer is marked empty.  Rows past a segment's end
-  // re-read its first row, so every address lies inside a segment's rows.
+  // Loads of one tile (called only while the stream has tiles; past its end
+  // the last real tile would be read again and the buffer marked empty).
+  // Rows past a segment's end re-read its first row, so every address lies
+  // inside a segment's rows.
   auto issue = [&](int buf) {
     if (is < nseg) {
       lseg = is;
@@ -813,16 +814,31 @@ void decode_stream_v2_kernel(DecodeArgs a) {
   }
   __syncthreads();
 
-  if (is < nseg) {
+  // This wave's tiles (tile u of a segment for u = wave, wave + 8, ...) are
+  // counted first, so that every issue loads a real tile: no load is still
+  // in flight when the stream ends.  Buffer 0 holds tile i on entry to the
+  // loop, whose body keeps one tile in flight while it consumes another.
+  int n_my = 0;
+  for (int s2 = 0; s2 < nseg; ++s2) {
+    const int u = s_seg[s2].n_units;
+    n_my += u > wave ? (u - wave + WAVES - 1) / WAVES : 0;
+  }
+  if (n_my > 0) {
     issue(0);
-    bool more = true;
-    while (more) {
-#pragma unroll
-      for (int B = 0; B < 2; ++B) {
-        issue(B ^ 1);
-        if (meta_seg[B] >= 0) consume(B);
-        else more = false;
-      }
+    int i = 0;
+    while (i + 2 < n_my) {     // tiles i, i + 1 and i + 2 exist
+      issue(1);
+      consume(0);
+      issue(0);
+      consume(1);
+      i += 2;
+    }
+    if (i + 1 < n_my) {
+      issue(1);
+      consume(0);
+      consume(1);
+    } else {
+      consume(0);
     }
   }
   while (merged < nseg) merge(merged++);
