@@ -255,6 +255,7 @@ SEL_CASES = [
     ("ctx32k_bf16", dict(n=64 + 8 * 9000 + 5, hq=8, hkv=2, budget=8)),   # 4096-score slices, k = 1
     ("ctx32k_bf16", dict(n=6000 + 11, hq=4, hkv=4)),          # one query head per KV head (64 rows)
     ("ctx32k_bf16", dict(n=6000 + 29, hq=8, hkv=4, l_obs=32)), # G = 2 at 32 window rows (64 rows)
+    ("ctx32k_bf16", dict(n=7000 + 3, l_obs=37)),              # 148 rows, padded to 256
 ]
 
 
@@ -369,6 +370,7 @@ CV_CASES = [
     ("ctx32k_bf16", dict(n=3000, hq=16, hkv=2), False),
     ("ctx32k_bf16", dict(n=5000, hq=4, hkv=4), True),      # one query head per KV head
     ("ctx32k_bf16", dict(n=4000, hq=8, hkv=4), False),     # two
+    ("ctx32k_bf16", dict(n=4500, l_obs=37), True),         # 148 rows: padding rows in every pass
 ]
 
 
