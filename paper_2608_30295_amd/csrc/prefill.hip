@@ -322,12 +322,14 @@ __global__ __launch_bounds__(kTopkThreads) void topk_kernel(const float* __restr
 // contiguous range [w * PER * 64, (w + 1) * PER * 64): its row i is the 64
 // consecutive chunks from w * PER * 64 + 64 i, one per lane, so every load
 // of the wave is one contiguous 256-byte read and ascending (row, lane) is
-// ascending index.  Radix passes over 8-bit digits count into 16 LDS copies
-// (lane & 15) of the histogram, double-buffered so the copy for the next
-// pass is cleared during this one; wave 0 sums the copies and finds the bin
-// of the target rank with a suffix scan, so a pass costs two barriers.  The
-// positions of the selected entries come from per-row ballots and one
-// exchange of the per-wave counts.
+// ascending index.  Radix passes over 8-bit digits, from the highest bit in
+// which the keys differ, count into 16 LDS copies (lane & 15) of the
+// histogram, double-buffered so the copy for the next pass is cleared during
+// this one; wave 0 sums the copies and finds the bin of the target rank with a
+// suffix scan (DPP steps), so a pass costs two barriers.  Once the target bin
+// holds at most 64 keys, they are listed and one wave ranks them, in place of
+// the remaining passes.  The positions of the selected entries come from
+// per-row ballots and one exchange of the per-wave counts.
 //
 // Three uses (MODE): a whole row of scores; one slice of a row (rows are cut
 // into PER * kTopkThreads-score slices whose own k best, in ascending order,
@@ -358,17 +360,59 @@ struct TopkArgs {
   TopkCand* cand;          // kTopkSliceMode: [rows][n_slices][k]
 };
 
+// Wave-wide AND / OR of a word (every lane gets it): DPP steps inside each
+// row of 16 lanes, then the gfx950 row swaps; no LDS traffic.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, false);
+}
+__device__ __forceinline__ uint32_t wave_and(uint32_t x) {
+  x &= dpp_u32<kDppXor1>(x);
+  x &= dpp_u32<kDppXor2>(x);
+  x &= dpp_u32<kDppHalfMirror>(x);
+  x &= dpp_u32<kDppMirror>(x);
+  const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  x = r[0] & r[1];
+  const auto r2 = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+  return r2[0] & r2[1];
+}
+__device__ __forceinline__ uint32_t wave_or(uint32_t x) {
+  x |= dpp_u32<kDppXor1>(x);
+  x |= dpp_u32<kDppXor2>(x);
+  x |= dpp_u32<kDppHalfMirror>(x);
+  x |= dpp_u32<kDppMirror>(x);
+  const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+  x = r[0] | r[1];
+  const auto r2 = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+  return r2[0] | r2[1];
+}
+// Inclusive suffix sums over the 64 lanes (lane l gets the sum over lanes
+// l..63): row_shl steps (lane l reads lane l + s of its row, 0 past the row's
+// end), then the totals of the rows above by readlane.
+__device__ __forceinline__ int wave_suffix_sum(int x) {
+  x += (int)dpp_u32<0x101>((uint32_t)x);
+  x += (int)dpp_u32<0x102>((uint32_t)x);
+  x += (int)dpp_u32<0x104>((uint32_t)x);
+  x += (int)dpp_u32<0x108>((uint32_t)x);
+  const int r1 = __builtin_amdgcn_readlane(x, 16), r2 = __builtin_amdgcn_readlane(x, 32),
+            r3 = __builtin_amdgcn_readlane(x, 48);
+  const int row = (int)(threadIdx.x & 63) >> 4;
+  return x + (row < 1 ? r1 : 0) + (row < 2 ? r2 : 0) + (row < 3 ? r3 : 0);
+}
+
 template <int PER, int MODE>
 __device__ __forceinline__ void topk_body(const TopkArgs& a, int row, int slice, int n_slices) {
   constexpr int NW = kTopkThreads / 64;
   constexpr int NCOPY = 16;
   constexpr int RS = 260;                  // words per copy: 256 bins, rows 16-byte aligned
+  constexpr int kSmallBin = 64;            // a target bin this small is ranked by one wave
   static_assert(PER <= 32, "validity is a 32-bit mask per lane");
   __shared__ __attribute__((aligned(16))) int s_h[2][NCOPY][RS];
   __shared__ uint32_t s_and[NW], s_or[NW];
   __shared__ int s_gt[NW], s_eq[NW];
   __shared__ uint32_t s_prefix;
-  __shared__ int s_remaining;
+  __shared__ int s_remaining, s_small, s_nlist;
+  __shared__ uint32_t s_list[kSmallBin];
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const float* Ss = a.S + (size_t)row * a.n;
   int64_t start = 0, len = a.n;
@@ -395,49 +439,59 @@ __device__ __forceinline__ void topk_body(const TopkArgs& a, int row, int slice,
   uint32_t key[PER];
   int32_t idx[KEEP ? PER : 1];
   uint32_t vmask = 0;                                          // bit i: row i holds an entry
-  const int64_t rem = len - base;
-  const int nv = rem <= 0 ? 0 : (int)min<int64_t>(PER, (rem + 63) / 64);
+  // every load is issued (entries past the end re-read the last one, len >= 1
+  // in every mode), so none waits behind a branch
+  const int64_t last = len - 1;
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
+    const int64_t e = base + 64 * i;
+    const bool in = e < len;
+    const int64_t ec = in ? e : last;
     if (MODE == kTopkList) {
-      TopkCand c = 0xFFFFFFFF00000000ull;
-      if (i < nv) c = __hip_atomic_load(&lst[base + 64 * i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      const int32_t j = (int32_t)(c >> 32);
+      const TopkCand c = __hip_atomic_load(&lst[ec], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const int32_t j = in ? (int32_t)(c >> 32) : -1;
       if (KEEP) idx[KEEP ? i : 0] = j;
       key[i] = j >= 0 ? (uint32_t)c : 0u;
       vmask |= (j >= 0 ? 1u : 0u) << i;
     } else {
-      key[i] = i < nv ? ord_key(Ss[start + base + 64 * i]) : 0u;
-      vmask |= (i < nv ? 1u : 0u) << i;
+      const uint32_t kk = ord_key(Ss[start + ec]);
+      key[i] = in ? kk : 0u;
+      vmask |= (in ? 1u : 0u) << i;
     }
   }
   auto valid = [&](int i) { return (vmask >> i) & 1u; };
 
-  // bits shared by every key: a digit made only of such bits puts all keys in
-  // one bin, so its pass is skipped (chunk scores share sign and most exponent bits)
+  // bits shared by every key need no pass: the digits start at the highest
+  // bit that differs between keys (chunk scores share sign and most exponent
+  // bits), and a digit made only of shared bits is skipped
   uint32_t kand = 0xFFFFFFFFu, kor = 0u;
 #pragma unroll
   for (int i = 0; i < PER; ++i)
     if (valid(i)) { kand &= key[i]; kor |= key[i]; }
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    kand &= (uint32_t)__shfl_xor((int)kand, off);
-    kor |= (uint32_t)__shfl_xor((int)kor, off);
-  }
+  kand = wave_and(kand);
+  kor = wave_or(kor);
   if (lane == 0) { s_and[wave] = kand; s_or[wave] = kor; }
   for (int i = t; i < NCOPY * RS; i += kTopkThreads) (&s_h[0][0][0])[i] = 0;
+  if (t == 0) { s_small = 0; s_nlist = 0; }
   __syncthreads();
   kand = 0xFFFFFFFFu;
   kor = 0u;
 #pragma unroll
   for (int w = 0; w < NW; ++w) { kand &= s_and[w]; kor |= s_or[w]; }
-  const uint32_t varying = kand ^ kor;
+  const uint32_t varying = __builtin_amdgcn_readfirstlane(kand ^ kor);
+  kand = __builtin_amdgcn_readfirstlane(kand);
+  const int hb = varying ? 31 - __builtin_clz(varying) : -1;
 
-  uint32_t prefix = 0, mask = 0;
+  // the bits above hb are every key's: the prefix starts with them
+  const uint32_t low = varying ? (2u << hb) - 1u : 0u;
+  uint32_t prefix = kand & ~low, mask = ~low;
   int remaining = k;       // rank (from the top) still to locate among keys matching the prefix
   int cur = 0;
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 24 - 8 * pass;
+  bool small = false;
+  for (int top = hb; top >= 0; top -= 8) {
+    // the last digit may reach below bit 0: it then starts at bit 0 and its
+    // upper bits, already fixed by the prefix, are the same for every key counted
+    const int shift = top >= 7 ? top - 7 : 0;
     if (((varying >> shift) & 255u) == 0u) {      // the same digit everywhere (uniform branch)
       prefix |= kand & (255u << shift);
       mask |= 255u << shift;
@@ -458,22 +512,19 @@ __device__ __forceinline__ void topk_body(const TopkArgs& a, int row, int slice,
         h0 += v.x; h1 += v.y; h2 += v.z; h3 += v.w;
       }
       const int c4 = h0 + h1 + h2 + h3;
-      int incl = c4;
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const int y = __shfl_down(incl, off);
-        if (lane + off < 64) incl += y;
-      }
+      const int incl = wave_suffix_sum(c4);
       const int excl = incl - c4;
       if (excl < remaining && incl >= remaining) {
-        const int h[4] = {h0, h1, h2, h3};
-        int cum = excl, j = 3;
-        for (; j > 0; --j) {
-          if (cum + h[j] >= remaining) break;
-          cum += h[j];
-        }
+        // the bin among the lane's four (highest first) where the rank falls;
+        // cum counts the keys in the bins above it
+        int cum = excl, j, hj;
+        if (cum + h3 >= remaining) { j = 3; hj = h3; }
+        else if ((cum += h3) + h2 >= remaining) { j = 2; hj = h2; }
+        else if ((cum += h2) + h1 >= remaining) { j = 1; hj = h1; }
+        else { cum += h1; j = 0; hj = h0; }
         s_prefix = prefix | ((uint32_t)(4 * lane + j) << shift);
         s_remaining = remaining - cum;
+        s_small = top >= 8 && hj <= kSmallBin;   // more passes to go, few keys left in the bin
       }
     }
     __syncthreads();
@@ -481,26 +532,58 @@ __device__ __forceinline__ void topk_body(const TopkArgs& a, int row, int slice,
     remaining = s_remaining;
     mask |= 255u << shift;
     cur ^= 1;
+    small = s_small;
+    if (small) break;
+  }
+  if (small) {
+    // the keys matching the prefix (at most kSmallBin) go to a list, and one
+    // wave finds the key of rank `remaining` among them by counting, for
+    // each, the keys above and at it
+#pragma unroll
+    for (int i = 0; i < PER; ++i)
+      if (valid(i) && (key[i] & mask) == prefix) {
+        const int p = atomicAdd(&s_nlist, 1);
+        if (p < kSmallBin) s_list[p] = key[i];
+      }
+    __syncthreads();
+    if (wave == 0) {
+      const int m = min(s_nlist, kSmallBin);
+      const uint32_t mine = lane < m ? s_list[lane] : 0u;
+      int gt = 0, ge = 0;
+      for (int j = 0; j < m; ++j) {
+        const uint32_t kj = (uint32_t)__builtin_amdgcn_readlane((int)mine, j);
+        gt += kj > mine;
+        ge += kj >= mine;
+      }
+      if (lane < m && gt < remaining && remaining <= ge) {   // lanes holding that key write alike
+        s_prefix = mine;
+        s_remaining = remaining - gt;
+      }
+    }
+    __syncthreads();
+    prefix = s_prefix;
+    remaining = s_remaining;
   }
   const uint32_t tau = prefix;   // key of the k-th largest score
   // `remaining` entries equal to tau are taken, lowest indices first
 
-  int n_gt = 0, n_eq = 0;
+  int n_gt = 0, n_eq = 0;        // the wave's counts, from ballots (wave-uniform)
 #pragma unroll
-  for (int i = 0; i < PER; ++i)
-    if (valid(i)) { n_gt += key[i] > tau; n_eq += key[i] == tau; }
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    n_gt += __shfl_xor(n_gt, off);
-    n_eq += __shfl_xor(n_eq, off);
+  for (int i = 0; i < PER; ++i) {
+    const bool v = valid(i);
+    n_gt += __popcll(__ballot(v && key[i] > tau));
+    n_eq += __popcll(__ballot(v && key[i] == tau));
   }
   if (lane == 0) { s_gt[wave] = n_gt; s_eq[wave] = n_eq; }
   __syncthreads();
   int pos = 0, eqr = 0;          // entries taken and ties seen in the waves before this one
-  for (int w = 0; w < wave; ++w) {
-    const int e = s_eq[w];
-    pos += s_gt[w] + min(max(remaining - eqr, 0), e);
-    eqr += e;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    if (w < wave) {
+      const int e = s_eq[w];
+      pos += s_gt[w] + min(max(remaining - eqr, 0), e);
+      eqr += e;
+    }
   }
   const uint64_t below = __lanemask_lt();
 #pragma unroll

@@ -268,6 +268,33 @@ def test_retrieve_exact_ties_long_candidate_lists(n_pages, n_keep):
     assert idx.tolist() == want.tolist()
 
 
+@pytest.mark.parametrize("n_pages,n_keep", [(16384, 256), (3000, 700), (30000, 1000)])
+def test_retrieve_small_tie_group_at_kth(n_pages, n_keep):
+    """Distinct pages except 21 equal ones that hold the k-th score: the
+    top-k's last bin is small, so its keys are ranked by one wave instead of
+    more radix passes, and the tie must still go to the lower pages (row
+    paths at 3000 and 30000 pages, slices then candidates at 16384)."""
+    rng = np.random.default_rng(500 + n_pages + n_keep)
+    cs, G = 8, 4
+    kk = synth.f32_to_bf16_bits(rng.standard_normal((n_pages, cs, 128), dtype=np.float32))
+    q_st = synth.f32_to_bf16_bits(rng.standard_normal((G, 128), dtype=np.float32))
+
+    def scores(pages):
+        mn, mx = O.page_bounds(f64(pages.reshape(n_pages * cs, 128)), cs)
+        return O.page_scores(f64(q_st), mn, mx)
+
+    kth_page = np.argsort(-scores(kk), kind="stable")[n_keep - 1]
+    dup = rng.choice(np.setdiff1d(np.arange(n_pages), [kth_page]), 20, replace=False)
+    kk[dup] = kk[kth_page]
+    sc = scores(kk)
+    kth = np.sort(sc)[::-1][n_keep - 1]
+    assert (sc == kth).sum() == 21 and (sc > kth).sum() < n_keep
+    say(f"retrieve small tie group: pages={n_pages} keep={n_keep}")
+    kmin, kmax = ck.page_bounds(to_dev(kk.reshape(1, n_pages * cs, 128)), [0], cs)
+    idx = ck.retrieve_pages(to_dev(q_st), kmin, kmax, [0], 1, n_keep).cpu().numpy()[0]
+    assert idx.tolist() == O.argtopk_ascending(sc, n_keep).tolist()
+
+
 # ---------------------------------------------------- attention recall
 
 def test_recall_of_gpu_selection_and_retrieval_matches_oracle():
