@@ -659,18 +659,20 @@ __global__ void compact_kernel(CompactArgs a) {
   const int sel = blockIdx.y;
   const int h = a.heads[sel];
   const int32_t* ix = a.idx + (size_t)sel * a.b;
+  const int64_t flat = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t row = flat / SEG;
+  const int seg = (int)(flat - row * SEG);
+  // the row's chunk index is read alongside the last one (window rows read
+  // the last one twice), so both loads take one round trip
   const int64_t last = ix[a.b_eff - 1];
+  int64_t c = ix[min(row / a.cs, (int64_t)a.b_eff - 1)];
   const int64_t tail = a.n_keys - (a.n_chunks - 1) * a.cs;        // size of the last chunk
   const int64_t n_sel_tok = (int64_t)a.b_eff * a.cs - ((last == a.n_chunks - 1) ? (a.cs - tail) : 0);
   const int64_t len = n_sel_tok + a.l_obs;
   if (blockIdx.x == 0 && threadIdx.x == 0) a.lens_out[h] = len;
-  const int64_t flat = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t row = flat / SEG;
-  const int seg = (int)(flat - row * SEG);
   if (row >= len) return;
   int64_t src;
   if (row < n_sel_tok) {
-    int64_t c = ix[row / a.cs];
     c = c < 0 ? 0 : (c >= a.n_chunks ? a.n_chunks - 1 : c);      // defensive clamp
     src = c * a.cs + row % a.cs;
     src = src < a.n_keys ? src : a.n_keys - 1;
