@@ -295,6 +295,24 @@ def test_retrieve_small_tie_group_at_kth(n_pages, n_keep):
     assert idx.tolist() == O.argtopk_ascending(sc, n_keep).tolist()
 
 
+@pytest.mark.parametrize("n_pages,n_keep", [(3000, 700), (16384, 256), (30000, 1000), (40000, 700)])
+def test_retrieve_all_pages_equal(n_pages, n_keep):
+    """Every page the same: all scores tie, no key bit differs, so the
+    top-k runs no radix pass and must return the first n_keep pages (one
+    workgroup per row, 4096-score slices, 16384-score slices)."""
+    rng = np.random.default_rng(600 + n_pages)
+    cs, G = 8, 4
+    page = synth.f32_to_bf16_bits(rng.standard_normal((1, cs, 128), dtype=np.float32))
+    kk = np.repeat(page, n_pages, axis=0).reshape(1, n_pages * cs, 128)
+    q_st = synth.f32_to_bf16_bits(rng.standard_normal((G, 128), dtype=np.float32))
+    say(f"retrieve equal pages: pages={n_pages} keep={n_keep}")
+    kmin, kmax = ck.page_bounds(to_dev(kk), [0], cs)
+    idx = ck.retrieve_pages(to_dev(q_st), kmin, kmax, [0], 1, n_keep).cpu().numpy()[0]
+    mn, mx = O.page_bounds(f64(page[0]), cs)
+    sc = np.repeat(O.page_scores(f64(q_st), mn, mx), n_pages)
+    assert idx.tolist() == O.argtopk_ascending(sc, n_keep).tolist() == list(range(n_keep))
+
+
 # ---------------------------------------------------- attention recall
 
 def test_recall_of_gpu_selection_and_retrieval_matches_oracle():
